@@ -1,0 +1,284 @@
+"""Plain fp64 CPU oracle for the Wan-Streamer v0.2 performer unit attention.
+
+TEST INFRASTRUCTURE ONLY.  The test suite, ``__graft_entry__.smoke()`` and the
+benchmark's ``cpu_baseline`` leg are the only code allowed to import this
+package.  The product (``paper_2607_04443_amd`` and its HIP library) never
+imports it, and it never imports the product: the two share no code.  Inputs
+reach both sides as the same bf16 bit patterns from the seeded generators.
+
+What is computed, and where the paper fixes it (Wan-Streamer v0.2):
+  * the performer denoises the next 160 ms unit while conditioned on a K/V
+    cache: the thinker's K/V slice plus the history units committed after each
+    unit (Abstract; Sec. 2.1; Sec. 3, the "Performer" item and the unit-k
+    schedule paragraph);
+  * visibility is block-causal on one shared timeline (Fig. 1 caption): the
+    block is the streaming unit, so a query of unit u sees every cached key of
+    a unit <= u, and the keys of its own unit in both directions;
+  * the long video latent sequence and the short audio latent sequence are two
+    separate query sets (Sec. 3);
+  * the paper states no attention, norm or rotary equations, so the oracle
+    uses the textbook forms (see ``ws_oracle.c``) with these conventions:
+    softmax scale 1/sqrt(D) unless given; RMS-norm over the head dimension
+    per (token, head) with a weight gamma[D], applied before the rotation;
+    rotary pairs (2p, 2p+1), the first 22 pairs driven by t, the next 21 by h
+    and the last 21 by w, base theta = 10000; the thinker's slice is stored
+    as given (it arrives in final form), values are never transformed.
+
+Everything arithmetic runs in double precision in ``libws_oracle.so`` (plain C
+loops).  This module only decodes bf16 bit patterns, selects the keys a mask
+makes visible, and hands contiguous float64 arrays to the C routines.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libws_oracle.so")
+_lib = None
+
+# Segment kinds, in the oracle's own numbering (cond slice, video, audio).
+KIND_COND, KIND_VIDEO, KIND_AUDIO = 0, 1, 2
+MODE_RAW, MODE_NORM_ROPE = 0, 1
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(
+                f"oracle library missing: {_LIB_PATH}; build it with "
+                "`python oracle/build.py` or __graft_entry__.build()")
+        lib = ctypes.CDLL(_LIB_PATH)
+        lib.ws_oracle_bf16_decode.argtypes = [ctypes.c_void_p, ctypes.c_int64, _dp]
+        lib.ws_oracle_rmsnorm.argtypes = [_dp, ctypes.c_int64, ctypes.c_int64, _dp,
+                                          ctypes.c_double, _dp]
+        lib.ws_oracle_rope_angle.argtypes = [ctypes.c_int64, _i32p, _i32p, ctypes.c_double]
+        lib.ws_oracle_rope_angle.restype = ctypes.c_double
+        lib.ws_oracle_rope.argtypes = [_dp, _i32p, ctypes.c_int64, ctypes.c_int64, _i32p,
+                                       ctypes.c_double, _dp]
+        lib.ws_oracle_attention.argtypes = [_dp, _dp, _dp, ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_double,
+                                            _dp, _dp]
+        lib.ws_oracle_lse_merge.argtypes = [_dp, _dp, ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.c_int64, _dp, _dp]
+        _lib = lib
+    return _lib
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _ptr(a, t=_dp):
+    return a.ctypes.data_as(t)
+
+
+# --------------------------------------------------------------------------- #
+# Elementary routines (thin marshalling over the C library)
+# --------------------------------------------------------------------------- #
+def bf16_decode(bits) -> np.ndarray:
+    """bf16 bit patterns (uint16, any shape) -> exact float64 values."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty(b.shape, dtype=np.float64)
+    _load().ws_oracle_bf16_decode(b.ctypes.data, b.size, _ptr(out))
+    return out
+
+
+def rmsnorm(x, gamma, eps) -> np.ndarray:
+    """RMS-normalise each row of x [..., d] and weight it by gamma [d]."""
+    x = _f64(x)
+    d = x.shape[-1]
+    g = _f64(np.broadcast_to(np.asarray(gamma, dtype=np.float64), (d,)))
+    out = np.empty_like(x)
+    _load().ws_oracle_rmsnorm(_ptr(x), x.size // d, d, _ptr(g), float(eps), _ptr(out))
+    return out
+
+
+def rope(x, positions, band_pairs=(22, 21, 21), theta=10000.0) -> np.ndarray:
+    """Rotary positions over (t, h, w); x [n, d], positions int [n, 3]."""
+    x = _f64(x)
+    n, d = x.shape
+    pos = np.ascontiguousarray(positions, dtype=np.int32).reshape(n, 3)
+    bp = np.ascontiguousarray(band_pairs, dtype=np.int32)
+    if 2 * int(bp.sum()) != d:
+        raise ValueError("band pairs must cover the head dimension")
+    out = np.empty_like(x)
+    _load().ws_oracle_rope(_ptr(x), _ptr(pos, _i32p), n, d, _ptr(bp, _i32p), float(theta),
+                           _ptr(out))
+    return out
+
+
+def rope_angle(pair, position, band_pairs=(22, 21, 21), theta=10000.0) -> float:
+    pos = np.ascontiguousarray(position, dtype=np.int32)
+    bp = np.ascontiguousarray(band_pairs, dtype=np.int32)
+    return _load().ws_oracle_rope_angle(int(pair), _ptr(pos, _i32p), _ptr(bp, _i32p),
+                                        float(theta))
+
+
+def attention(q, k, v, scale, visible=None):
+    """Dense attention for one head: q [nq, d], k/v [nk, d] -> (out [nq, d], lse [nq])."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    nq, d = q.shape
+    nk = k.shape[0]
+    out = np.empty((nq, d), dtype=np.float64)
+    lse = np.empty(nq, dtype=np.float64)
+    vis = None
+    if visible is not None:
+        vis = np.ascontiguousarray(visible, dtype=np.uint8).reshape(nq, nk)
+    _load().ws_oracle_attention(_ptr(q), _ptr(k), _ptr(v), nq, nk, d,
+                                None if vis is None else vis.ctypes.data, float(scale),
+                                _ptr(out), _ptr(lse))
+    return out, lse
+
+
+def lse_merge(o_parts, lse_parts):
+    """Merge attention over disjoint key subsets: o_parts [S, nq, d], lse_parts [S, nq]."""
+    o = _f64(o_parts)
+    l = _f64(lse_parts)
+    s, nq, d = o.shape
+    out = np.empty((nq, d), dtype=np.float64)
+    lse = np.empty(nq, dtype=np.float64)
+    _load().ws_oracle_lse_merge(_ptr(o), _ptr(l), s, nq, d, _ptr(out), _ptr(lse))
+    return out, lse
+
+
+# --------------------------------------------------------------------------- #
+# Logical K/V cache: the state that conditions generation, without paging
+# --------------------------------------------------------------------------- #
+@dataclass
+class Segment:
+    unit: int
+    kind: int
+    mode: int
+    k_bits: np.ndarray            # uint16 [n, H, D]
+    v_bits: np.ndarray            # uint16 [n, H, D]
+    positions: np.ndarray | None  # int32 [n, 3] for MODE_NORM_ROPE
+    gamma: np.ndarray | None      # float [D]
+    eps: float
+    committed: bool = False
+
+
+@dataclass
+class OracleCache:
+    """The cache as the paper describes it: an ordered list of K/V segments.
+
+    The thinker's slice is stored as it arrives (Sec. 3: ranks write incoming
+    K/V into their cache).  A generated unit's keys are stored after per-head
+    RMS-norm and rotary positions; values are stored as given.  Rewriting an
+    uncommitted (unit, kind) replaces it in place; committing freezes it as
+    history (Sec. 2.1); eviction drops generated units older than a window.
+    """
+    num_heads: int
+    head_dim: int = 128
+    band_pairs: tuple = (22, 21, 21)
+    theta: float = 10000.0
+    segments: list = field(default_factory=list)
+
+    def _find(self, unit, kind):
+        for i, s in enumerate(self.segments):
+            if s.unit == unit and s.kind == kind:
+                return i
+        return None
+
+    def append(self, unit, kind, k_bits, v_bits, mode, positions=None, gamma=None, eps=1e-6):
+        k_bits = np.asarray(k_bits, dtype=np.uint16)
+        v_bits = np.asarray(v_bits, dtype=np.uint16)
+        seg = Segment(unit, kind, mode, k_bits, v_bits,
+                      None if positions is None else np.asarray(positions, dtype=np.int32),
+                      None if gamma is None else np.asarray(gamma, dtype=np.float64), eps)
+        i = self._find(unit, kind)
+        if i is None:
+            self.segments.append(seg)
+        else:
+            old = self.segments[i]
+            if old.committed:
+                raise ValueError("segment is committed history")
+            if old.k_bits.shape[0] != k_bits.shape[0]:
+                raise ValueError("rewrite must keep the token count")
+            self.segments[i] = seg
+
+    def commit(self, unit):
+        for s in self.segments:
+            if s.unit == unit and s.kind != KIND_COND:
+                s.committed = True
+
+    def evict_before(self, unit):
+        self.segments = [s for s in self.segments if s.kind == KIND_COND or s.unit >= unit]
+
+    def release(self, unit, kind):
+        i = self._find(unit, kind)
+        if i is None:
+            raise KeyError((unit, kind))
+        del self.segments[i]
+
+    def segment_kv(self, seg: Segment, head: int):
+        """Stored (K', V) of one segment for one head, float64 [n, D]."""
+        k = bf16_decode(seg.k_bits[:, head, :])
+        v = bf16_decode(seg.v_bits[:, head, :])
+        if seg.mode == MODE_NORM_ROPE:
+            k = rope(rmsnorm(k, seg.gamma, seg.eps), seg.positions, self.band_pairs, self.theta)
+        return k, v
+
+    def visible_segments(self, q_unit, min_visible_unit, kind_mask):
+        """Block-causal visibility of whole segments for a query set of unit q_unit."""
+        out = []
+        for s in self.segments:
+            if not (kind_mask >> s.kind) & 1:
+                continue
+            if s.unit > q_unit:
+                continue
+            if s.kind != KIND_COND and s.unit < min_visible_unit:
+                continue
+            out.append(s)
+        return out
+
+    def keys_values(self, head, q_unit, min_visible_unit, kind_mask):
+        segs = self.visible_segments(q_unit, min_visible_unit, kind_mask)
+        if not segs:
+            return (np.zeros((0, self.head_dim)), np.zeros((0, self.head_dim)))
+        ks, vs = zip(*(self.segment_kv(s, head) for s in segs))
+        return np.concatenate(ks), np.concatenate(vs)
+
+
+def query_prologue(q_bits_head, mode, positions, gamma, eps, band_pairs=(22, 21, 21),
+                   theta=10000.0):
+    """Q' of one head: decoded, and for MODE_NORM_ROPE RMS-normed then rotated."""
+    q = bf16_decode(q_bits_head)
+    if mode == MODE_NORM_ROPE:
+        q = rope(rmsnorm(q, gamma, eps), positions, band_pairs, theta)
+    return q
+
+
+def unit_attention(cache: OracleCache, q_bits, q_unit, *, mode=MODE_NORM_ROPE, positions=None,
+                   gamma=None, eps=1e-6, scale=None, min_visible_unit=-(2 ** 31),
+                   kind_mask=0b011, heads=None):
+    """Attention of a unit's queries q_bits [n_q, H, D] over the visible cache.
+
+    Returns (out [n_q, len(heads), D], lse [len(heads), n_q]) in float64.
+    """
+    q_bits = np.asarray(q_bits, dtype=np.uint16)
+    n_q, H, D = q_bits.shape
+    heads = list(range(H)) if heads is None else list(heads)
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    if gamma is None:
+        gamma = np.ones(D)
+    out = np.zeros((n_q, len(heads), D))
+    lse = np.full((len(heads), n_q), -np.inf)
+    for hi, h in enumerate(heads):
+        qh = query_prologue(q_bits[:, h, :], mode, positions, gamma, eps, cache.band_pairs,
+                            cache.theta)
+        k, v = cache.keys_values(h, q_unit, min_visible_unit, kind_mask)
+        if k.shape[0] == 0:
+            continue
+        o, l = attention(qh, k, v, scale)
+        out[:, hi, :] = o
+        lse[hi] = l
+    return out, lse
