@@ -1,0 +1,254 @@
+#!/usr/bin/env python3
+"""Benchmark: one streaming unit of the Wan-Streamer v0.2 performer's attention
+path at 640x368 on one MI355X.
+
+A step is one pass of the whole hot path for the next 160 ms unit u, at steady
+state with an 8-unit history window (Wan-Streamer v0.2, Sec. 3 unit schedule;
+Sec. 2.1 history commit):
+  1. the thinker's 256-token conditioning slice is written into the cache
+     (stored as given, in place of the previous unit's slice);
+  2. unit u's 920 video and 4 audio K/V are appended (RMS-norm + rotary on K);
+  3. video attention: 920 queries (norm + rotary fused) over 256 + 9 x 920 =
+     8536 keys;
+  4. audio attention: 4 queries over cond + 9 x (920 + 4) = 8572 keys;
+  5. unit u is committed to history and the unit that left the window evicted.
+All inputs are synthetic N(0,1) bf16 resident in HBM; H = 40 heads of 128.
+
+Prints one JSON line.  `value` is attention TFLOP/s over the whole step
+(video + audio FLOP / step time).  `roofline` is for the video attention
+kernel (the dominant one), timed with HIP events on its stream over the timed
+region.  `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+H, D, GRID, COND, HIST, AUDIO = 40, 128, (23, 40), 256, 8, 4
+LU = GRID[0] * GRID[1]
+PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12   # 2516.6 dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def video_flop(lq, lk):
+    return 4.0 * H * lq * lk * D
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--video-splits", type=int, default=0)
+    ap.add_argument("--audio-splits", type=int, default=0)
+    ap.add_argument("--cold-audio-reps", type=int, default=20)
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(budget_s=12.0):
+    """The fp64 oracle on whole heads of the video attention, as many as fit in
+    about budget_s seconds (a bounded sample), scaled to TFLOP/s."""
+    import numpy as np
+    import oracle
+    from paper_2607_04443_amd import synth
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 2))
+    lk = COND + (HIST + 1) * LU
+    pos_q = synth.video_positions(HIST, GRID)
+    pos_k = np.concatenate([synth.video_positions(u, GRID) for u in range(HIST + 1)])
+    heads, dt = 0, 0.0
+    while heads < H and dt < budget_s:
+        q = synth.normal_bf16(rng, (LU, D))
+        k = synth.normal_bf16(rng, (lk, D))
+        v = synth.normal_bf16(rng, (lk, D))
+        t0 = time.perf_counter()
+        qq = oracle.rope(oracle.rmsnorm(oracle.bf16_decode(q), np.ones(D), 1e-6), pos_q)
+        kk = oracle.bf16_decode(k)
+        kk[COND:] = oracle.rope(oracle.rmsnorm(kk[COND:], np.ones(D), 1e-6), pos_k)
+        oracle.attention(qq, kk, oracle.bf16_decode(v), 1.0 / np.sqrt(D))
+        dt += time.perf_counter() - t0
+        heads += 1
+    flop = video_flop(LU, lk) / H * heads
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{heads} of {H} heads of the video attention ({LU} queries x {lk} keys, "
+                      f"fp64, with those heads' Q/K RMS-norm and rotary): {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2607_04443_amd import _build
+    if not os.path.exists(_build.LIB_PATH):
+        _build.build()
+    from paper_2607_04443_amd import synth, ws
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 2))
+
+    def dev_bf16(shape):
+        return torch.from_numpy(synth.normal_bf16(rng, shape).view(np.int16)).view(
+            torch.bfloat16).to(dev)
+
+    n_steps_total = args.warmup + args.steps
+    max_pages = 4 + (HIST + 2) * 16 + 8
+    cache = ws.Cache(H, max_pages, max_q_tokens=1024)
+    if args.video_splits:
+        cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, args.video_splits)
+    if args.audio_splits:
+        cache.set_option(ws.WS_OPT_AUDIO_KV_SPLITS, args.audio_splits)
+    gamma = torch.ones(D, dtype=torch.float32, device=dev)
+    eps = 1e-6
+
+    # resident inputs: two rotating sets of per-unit tensors, positions per unit
+    sets = [dict(ck=dev_bf16((COND, H, D)), cv=dev_bf16((COND, H, D)), k=dev_bf16((LU, H, D)),
+                 v=dev_bf16((LU, H, D)), ka=dev_bf16((AUDIO, H, D)), va=dev_bf16((AUDIO, H, D)),
+                 q=dev_bf16((LU, H, D)), qa=dev_bf16((AUDIO, H, D))) for _ in range(2)]
+    last_unit = HIST + n_steps_total
+    vpos = [torch.from_numpy(synth.video_positions(u, GRID)).to(dev) for u in range(last_unit + 1)]
+    apos = [torch.from_numpy(synth.audio_positions(u, AUDIO)).to(dev) for u in range(last_unit + 1)]
+    out_v = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
+    out_a = torch.empty((AUDIO, H, D), dtype=torch.bfloat16, device=dev)
+
+    # history: units 0..HIST-1, committed
+    s0 = sets[0]
+    cache.append(0, ws.WS_KIND_COND, s0["ck"], s0["cv"], ws.WS_APPEND_RAW)
+    for u in range(HIST):
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma, eps)
+        cache.commit(u)
+    torch.cuda.synchronize()
+
+    ev = {name: [] for name in ("append", "video", "audio")}
+
+    def step(u, timed):
+        s = sets[u % 2]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if timed else None
+        if timed:
+            e[0].record(stream)
+        cache.append(0, ws.WS_KIND_COND, s["ck"], s["cv"], ws.WS_APPEND_RAW)
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma,
+                     eps)
+        if timed:
+            e[1].record(stream)
+            e[2].record(stream)
+        cache.unit_attention(s["q"], out_v, ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
+                             ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        if timed:
+            e[3].record(stream)
+            e[4].record(stream)
+        cache.audio_attention(s["qa"], out_a,
+                              ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO,
+                                                         ws.WS_KIND_AUDIO)),
+                              ws.WS_APPEND_NORM_ROPE, apos[u], gamma, eps)
+        if timed:
+            e[5].record(stream)
+            ev["append"].append((e[0], e[1]))
+            ev["video"].append((e[2], e[3]))
+            ev["audio"].append((e[4], e[5]))
+        cache.commit(u)
+        cache.evict_before(u - HIST + 1)
+
+    u = HIST
+    for _ in range(args.warmup):
+        step(u, False)
+        u += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(u, True)
+        u += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    def avg_us(name):
+        return 1e3 * sum(a.elapsed_time(b) for a, b in ev[name]) / len(ev[name])
+
+    lk_v = COND + (HIST + 1) * LU
+    lk_a = COND + (HIST + 1) * (LU + AUDIO)
+    fv = video_flop(LU, lk_v)
+    fa = 4.0 * H * AUDIO * lk_a * D
+    t_video, t_audio, t_append = avg_us("video"), avg_us("audio"), avg_us("append")
+    audio_bytes = 2.0 * lk_a * H * D * 2 + 2.0 * AUDIO * H * D * 2
+    append_bytes = 4.0 * (COND + LU + AUDIO) * H * D * 2
+
+    # audio path with cold caches: a 1 GiB scrub between repetitions, events
+    # around the audio call only
+    cold = None
+    if args.cold_audio_reps > 0:
+        scrub = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma,
+                     eps)
+        amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
+        times = []
+        for _ in range(args.cold_audio_reps):
+            scrub.fill_(1.0)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            cache.audio_attention(s["qa"], out_a, amask, ws.WS_APPEND_NORM_ROPE, apos[u], gamma,
+                                  eps)
+            b.record(stream)
+            b.synchronize()
+            times.append(a.elapsed_time(b) * 1e3)
+        times.sort()
+        med = times[len(times) // 2]
+        cold = {"us_median": med, "gbps": audio_bytes / (med * 1e-6) / 1e9,
+                "frac_hbm": audio_bytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBS, "keys": lk_a}
+        del scrub
+
+    achieved = fv / (t_video * 1e-6) / 1e12
+    result = {
+        "metric": "unit-attention TFLOP/s + us per 160ms unit at 640x368; audio-path HBM GB/s",
+        "value": (fv + fa) / (ms_per_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "v0.2 streaming unit at 640x368 with an 8-unit history window: "
+                               f"H={H}, D={D}; video Q={LU} over {lk_v} keys; audio Q={AUDIO} "
+                               f"over {lk_a} keys; cond slice {COND}; 64-token pages",
+                   "global_batch": 1, "seq_len": lk_v, "parallelism": "single GPU"},
+        "us_per_unit": ms_per_step * 1e3,
+        "video_attention": {"us": t_video, "tflops": achieved, "flop": fv},
+        "audio_attention": {"us_warm": t_audio, "gbps_warm": audio_bytes / (t_audio * 1e-6) / 1e9,
+                            "bytes": audio_bytes, "cold": cold},
+        "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+        "cpu_baseline": None,
+    }
+    cache.close()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,223 @@
+/*
+ * ws.h -- C ABI of the Wan-Streamer v0.2 performer unit-attention library
+ * (libws.so, HIP on MI355X / gfx950).
+ *
+ * The library owns one paged K/V cache per ws_cache handle and runs the
+ * performer's per-denoising-step attention of the next streaming unit over it
+ * (Wan-Streamer v0.2, arXiv 2607.04443):
+ *   - each performer rank writes incoming K/V into a pre-allocated local cache
+ *     (Abstract; Sec. 3, "Performer" item and the unit-k schedule paragraph);
+ *   - generated latents are committed into history after every unit
+ *     (Sec. 2.1); the full-history cache is updated per unit (Sec. 3);
+ *   - attention is block-causal on one timeline, the block being the 160 ms
+ *     unit (Fig. 1 caption; Sec. 1);
+ *   - the long video latent sequence and the short, unsharded audio latent
+ *     sequence are separate query sets (Sec. 3).
+ * On one GPU the cache holds every head (no sequence sharding, no collectives).
+ *
+ * Numeric conventions (the paper states none): bf16 storage, fp32
+ * accumulation; head_dim 128; 64-token pages; per-head RMS-norm over the head
+ * dimension, eps and weight gamma[128] given by the caller, applied before
+ * rotary positions; rotary pairs (2p, 2p+1) with the first rope_pairs[0]
+ * pairs driven by t, the next rope_pairs[1] by h and the rest by w, pair p_b
+ * of a band of n_b pairs turning by pos * theta^(-p_b / n_b); softmax scale
+ * 1/sqrt(head_dim) unless given.
+ *
+ * Conventions common to every call:
+ *   - Pointers named "device" are HIP device pointers (e.g. from torch
+ *     tensors); the caller owns them and keeps them alive until the work
+ *     enqueued on the given stream has completed.
+ *   - Tensors are bf16 with element strides given in elements; the innermost
+ *     (head_dim) stride is 1.  Pointers must be 16-byte aligned and strides
+ *     multiples of 8 elements.
+ *   - Calls that take a hip_stream (a hipStream_t; NULL = the null stream)
+ *     enqueue work and return without waiting.  Host-side validation happens
+ *     before anything is enqueued; a call that fails validation changes no
+ *     state.  After a failed launch the call returns WS_ERR_HIP.
+ *   - ws_last_error() returns a thread-local message for the last non-OK
+ *     status of the calling thread.
+ *   - One ws_cache is used from one host thread at a time.  Calls on one
+ *     cache must be issued on one stream (or be ordered by the caller).
+ *   - The attention calls allocate nothing: pools, page tables and split-KV
+ *     workspaces are allocated by ws_cache_create.
+ */
+#ifndef WS_H_
+#define WS_H_
+
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define WS_API __attribute__((visibility("default")))
+#else
+#define WS_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ws_cache ws_cache; /* opaque; owned by the library */
+
+typedef enum ws_status {
+  WS_OK = 0,
+  WS_ERR_INVALID_ARG = 1,   /* null pointer, bad enum, misaligned pointer or stride */
+  WS_ERR_SHAPE = 2,         /* sizes outside the supported range, token count mismatch */
+  WS_ERR_OUT_OF_PAGES = 3,  /* the page pool cannot hold the new segment */
+  WS_ERR_UNKNOWN_UNIT = 4,  /* no segment for the named (unit, kind) */
+  WS_ERR_COMMITTED = 5,     /* rewrite of a segment already committed to history */
+  WS_ERR_UNSUPPORTED = 6,   /* head_dim != 128, page_tokens != 64, ... */
+  WS_ERR_HIP = 7            /* a HIP runtime call or kernel launch failed */
+} ws_status;
+
+/* Segment kinds: the thinker's conditioning slice, and a unit's generated
+ * video or audio latents. */
+typedef enum ws_kind { WS_KIND_COND = 0, WS_KIND_VIDEO = 1, WS_KIND_AUDIO = 2 } ws_kind;
+#define WS_KIND_BIT(kind) (1u << (unsigned)(kind))
+
+/* RAW: keys stored as given (the thinker's slice arrives in final form).
+ * NORM_ROPE: keys RMS-normed per head, weighted by gamma, then rotated. */
+typedef enum ws_append_mode { WS_APPEND_RAW = 0, WS_APPEND_NORM_ROPE = 1 } ws_append_mode;
+
+typedef struct ws_cache_config {
+  int32_t num_heads;       /* H >= 1 */
+  int32_t head_dim;        /* must be 128 */
+  int32_t page_tokens;     /* must be 64 */
+  int32_t max_pages;       /* pool capacity; each page holds 64 tokens of every head */
+  int32_t max_q_tokens;    /* largest n_q accepted by the attention calls (>= 1) */
+  int32_t rope_max_pos[3]; /* exclusive bounds of the t, h, w positions (each >= 1) */
+  int32_t rope_pairs[3];   /* rotary pairs per band t, h, w; must sum to head_dim / 2 */
+  double rope_theta;       /* rotary base (> 1), e.g. 10000 */
+} ws_cache_config;
+
+typedef struct ws_append_desc {
+  int32_t unit;              /* streaming unit the tokens belong to */
+  ws_kind kind;
+  int32_t n_tokens;          /* >= 1; a rewrite must repeat the first append's count */
+  ws_append_mode mode;
+  const int32_t* positions;  /* device int32 [n_tokens][3] (t, h, w); NORM_ROPE only */
+  const float* gamma;        /* device fp32 [head_dim]; NORM_ROPE only */
+  float eps;                 /* RMS-norm epsilon (>= 0); NORM_ROPE only */
+} ws_append_desc;
+
+typedef struct ws_query_desc {
+  ws_append_mode mode;       /* NORM_ROPE: RMS-norm + rotary on Q; RAW: Q used as given */
+  const int32_t* positions;  /* device int32 [n_q][3]; NORM_ROPE only */
+  const float* gamma;        /* device fp32 [head_dim]; NORM_ROPE only */
+  float eps;
+  float softmax_scale;       /* logit scale; 0 selects 1/sqrt(head_dim) */
+} ws_query_desc;
+
+/* Block-causal visibility for a query set that belongs to unit q_unit.  A
+ * segment (unit u, kind k) is visible iff bit k of kind_mask is set, u <= q_unit,
+ * and, for VIDEO and AUDIO segments, u >= min_visible_unit (history window;
+ * INT32_MIN for no window).  Within a unit keys are visible in both
+ * directions.  A query with no visible key gets a zero output. */
+typedef struct ws_mask_spec {
+  int32_t q_unit;
+  int32_t min_visible_unit;
+  uint32_t kind_mask;        /* OR of WS_KIND_BIT(...) */
+} ws_mask_spec;
+
+typedef struct ws_cache_stats {
+  int32_t pages_total;
+  int32_t pages_free;
+  int32_t n_segments;
+  int32_t reserved;
+} ws_cache_stats;
+
+/* Tuning knobs (0 = automatic choice).  They change scheduling only, never
+ * results beyond floating-point summation order. */
+typedef enum ws_option {
+  WS_OPT_VIDEO_KV_SPLITS = 0,  /* key-range splits of the video kernel (1..8) */
+  WS_OPT_AUDIO_KV_SPLITS = 1   /* key-range splits of the audio kernel (1..512) */
+} ws_option;
+
+/* Creates a cache: allocates the K and V page pools (2 * max_pages * H * 64 *
+ * 128 * 2 bytes), the rotary cos/sin tables (built in double precision on the
+ * host, stored as fp32), page-list arenas and split-KV workspaces, and clears
+ * the pools to zero.  Uses the current HIP device.  Synchronous.
+ * On success *out owns all of it until ws_cache_destroy. */
+WS_API ws_status ws_cache_create(const ws_cache_config* cfg, ws_cache** out);
+
+/* Waits for the device, then frees everything the cache owns.  NULL is a no-op. */
+WS_API ws_status ws_cache_destroy(ws_cache* cache);
+
+/* Drops every segment and returns all pages to the pool (host-side only;
+ * the pool contents are left as they are). */
+WS_API ws_status ws_cache_reset(ws_cache* cache);
+
+/* Writes n_tokens K/V of one (unit, kind) into the cache: a thinker slice
+ * (Sec. 3: ranks write incoming K/V into their cache) or a generated unit's
+ * K/V at a denoising step.  The first append of a (unit, kind) takes fresh
+ * pages (WS_ERR_OUT_OF_PAGES if the pool is short); a later append of the same
+ * uncommitted (unit, kind) rewrites its slots in place (same n_tokens, else
+ * WS_ERR_SHAPE; WS_ERR_COMMITTED after ws_unit_commit).
+ *   k, v: device bf16, element (t, h, d) at [t * tok_stride + h * head_stride + d],
+ *         t < n_tokens, h < num_heads, d < 128.
+ * NORM_ROPE keys: K' = RoPE(RMSNorm(K) * gamma, positions), computed in fp32,
+ * rounded to bf16.  Values are always stored as given.  Positions outside
+ * [0, rope_max_pos) are clamped and flagged (ws_cache_check). */
+WS_API ws_status ws_kv_append(ws_cache* cache, const void* k, const void* v, int64_t tok_stride,
+                       int64_t head_stride, const ws_append_desc* desc, void* hip_stream);
+
+/* Marks the VIDEO and AUDIO segments of `unit` as committed history
+ * (Sec. 2.1); they can no longer be rewritten.  Host-only. */
+WS_API ws_status ws_unit_commit(ws_cache* cache, int32_t unit);
+
+/* Frees the VIDEO and AUDIO segments of every unit < `unit` (history window
+ * advance).  Conditioning slices are kept.  Host-only; the caller must not
+ * have work in flight that still reads those pages. */
+WS_API ws_status ws_kv_evict_before(ws_cache* cache, int32_t unit);
+
+/* Frees one (unit, kind) segment (e.g. a superseded conditioning slice).
+ * Host-only, with the same in-flight caveat. */
+WS_API ws_status ws_kv_release(ws_cache* cache, int32_t unit, ws_kind kind);
+
+/* The performer's attention of a unit's video latent queries over the
+ * visible cache (Sec. 3, the expensive latent-generation path):
+ *   Q' = RoPE(RMSNorm(Q) * gamma, positions) (or Q for RAW),
+ *   out[i] = sum_j softmax_j(scale * <Q'_i, K'_j>) V_j over the visible keys.
+ *   q:   device bf16 [n_q][H][128] with strides (q_tok_stride, q_head_stride).
+ *   out: device bf16 [n_q][H][128] with strides (out_tok_stride, out_head_stride).
+ * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 128-query tiles, 64-key pages. */
+WS_API ws_status ws_unit_attention(const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+                            int32_t n_q, const ws_query_desc* qdesc, ws_cache* cache,
+                            const ws_mask_spec* mask, void* out, int64_t out_tok_stride,
+                            int64_t out_head_stride, void* hip_stream);
+
+/* The same attention for the few audio latent queries of a unit (Sec. 3:
+ * short, unsharded).  Memory-bound split-KV kernel: fp32 partials over key
+ * ranges, merged by log-sum-exp.  Arguments as ws_unit_attention;
+ * 1 <= n_q <= min(max_q_tokens, 64). */
+WS_API ws_status ws_audio_attention(const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+                             int32_t n_q, const ws_query_desc* qdesc, ws_cache* cache,
+                             const ws_mask_spec* mask, void* out, int64_t out_tok_stride,
+                             int64_t out_head_stride, void* hip_stream);
+
+/* Debug read-back of one segment in logical order: k_host and v_host receive
+ * bf16 [n_tokens][H][128] (contiguous host buffers owned by the caller).
+ * Waits for the device.  k_host or v_host may be NULL to skip it. */
+WS_API ws_status ws_cache_export(ws_cache* cache, int32_t unit, ws_kind kind, void* k_host,
+                          void* v_host);
+
+/* Token count of a segment (WS_ERR_UNKNOWN_UNIT if absent). */
+WS_API ws_status ws_segment_tokens(ws_cache* cache, int32_t unit, ws_kind kind, int32_t* n_tokens);
+
+/* Page-pool occupancy.  Host-only. */
+WS_API ws_status ws_cache_info(ws_cache* cache, ws_cache_stats* stats);
+
+/* Waits for the device and returns (and clears) the device-side flags:
+ * bit 0 = a position outside [0, rope_max_pos) was clamped. */
+WS_API ws_status ws_cache_check(ws_cache* cache, uint32_t* flags);
+
+/* Sets a tuning knob (see ws_option); value 0 restores the automatic choice. */
+WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t value);
+
+/* Thread-local message for the last non-OK status ("" if none). */
+WS_API const char* ws_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WS_H_ */

@@ -68,8 +68,14 @@ def _load():
                                             _dp, _dp]
         lib.ws_oracle_lse_merge.argtypes = [_dp, _dp, ctypes.c_int64, ctypes.c_int64,
                                             ctypes.c_int64, _dp, _dp]
+        lib.ws_oracle_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's attention loop runs on."""
+    return int(_load().ws_oracle_num_threads())
 
 
 def _f64(a):

@@ -24,10 +24,14 @@
  * forms, invariants and library routines (see tests/test_oracle_*.py).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <string.h>
 
 #define WS_ORACLE_API __attribute__((visibility("default")))
+
+/* Threads the parallel loops below run on (for reporting CPU timings). */
+WS_ORACLE_API int ws_oracle_num_threads(void) { return omp_get_max_threads(); }
 
 /* bf16 is the upper half of an IEEE binary32; widening is exact. */
 WS_ORACLE_API void ws_oracle_bf16_decode(const uint16_t* src, int64_t n, double* dst) {

@@ -1,0 +1,576 @@
+// C ABI of the performer unit-attention library (declared in include/ws.h).
+//
+// Host responsibilities: argument validation (before anything is enqueued),
+// the page table, the visible-page lists (uploaded once per change of the
+// cache structure and reused by every denoising step in between), the choice
+// of key-range splits, and the kernel launches.  Nothing here computes
+// attention: every arithmetic step runs in kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "pagetable.hpp"
+#include "ws.h"
+#include "ws_kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ws_status fail(ws_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+ws_status hip_fail(hipError_t e, const char* what) {
+  return fail(WS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define WS_HIP(call)                                  \
+  do {                                                \
+    hipError_t e_ = (call);                           \
+    if (e_ != hipSuccess) return hip_fail(e_, #call); \
+  } while (0)
+
+constexpr int kMaxVideoSplits = 8;
+constexpr int kMaxAudioSplits = 512;
+constexpr int kMaxAudioQ = 64;
+
+struct ListCacheEntry {
+  bool valid = false;
+  ws::MaskSpec mask{};
+  uint64_t version = 0;
+  size_t offset = 0;
+  int32_t n = 0;
+};
+
+}  // namespace
+
+struct ws_cache {
+  ws_cache_config cfg{};
+  int device = 0;
+  int num_cus = 256;
+  ws::PageTable pt;
+  uint16_t* kpool = nullptr;
+  uint16_t* vpool = nullptr;
+  float2* rope_dev = nullptr;
+  ws::RopeTables rope{};
+  uint32_t* flags_dev = nullptr;
+  int2* arena_dev = nullptr;
+  int2* arena_host = nullptr;  // pinned
+  size_t arena_cap = 0;
+  size_t arena_used = 0;
+  ListCacheEntry lists[4];
+  int list_next = 0;
+  float* part_o = nullptr;
+  float* part_lse = nullptr;
+  int64_t part_rows = 0;  // capacity in (split, head, query) rows
+  int32_t opt_video_splits = 0;
+  int32_t opt_audio_splits = 0;
+  std::vector<ws::PageRef> scratch_list;
+
+  ws_cache(int32_t page_tokens, int32_t max_pages) : pt(page_tokens, max_pages) {}
+};
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+ws_status check_device(const ws_cache* c) {
+  int dev = -1;
+  WS_HIP(hipGetDevice(&dev));
+  if (dev != c->device)
+    return fail(WS_ERR_INVALID_ARG, "cache lives on device %d but device %d is current", c->device,
+                dev);
+  return WS_OK;
+}
+
+ws_status check_kind(int kind) {
+  if (kind < WS_KIND_COND || kind > WS_KIND_AUDIO) return fail(WS_ERR_INVALID_ARG, "bad kind %d", kind);
+  return WS_OK;
+}
+
+ws_status check_strides(const char* what, const void* p, int64_t tok_stride, int64_t head_stride,
+                        int32_t n_tok, int32_t n_heads) {
+  if (!p) return fail(WS_ERR_INVALID_ARG, "%s is NULL", what);
+  if (!aligned16(p)) return fail(WS_ERR_INVALID_ARG, "%s is not 16-byte aligned", what);
+  if (tok_stride < 0 || head_stride < 0 || tok_stride % 8 || head_stride % 8)
+    return fail(WS_ERR_INVALID_ARG, "%s strides must be non-negative multiples of 8 elements", what);
+  if (n_tok > 1 && tok_stride < ws::kHeadDim)
+    return fail(WS_ERR_INVALID_ARG, "%s token stride %lld overlaps a head row", what,
+                static_cast<long long>(tok_stride));
+  if (n_heads > 1 && head_stride < ws::kHeadDim)
+    return fail(WS_ERR_INVALID_ARG, "%s head stride %lld overlaps a head row", what,
+                static_cast<long long>(head_stride));
+  // the kernels index with 32-bit token offsets times a 64-bit stride
+  const long double span = static_cast<long double>(tok_stride) * n_tok +
+                           static_cast<long double>(head_stride) * n_heads;
+  if (span > 9.0e18L) return fail(WS_ERR_INVALID_ARG, "%s strides overflow", what);
+  return WS_OK;
+}
+
+// Uploads a page list into the device arena (async, on `stream`) and returns
+// its element offset.  A full arena wraps after waiting for the device.
+ws_status upload_list(ws_cache* c, const std::vector<ws::PageRef>& list, hipStream_t stream,
+                      size_t* offset) {
+  const size_t n = std::max<size_t>(list.size(), 1);
+  if (n > c->arena_cap) return fail(WS_ERR_SHAPE, "page list of %zu entries exceeds arena", n);
+  if (c->arena_used + n > c->arena_cap) {
+    WS_HIP(hipDeviceSynchronize());
+    c->arena_used = 0;
+    for (auto& e : c->lists) e.valid = false;
+  }
+  const size_t off = c->arena_used;
+  for (size_t i = 0; i < list.size(); ++i)
+    c->arena_host[off + i] = make_int2(list[i].page, list[i].n_valid);
+  if (list.empty()) c->arena_host[off] = make_int2(0, 0);
+  WS_HIP(hipMemcpyAsync(c->arena_dev + off, c->arena_host + off, n * sizeof(int2),
+                        hipMemcpyHostToDevice, stream));
+  c->arena_used += (n + 63) & ~size_t(63);
+  if (c->arena_used > c->arena_cap) c->arena_used = c->arena_cap;
+  *offset = off;
+  return WS_OK;
+}
+
+ws_status visible_list(ws_cache* c, const ws_mask_spec* m, hipStream_t stream, const int2** dev,
+                       int32_t* n) {
+  const ws::MaskSpec mask{m->q_unit, m->min_visible_unit, m->kind_mask};
+  const uint64_t ver = c->pt.version();
+  for (auto& e : c->lists) {
+    if (e.valid && e.version == ver && e.mask.q_unit == mask.q_unit &&
+        e.mask.min_visible_unit == mask.min_visible_unit && e.mask.kind_mask == mask.kind_mask) {
+      *dev = c->arena_dev + e.offset;
+      *n = e.n;
+      return WS_OK;
+    }
+  }
+  c->pt.visible_pages(mask, &c->scratch_list);
+  size_t off = 0;
+  ws_status st = upload_list(c, c->scratch_list, stream, &off);
+  if (st != WS_OK) return st;
+  ListCacheEntry& e = c->lists[c->list_next];
+  c->list_next = (c->list_next + 1) % 4;
+  e.valid = true;
+  e.mask = mask;
+  e.version = ver;
+  e.offset = off;
+  e.n = static_cast<int32_t>(c->scratch_list.size());
+  *dev = c->arena_dev + off;
+  *n = e.n;
+  return WS_OK;
+}
+
+ws_status fill_rope(ws_cache* c) {
+  const ws_cache_config& g = c->cfg;
+  size_t total = 0;
+  for (int b = 0; b < 3; ++b) total += static_cast<size_t>(g.rope_max_pos[b]) * g.rope_pairs[b];
+  std::vector<float2> host(std::max<size_t>(total, 1));
+  size_t off[3];
+  size_t o = 0;
+  for (int b = 0; b < 3; ++b) {
+    off[b] = o;
+    const int np = g.rope_pairs[b];
+    for (int pos = 0; pos < g.rope_max_pos[b]; ++pos)
+      for (int pb = 0; pb < np; ++pb) {
+        // angle in double precision, rounded once to fp32 per cos/sin
+        const double ang = static_cast<double>(pos) *
+                           std::pow(g.rope_theta, -static_cast<double>(pb) / static_cast<double>(np));
+        host[o++] = make_float2(static_cast<float>(std::cos(ang)), static_cast<float>(std::sin(ang)));
+      }
+  }
+  WS_HIP(hipMalloc(&c->rope_dev, host.size() * sizeof(float2)));
+  WS_HIP(hipMemcpy(c->rope_dev, host.data(), host.size() * sizeof(float2), hipMemcpyHostToDevice));
+  for (int b = 0; b < 3; ++b) {
+    c->rope.tab[b] = c->rope_dev + off[b];
+    c->rope.max_pos[b] = g.rope_max_pos[b];
+    c->rope.pairs[b] = g.rope_pairs[b];
+  }
+  return WS_OK;
+}
+
+void free_all(ws_cache* c) {
+  if (c->kpool) (void)hipFree(c->kpool);
+  if (c->vpool) (void)hipFree(c->vpool);
+  if (c->rope_dev) (void)hipFree(c->rope_dev);
+  if (c->flags_dev) (void)hipFree(c->flags_dev);
+  if (c->arena_dev) (void)hipFree(c->arena_dev);
+  if (c->arena_host) (void)hipHostFree(c->arena_host);
+  if (c->part_o) (void)hipFree(c->part_o);
+  if (c->part_lse) (void)hipFree(c->part_lse);
+  c->kpool = c->vpool = nullptr;
+  c->rope_dev = nullptr;
+  c->flags_dev = nullptr;
+  c->arena_dev = c->arena_host = nullptr;
+  c->part_o = c->part_lse = nullptr;
+}
+
+ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
+  if (!cfg || !out) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  *out = nullptr;
+  if (cfg->head_dim != ws::kHeadDim)
+    return fail(WS_ERR_UNSUPPORTED, "head_dim %d unsupported (only 128)", cfg->head_dim);
+  if (cfg->page_tokens != ws::kPageTokens)
+    return fail(WS_ERR_UNSUPPORTED, "page_tokens %d unsupported (only 64)", cfg->page_tokens);
+  if (cfg->num_heads < 1 || cfg->num_heads > 4096)
+    return fail(WS_ERR_SHAPE, "num_heads %d out of range [1, 4096]", cfg->num_heads);
+  if (cfg->max_pages < 1 || cfg->max_q_tokens < 1 || cfg->max_q_tokens > (1 << 20))
+    return fail(WS_ERR_SHAPE, "max_pages and max_q_tokens must be >= 1 (max_q_tokens <= 2^20)");
+  int pair_sum = 0;
+  for (int b = 0; b < 3; ++b) {
+    if (cfg->rope_max_pos[b] < 1 || cfg->rope_max_pos[b] > (1 << 24))
+      return fail(WS_ERR_SHAPE, "rope_max_pos[%d] = %d out of range", b, cfg->rope_max_pos[b]);
+    if (cfg->rope_pairs[b] < 0) return fail(WS_ERR_SHAPE, "rope_pairs[%d] negative", b);
+    pair_sum += cfg->rope_pairs[b];
+  }
+  if (pair_sum != ws::kHeadDim / 2)
+    return fail(WS_ERR_SHAPE, "rope_pairs sum to %d, need %d", pair_sum, ws::kHeadDim / 2);
+  if (!(cfg->rope_theta > 1.0) || !std::isfinite(cfg->rope_theta))
+    return fail(WS_ERR_INVALID_ARG, "rope_theta must be a finite value > 1");
+
+  ws_cache* c = new ws_cache(cfg->page_tokens, cfg->max_pages);
+  c->cfg = *cfg;
+  auto bail = [&](ws_status st) {
+    free_all(c);
+    delete c;
+    return st;
+  };
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) return bail(hip_fail(e, "hipGetDevice"));
+  e = hipDeviceGetAttribute(&c->num_cus, hipDeviceAttributeMultiprocessorCount, c->device);
+  if (e != hipSuccess) return bail(hip_fail(e, "hipDeviceGetAttribute"));
+
+  const size_t pool_elems =
+      static_cast<size_t>(cfg->max_pages) * cfg->num_heads * static_cast<size_t>(ws::kPageHeadElems);
+  if ((e = hipMalloc(&c->kpool, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMalloc(K pool)"));
+  if ((e = hipMalloc(&c->vpool, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMalloc(V pool)"));
+  if ((e = hipMemset(c->kpool, 0, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
+  if ((e = hipMemset(c->vpool, 0, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
+  if (ws_status st = fill_rope(c); st != WS_OK) return bail(st);
+  if ((e = hipMalloc(&c->flags_dev, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMalloc"));
+  if ((e = hipMemset(c->flags_dev, 0, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
+  c->arena_cap = std::max<size_t>(65536, 16 * static_cast<size_t>(cfg->max_pages));
+  if ((e = hipMalloc(&c->arena_dev, c->arena_cap * sizeof(int2))) != hipSuccess)
+    return bail(hip_fail(e, "hipMalloc(arena)"));
+  if ((e = hipHostMalloc(reinterpret_cast<void**>(&c->arena_host), c->arena_cap * sizeof(int2),
+                         hipHostMallocDefault)) != hipSuccess)
+    return bail(hip_fail(e, "hipHostMalloc(arena)"));
+  c->part_rows = static_cast<int64_t>(kMaxVideoSplits) * cfg->num_heads *
+                 std::max<int64_t>(cfg->max_q_tokens, kMaxAudioQ);
+  if ((e = hipMalloc(&c->part_o, static_cast<size_t>(c->part_rows) * ws::kHeadDim * sizeof(float))) != hipSuccess)
+    return bail(hip_fail(e, "hipMalloc(partials)"));
+  if ((e = hipMalloc(&c->part_lse, static_cast<size_t>(c->part_rows) * sizeof(float))) != hipSuccess)
+    return bail(hip_fail(e, "hipMalloc(partials)"));
+  *out = c;
+  return WS_OK;
+}
+
+int choose_video_splits(const ws_cache* c, int n_items, int n_pages) {
+  if (c->opt_video_splits > 0) return c->opt_video_splits;
+  // aim at two resident workgroups per CU, without splits shorter than 4 pages
+  int s = 1;
+  while (s < kMaxVideoSplits && static_cast<int64_t>(n_items) * s < 2LL * c->num_cus &&
+         n_pages >= 4 * (s + 1))
+    ++s;
+  return s;
+}
+
+int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
+  if (c->opt_audio_splits > 0) return c->opt_audio_splits;
+  // enough independent waves to keep HBM busy: ~8 per CU, >= 2 pages per wave
+  const int target = (8 * c->num_cus + n_items - 1) / n_items;
+  return std::max(1, std::min({target, std::max(1, n_pages / 2), kMaxAudioSplits}));
+}
+
+ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+                         int32_t n_q, const ws_query_desc* qd, ws_cache* c, const ws_mask_spec* m,
+                         void* out, int64_t out_tok_stride, int64_t out_head_stride,
+                         void* hip_stream) {
+  if (!c || !qd || !m) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (ws_status st = check_device(c); st != WS_OK) return st;
+  const int H = c->cfg.num_heads;
+  const int max_q = audio ? std::min(c->cfg.max_q_tokens, kMaxAudioQ) : c->cfg.max_q_tokens;
+  if (n_q < 1 || n_q > max_q) return fail(WS_ERR_SHAPE, "n_q %d out of range [1, %d]", n_q, max_q);
+  if (ws_status st = check_strides("q", q, q_tok_stride, q_head_stride, n_q, H); st != WS_OK) return st;
+  if (ws_status st = check_strides("out", out, out_tok_stride, out_head_stride, n_q, H); st != WS_OK)
+    return st;
+  if (qd->mode != WS_APPEND_RAW && qd->mode != WS_APPEND_NORM_ROPE)
+    return fail(WS_ERR_INVALID_ARG, "bad query mode %d", static_cast<int>(qd->mode));
+  if (qd->mode == WS_APPEND_NORM_ROPE) {
+    if (!qd->positions || !qd->gamma) return fail(WS_ERR_INVALID_ARG, "NORM_ROPE needs positions and gamma");
+    if (!aligned16(qd->gamma)) return fail(WS_ERR_INVALID_ARG, "gamma is not 16-byte aligned");
+    if (!(qd->eps >= 0.f) || !std::isfinite(qd->eps)) return fail(WS_ERR_INVALID_ARG, "bad eps");
+  }
+  if (!std::isfinite(qd->softmax_scale) || qd->softmax_scale < 0.f)
+    return fail(WS_ERR_INVALID_ARG, "bad softmax_scale");
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+
+  const int2* plist = nullptr;
+  int32_t n_pages = 0;
+  if (ws_status st = visible_list(c, m, stream, &plist, &n_pages); st != WS_OK) return st;
+
+  ws::AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_tok_stride = q_tok_stride;
+  a.q_head_stride = q_head_stride;
+  a.n_q = n_q;
+  a.num_heads = H;
+  a.mode = static_cast<int32_t>(qd->mode);
+  a.positions = qd->positions;
+  a.gamma = qd->gamma;
+  a.eps = qd->eps;
+  const float scale = qd->softmax_scale > 0.f ? qd->softmax_scale
+                                              : static_cast<float>(1.0 / std::sqrt(double(ws::kHeadDim)));
+  a.scale_log2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  a.rope = c->rope;
+  a.kpool = c->kpool;
+  a.vpool = c->vpool;
+  a.pages = plist;
+  a.n_pages = n_pages;
+  a.out = static_cast<uint16_t*>(out);
+  a.out_tok_stride = out_tok_stride;
+  a.out_head_stride = out_head_stride;
+  a.part_o = c->part_o;
+  a.part_lse = c->part_lse;
+  a.flags = c->flags_dev;
+  const int qtile = audio ? ws::kAudioQTile : ws::kVideoQTile;
+  a.n_qtiles = (n_q + qtile - 1) / qtile;
+  const int n_items = a.n_qtiles * H;
+  int splits = audio ? choose_audio_splits(c, n_items, n_pages) : choose_video_splits(c, n_items, n_pages);
+  splits = std::max(1, std::min(splits, std::max(1, n_pages)));
+  const int64_t cap = c->part_rows / (static_cast<int64_t>(H) * n_q);
+  splits = static_cast<int>(std::min<int64_t>(splits, std::max<int64_t>(cap, 1)));
+  const int pps = n_pages > 0 ? (n_pages + splits - 1) / splits : 0;
+  splits = pps > 0 ? (n_pages + pps - 1) / pps : 1;  // no empty splits
+  if (audio && cap < splits) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
+  a.n_splits = splits;
+  a.pages_per_split = pps;
+
+  hipError_t e = audio ? ws::launch_audio_attention(a, stream) : ws::launch_unit_attention(a, stream);
+  if (e != hipSuccess) return hip_fail(e, audio ? "audio_attn launch" : "unit_attn launch");
+  if (audio || splits > 1) {
+    ws::CombineArgs cb{};
+    cb.part_o = c->part_o;
+    cb.part_lse = c->part_lse;
+    cb.n_splits = splits;
+    cb.n_q = n_q;
+    cb.num_heads = H;
+    cb.out = a.out;
+    cb.out_tok_stride = out_tok_stride;
+    cb.out_head_stride = out_head_stride;
+    e = ws::launch_combine(cb, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine launch");
+  }
+  return WS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ws_status ws_cache_create(const ws_cache_config* cfg, ws_cache** out) {
+  try {
+    return create_impl(cfg, out);
+  } catch (...) {
+    return fail(WS_ERR_INVALID_ARG, "host allocation failed");
+  }
+}
+
+ws_status ws_cache_destroy(ws_cache* cache) {
+  if (!cache) return WS_OK;
+  hipError_t e = hipDeviceSynchronize();
+  free_all(cache);
+  delete cache;
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  return WS_OK;
+}
+
+ws_status ws_cache_reset(ws_cache* cache) {
+  if (!cache) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  cache->pt.reset();
+  return WS_OK;
+}
+
+ws_status ws_kv_append(ws_cache* c, const void* k, const void* v, int64_t tok_stride,
+                       int64_t head_stride, const ws_append_desc* d, void* hip_stream) {
+  if (!c || !d) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (ws_status st = check_device(c); st != WS_OK) return st;
+  if (ws_status st = check_kind(d->kind); st != WS_OK) return st;
+  if (d->mode != WS_APPEND_RAW && d->mode != WS_APPEND_NORM_ROPE)
+    return fail(WS_ERR_INVALID_ARG, "bad append mode %d", static_cast<int>(d->mode));
+  if (d->n_tokens < 1) return fail(WS_ERR_SHAPE, "n_tokens must be >= 1");
+  const int H = c->cfg.num_heads;
+  if (ws_status st = check_strides("k", k, tok_stride, head_stride, d->n_tokens, H); st != WS_OK) return st;
+  if (ws_status st = check_strides("v", v, tok_stride, head_stride, d->n_tokens, H); st != WS_OK) return st;
+  if (d->mode == WS_APPEND_NORM_ROPE) {
+    if (!d->positions || !d->gamma) return fail(WS_ERR_INVALID_ARG, "NORM_ROPE needs positions and gamma");
+    if (!aligned16(d->gamma)) return fail(WS_ERR_INVALID_ARG, "gamma is not 16-byte aligned");
+    if (!(d->eps >= 0.f) || !std::isfinite(d->eps)) return fail(WS_ERR_INVALID_ARG, "bad eps");
+  }
+  ws::Segment* seg = nullptr;
+  bool created = false;
+  switch (c->pt.acquire(d->unit, d->kind, d->n_tokens, &seg, &created)) {
+    case ws::PtStatus::ok: break;
+    case ws::PtStatus::out_of_pages:
+      return fail(WS_ERR_OUT_OF_PAGES, "pool has %d free pages, segment needs %d", c->pt.free_pages(),
+                  (d->n_tokens + ws::kPageTokens - 1) / ws::kPageTokens);
+    case ws::PtStatus::committed:
+      return fail(WS_ERR_COMMITTED, "unit %d kind %d is committed history", d->unit, static_cast<int>(d->kind));
+    case ws::PtStatus::shape:
+      return fail(WS_ERR_SHAPE, "rewrite of unit %d kind %d with %d tokens (segment has %d)", d->unit,
+                  static_cast<int>(d->kind), d->n_tokens, seg ? seg->n_tokens : -1);
+    default: return fail(WS_ERR_INVALID_ARG, "page table error");
+  }
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  ws::AppendArgs a{};
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.tok_stride = tok_stride;
+  a.head_stride = head_stride;
+  a.n_tokens = d->n_tokens;
+  a.mode = static_cast<int32_t>(d->mode);
+  a.positions = d->positions;
+  a.gamma = d->gamma;
+  a.eps = d->eps;
+  a.num_heads = H;
+  a.kpool = c->kpool;
+  a.vpool = c->vpool;
+  a.rope = c->rope;
+  a.flags = c->flags_dev;
+  const int n_pages = static_cast<int>(seg->pages.size());
+  for (int p0 = 0; p0 < n_pages; p0 += ws::AppendArgs::kMaxAppendPages) {
+    const int np = std::min(ws::AppendArgs::kMaxAppendPages, n_pages - p0);
+    a.first_page = p0;
+    a.n_pages = np;
+    for (int i = 0; i < np; ++i) a.pages[i] = seg->pages[static_cast<size_t>(p0 + i)];
+    hipError_t e = ws::launch_kv_append(a, stream);
+    if (e != hipSuccess) {
+      if (created && p0 == 0) c->pt.release(d->unit, d->kind);
+      return hip_fail(e, "kv_append launch");
+    }
+  }
+  return WS_OK;
+}
+
+ws_status ws_unit_commit(ws_cache* c, int32_t unit) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  c->pt.commit(unit);
+  return WS_OK;
+}
+
+ws_status ws_kv_evict_before(ws_cache* c, int32_t unit) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  c->pt.evict_before(unit);
+  return WS_OK;
+}
+
+ws_status ws_kv_release(ws_cache* c, int32_t unit, ws_kind kind) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  if (ws_status st = check_kind(kind); st != WS_OK) return st;
+  if (c->pt.release(unit, kind) != ws::PtStatus::ok)
+    return fail(WS_ERR_UNKNOWN_UNIT, "no segment for unit %d kind %d", unit, static_cast<int>(kind));
+  return WS_OK;
+}
+
+ws_status ws_unit_attention(const void* q, int64_t q_tok_stride, int64_t q_head_stride, int32_t n_q,
+                            const ws_query_desc* qdesc, ws_cache* cache, const ws_mask_spec* mask,
+                            void* out, int64_t out_tok_stride, int64_t out_head_stride,
+                            void* hip_stream) {
+  return attention_impl(false, q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
+                        out_tok_stride, out_head_stride, hip_stream);
+}
+
+ws_status ws_audio_attention(const void* q, int64_t q_tok_stride, int64_t q_head_stride, int32_t n_q,
+                             const ws_query_desc* qdesc, ws_cache* cache, const ws_mask_spec* mask,
+                             void* out, int64_t out_tok_stride, int64_t out_head_stride,
+                             void* hip_stream) {
+  return attention_impl(true, q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
+                        out_tok_stride, out_head_stride, hip_stream);
+}
+
+ws_status ws_cache_export(ws_cache* c, int32_t unit, ws_kind kind, void* k_host, void* v_host) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  if (ws_status st = check_device(c); st != WS_OK) return st;
+  if (ws_status st = check_kind(kind); st != WS_OK) return st;
+  const ws::Segment* s = c->pt.find(unit, kind);
+  if (!s) return fail(WS_ERR_UNKNOWN_UNIT, "no segment for unit %d kind %d", unit, static_cast<int>(kind));
+  WS_HIP(hipDeviceSynchronize());
+  const int H = c->cfg.num_heads;
+  const size_t page_elems = static_cast<size_t>(H) * ws::kPageHeadElems;
+  std::vector<uint16_t> kp(page_elems), vp(page_elems);
+  uint16_t* ko = static_cast<uint16_t*>(k_host);
+  uint16_t* vo = static_cast<uint16_t*>(v_host);
+  for (size_t pi = 0; pi < s->pages.size(); ++pi) {
+    const size_t base = static_cast<size_t>(s->pages[pi]) * page_elems;
+    if (ko) WS_HIP(hipMemcpy(kp.data(), c->kpool + base, page_elems * 2, hipMemcpyDeviceToHost));
+    if (vo) WS_HIP(hipMemcpy(vp.data(), c->vpool + base, page_elems * 2, hipMemcpyDeviceToHost));
+    for (int slot = 0; slot < ws::kPageTokens; ++slot) {
+      const size_t tok = pi * ws::kPageTokens + static_cast<size_t>(slot);
+      if (tok >= static_cast<size_t>(s->n_tokens)) break;
+      for (int h = 0; h < H; ++h)
+        for (int d = 0; d < ws::kHeadDim; ++d) {
+          const size_t dst = (tok * H + static_cast<size_t>(h)) * ws::kHeadDim + static_cast<size_t>(d);
+          const size_t hb = static_cast<size_t>(h) * ws::kPageHeadElems;
+          if (ko) ko[dst] = kp[hb + static_cast<size_t>(slot) * ws::kHeadDim + static_cast<size_t>(d)];
+          if (vo) vo[dst] = vp[hb + static_cast<size_t>(d) * ws::kPageTokens + static_cast<size_t>(slot)];
+        }
+    }
+  }
+  return WS_OK;
+}
+
+ws_status ws_segment_tokens(ws_cache* c, int32_t unit, ws_kind kind, int32_t* n_tokens) {
+  if (!c || !n_tokens) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  const ws::Segment* s = c->pt.find(unit, kind);
+  if (!s) return fail(WS_ERR_UNKNOWN_UNIT, "no segment for unit %d kind %d", unit, static_cast<int>(kind));
+  *n_tokens = s->n_tokens;
+  return WS_OK;
+}
+
+ws_status ws_cache_info(ws_cache* c, ws_cache_stats* st) {
+  if (!c || !st) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  st->pages_total = c->pt.max_pages();
+  st->pages_free = c->pt.free_pages();
+  st->n_segments = static_cast<int32_t>(c->pt.segments().size());
+  st->reserved = 0;
+  return WS_OK;
+}
+
+ws_status ws_cache_check(ws_cache* c, uint32_t* flags) {
+  if (!c || !flags) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (ws_status st = check_device(c); st != WS_OK) return st;
+  WS_HIP(hipDeviceSynchronize());
+  WS_HIP(hipMemcpy(flags, c->flags_dev, sizeof(uint32_t), hipMemcpyDeviceToHost));
+  WS_HIP(hipMemset(c->flags_dev, 0, sizeof(uint32_t)));
+  WS_HIP(hipDeviceSynchronize());
+  return WS_OK;
+}
+
+ws_status ws_cache_set_option(ws_cache* c, ws_option opt, int32_t value) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  switch (opt) {
+    case WS_OPT_VIDEO_KV_SPLITS:
+      if (value < 0 || value > kMaxVideoSplits) return fail(WS_ERR_INVALID_ARG, "video splits out of range");
+      c->opt_video_splits = value;
+      return WS_OK;
+    case WS_OPT_AUDIO_KV_SPLITS:
+      if (value < 0 || value > kMaxAudioSplits) return fail(WS_ERR_INVALID_ARG, "audio splits out of range");
+      c->opt_audio_splits = value;
+      return WS_OK;
+  }
+  return fail(WS_ERR_INVALID_ARG, "unknown option %d", static_cast<int>(opt));
+}
+
+const char* ws_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,100 @@
+// Launch interface of the gfx950 kernels (host side sees only these structs
+// and the launch functions; the kernels live in kernels.hip).
+//
+// Device memory layout of the paged cache (all bf16):
+//   K pool: [page][head][64 slots][128 d]   -- a (page, head) tile is 16 KB contiguous
+//   V pool: [page][head][128 d][64 slots]   -- stored transposed, so the P*V
+//           MFMA operand (eight consecutive keys of one d) is one 16-byte load
+// Slots past a segment's last token hold zeros, so masked keys never carry
+// non-finite values into the P*V product.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace ws {
+
+constexpr int kHeadDim = 128;
+constexpr int kPageTokens = 64;
+constexpr int64_t kPageHeadElems = int64_t(kHeadDim) * kPageTokens;  // 8192
+
+// Device error flags (ws_cache_check).
+constexpr uint32_t kFlagPositionClamped = 1u;
+
+struct RopeTables {
+  const float2* tab[3];  // (cos, sin) per band: [max_pos[b]][pairs[b]]
+  int32_t max_pos[3];
+  int32_t pairs[3];
+};
+
+struct AppendArgs {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t tok_stride;
+  int64_t head_stride;
+  int32_t n_tokens;      // tokens of the whole segment
+  int32_t first_page;    // index (within the segment) of pages[0]
+  int32_t n_pages;       // pages handled by this launch (<= kMaxAppendPages)
+  int32_t mode;          // 0 raw, 1 norm + rope
+  const int32_t* positions;
+  const float* gamma;
+  float eps;
+  int32_t num_heads;
+  uint16_t* kpool;
+  uint16_t* vpool;
+  RopeTables rope;
+  uint32_t* flags;
+  static constexpr int kMaxAppendPages = 192;
+  int32_t pages[kMaxAppendPages];
+};
+
+struct AttnArgs {
+  const uint16_t* q;
+  int64_t q_tok_stride;
+  int64_t q_head_stride;
+  int32_t n_q;
+  int32_t num_heads;
+  int32_t mode;          // query prologue: 0 raw, 1 norm + rope
+  const int32_t* positions;
+  const float* gamma;
+  float eps;
+  float scale_log2;      // softmax scale * log2(e)
+  RopeTables rope;
+  const uint16_t* kpool;
+  const uint16_t* vpool;
+  const int2* pages;     // visible pages: (page id, valid tokens)
+  int32_t n_pages;
+  int32_t n_splits;      // key-range splits (1: write bf16 output directly)
+  int32_t pages_per_split;
+  int32_t n_qtiles;
+  uint16_t* out;
+  int64_t out_tok_stride;
+  int64_t out_head_stride;
+  float* part_o;         // [split][head][n_q][128] fp32, normalised
+  float* part_lse;       // [split][head][n_q], log2 domain (scaled logits)
+  uint32_t* flags;
+};
+
+struct CombineArgs {
+  const float* part_o;
+  const float* part_lse;
+  int32_t n_splits;
+  int32_t n_q;
+  int32_t num_heads;
+  uint16_t* out;
+  int64_t out_tok_stride;
+  int64_t out_head_stride;
+};
+
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
+// Video path: 128-query tiles on 4 waves, 32x32x16 bf16 MFMA, LDS-staged pages.
+hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
+// Audio path: one wave per (head, key range), 16x16x32 bf16 MFMA, no LDS.
+hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+
+constexpr int kVideoQTile = 128;
+constexpr int kAudioQTile = 16;
+
+}  // namespace ws

@@ -1,0 +1,304 @@
+"""Thin ctypes binding of libws.so (the C ABI of include/ws.h).
+
+Functions carry the C names and only marshal arguments; every step of the
+attention path runs in the HIP kernels of libws.so.  ``Cache`` is a small
+convenience wrapper that takes torch tensors (device memory and the current
+stream are torch's; nothing is computed with torch).
+
+Importing this module loads libws.so and raises if it is missing: there is no
+fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from . import _build
+
+if not os.path.exists(_build.LIB_PATH):
+    raise ImportError(
+        f"libws.so not built ({_build.LIB_PATH}); run __graft_entry__.build() or "
+        "`python -m paper_2607_04443_amd._build`")
+
+_lib = ctypes.CDLL(_build.LIB_PATH)
+
+# --------------------------------------------------------------------------- #
+# types (mirror include/ws.h)
+# --------------------------------------------------------------------------- #
+WS_OK, WS_ERR_INVALID_ARG, WS_ERR_SHAPE, WS_ERR_OUT_OF_PAGES = 0, 1, 2, 3
+WS_ERR_UNKNOWN_UNIT, WS_ERR_COMMITTED, WS_ERR_UNSUPPORTED, WS_ERR_HIP = 4, 5, 6, 7
+STATUS_NAMES = {0: "WS_OK", 1: "WS_ERR_INVALID_ARG", 2: "WS_ERR_SHAPE", 3: "WS_ERR_OUT_OF_PAGES",
+                4: "WS_ERR_UNKNOWN_UNIT", 5: "WS_ERR_COMMITTED", 6: "WS_ERR_UNSUPPORTED",
+                7: "WS_ERR_HIP"}
+WS_KIND_COND, WS_KIND_VIDEO, WS_KIND_AUDIO = 0, 1, 2
+WS_APPEND_RAW, WS_APPEND_NORM_ROPE = 0, 1
+WS_OPT_VIDEO_KV_SPLITS, WS_OPT_AUDIO_KV_SPLITS = 0, 1
+INT32_MIN = -(2 ** 31)
+
+
+def WS_KIND_BIT(kind):
+    return 1 << kind
+
+
+class ws_cache_config(ctypes.Structure):
+    _fields_ = [("num_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_tokens", ctypes.c_int32), ("max_pages", ctypes.c_int32),
+                ("max_q_tokens", ctypes.c_int32), ("rope_max_pos", ctypes.c_int32 * 3),
+                ("rope_pairs", ctypes.c_int32 * 3), ("rope_theta", ctypes.c_double)]
+
+
+class ws_append_desc(ctypes.Structure):
+    _fields_ = [("unit", ctypes.c_int32), ("kind", ctypes.c_int32), ("n_tokens", ctypes.c_int32),
+                ("mode", ctypes.c_int32), ("positions", ctypes.c_void_p),
+                ("gamma", ctypes.c_void_p), ("eps", ctypes.c_float)]
+
+
+class ws_query_desc(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("positions", ctypes.c_void_p),
+                ("gamma", ctypes.c_void_p), ("eps", ctypes.c_float),
+                ("softmax_scale", ctypes.c_float)]
+
+
+class ws_mask_spec(ctypes.Structure):
+    _fields_ = [("q_unit", ctypes.c_int32), ("min_visible_unit", ctypes.c_int32),
+                ("kind_mask", ctypes.c_uint32)]
+
+
+class ws_cache_stats(ctypes.Structure):
+    _fields_ = [("pages_total", ctypes.c_int32), ("pages_free", ctypes.c_int32),
+                ("n_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+_vp, _i32, _i64, _u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+_P = ctypes.POINTER
+_SIGS = {
+    "ws_cache_create": [_P(ws_cache_config), _P(_vp)],
+    "ws_cache_destroy": [_vp],
+    "ws_cache_reset": [_vp],
+    "ws_kv_append": [_vp, _vp, _vp, _i64, _i64, _P(ws_append_desc), _vp],
+    "ws_unit_commit": [_vp, _i32],
+    "ws_kv_evict_before": [_vp, _i32],
+    "ws_kv_release": [_vp, _i32, _i32],
+    "ws_unit_attention": [_vp, _i64, _i64, _i32, _P(ws_query_desc), _vp, _P(ws_mask_spec), _vp,
+                          _i64, _i64, _vp],
+    "ws_audio_attention": [_vp, _i64, _i64, _i32, _P(ws_query_desc), _vp, _P(ws_mask_spec), _vp,
+                           _i64, _i64, _vp],
+    "ws_cache_export": [_vp, _i32, _i32, _vp, _vp],
+    "ws_segment_tokens": [_vp, _i32, _i32, _P(_i32)],
+    "ws_cache_info": [_vp, _P(ws_cache_stats)],
+    "ws_cache_check": [_vp, _P(_u32)],
+    "ws_cache_set_option": [_vp, _i32, _i32],
+}
+for _name, _args in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = ctypes.c_int
+_lib.ws_last_error.argtypes = []
+_lib.ws_last_error.restype = ctypes.c_char_p
+
+
+class WsError(RuntimeError):
+    def __init__(self, status, fn):
+        self.status = status
+        msg = _lib.ws_last_error().decode(errors="replace")
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)}: {msg}")
+
+
+def _check(status, fn):
+    if status != WS_OK:
+        raise WsError(status, fn)
+
+
+# --------------------------------------------------------------------------- #
+# same-named entry points (raw pointers / ints)
+# --------------------------------------------------------------------------- #
+def ws_cache_create(cfg: ws_cache_config) -> int:
+    h = _vp()
+    _check(_lib.ws_cache_create(ctypes.byref(cfg), ctypes.byref(h)), "ws_cache_create")
+    return h.value
+
+
+def ws_cache_destroy(cache):
+    _check(_lib.ws_cache_destroy(cache), "ws_cache_destroy")
+
+
+def ws_cache_reset(cache):
+    _check(_lib.ws_cache_reset(cache), "ws_cache_reset")
+
+
+def ws_kv_append(cache, k, v, tok_stride, head_stride, desc: ws_append_desc, stream):
+    _check(_lib.ws_kv_append(cache, k, v, tok_stride, head_stride, ctypes.byref(desc), stream),
+           "ws_kv_append")
+
+
+def ws_unit_commit(cache, unit):
+    _check(_lib.ws_unit_commit(cache, unit), "ws_unit_commit")
+
+
+def ws_kv_evict_before(cache, unit):
+    _check(_lib.ws_kv_evict_before(cache, unit), "ws_kv_evict_before")
+
+
+def ws_kv_release(cache, unit, kind):
+    _check(_lib.ws_kv_release(cache, unit, kind), "ws_kv_release")
+
+
+def ws_unit_attention(q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
+                      out_tok_stride, out_head_stride, stream):
+    _check(_lib.ws_unit_attention(q, q_tok_stride, q_head_stride, n_q, ctypes.byref(qdesc), cache,
+                                  ctypes.byref(mask), out, out_tok_stride, out_head_stride,
+                                  stream), "ws_unit_attention")
+
+
+def ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
+                       out_tok_stride, out_head_stride, stream):
+    _check(_lib.ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, ctypes.byref(qdesc), cache,
+                                   ctypes.byref(mask), out, out_tok_stride, out_head_stride,
+                                   stream), "ws_audio_attention")
+
+
+def ws_cache_export(cache, unit, kind, k_host, v_host):
+    _check(_lib.ws_cache_export(cache, unit, kind, k_host, v_host), "ws_cache_export")
+
+
+def ws_segment_tokens(cache, unit, kind) -> int:
+    n = _i32()
+    _check(_lib.ws_segment_tokens(cache, unit, kind, ctypes.byref(n)), "ws_segment_tokens")
+    return n.value
+
+
+def ws_cache_info(cache) -> ws_cache_stats:
+    st = ws_cache_stats()
+    _check(_lib.ws_cache_info(cache, ctypes.byref(st)), "ws_cache_info")
+    return st
+
+
+def ws_cache_check(cache) -> int:
+    f = _u32()
+    _check(_lib.ws_cache_check(cache, ctypes.byref(f)), "ws_cache_check")
+    return f.value
+
+
+def ws_cache_set_option(cache, opt, value):
+    _check(_lib.ws_cache_set_option(cache, opt, value), "ws_cache_set_option")
+
+
+def ws_last_error() -> str:
+    return _lib.ws_last_error().decode(errors="replace")
+
+
+# --------------------------------------------------------------------------- #
+# torch-facing convenience wrapper (marshalling only)
+# --------------------------------------------------------------------------- #
+def _stream_handle(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check_tensor(name, t, dtype):
+    import torch
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}")
+    if dtype == torch.bfloat16 and (t.dim() != 3 or t.stride(2) != 1):
+        raise ValueError(f"{name} must be [tokens, heads, 128] with unit innermost stride")
+
+
+class Cache:
+    """Owns one ws_cache; methods mirror ws_kv_append / ws_unit_attention / ..."""
+
+    def __init__(self, num_heads, max_pages, max_q_tokens=1024, rope_max_pos=(65536, 256, 256),
+                 rope_pairs=(22, 21, 21), rope_theta=10000.0):
+        cfg = ws_cache_config()
+        cfg.num_heads, cfg.head_dim, cfg.page_tokens = num_heads, 128, 64
+        cfg.max_pages, cfg.max_q_tokens = max_pages, max_q_tokens
+        cfg.rope_max_pos[:] = list(rope_max_pos)
+        cfg.rope_pairs[:] = list(rope_pairs)
+        cfg.rope_theta = rope_theta
+        self.num_heads = num_heads
+        self.handle = ws_cache_create(cfg)
+
+    def close(self):
+        if self.handle:
+            ws_cache_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def append(self, unit, kind, k, v, mode=WS_APPEND_RAW, positions=None, gamma=None, eps=1e-6,
+               stream=None):
+        import torch
+        _check_tensor("k", k, torch.bfloat16)
+        _check_tensor("v", v, torch.bfloat16)
+        if k.stride() != v.stride() or k.shape != v.shape:
+            raise ValueError("k and v must share shape and strides")
+        d = ws_append_desc()
+        d.unit, d.kind, d.n_tokens, d.mode = unit, kind, k.shape[0], mode
+        d.positions = positions.data_ptr() if positions is not None else None
+        d.gamma = gamma.data_ptr() if gamma is not None else None
+        d.eps = eps
+        ws_kv_append(self.handle, k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), d,
+                     _stream_handle(stream))
+
+    def _attn(self, fn, q, out, mask, mode, positions, gamma, eps, scale, stream):
+        import torch
+        _check_tensor("q", q, torch.bfloat16)
+        _check_tensor("out", out, torch.bfloat16)
+        qd = ws_query_desc()
+        qd.mode = mode
+        qd.positions = positions.data_ptr() if positions is not None else None
+        qd.gamma = gamma.data_ptr() if gamma is not None else None
+        qd.eps, qd.softmax_scale = eps, scale
+        fn(q.data_ptr(), q.stride(0), q.stride(1), q.shape[0], qd, self.handle, mask,
+           out.data_ptr(), out.stride(0), out.stride(1), _stream_handle(stream))
+        return out
+
+    def unit_attention(self, q, out, mask, mode=WS_APPEND_NORM_ROPE, positions=None, gamma=None,
+                       eps=1e-6, scale=0.0, stream=None):
+        return self._attn(ws_unit_attention, q, out, mask, mode, positions, gamma, eps, scale,
+                          stream)
+
+    def audio_attention(self, q, out, mask, mode=WS_APPEND_NORM_ROPE, positions=None,
+                        gamma=None, eps=1e-6, scale=0.0, stream=None):
+        return self._attn(ws_audio_attention, q, out, mask, mode, positions, gamma, eps, scale,
+                          stream)
+
+    def commit(self, unit):
+        ws_unit_commit(self.handle, unit)
+
+    def evict_before(self, unit):
+        ws_kv_evict_before(self.handle, unit)
+
+    def release(self, unit, kind):
+        ws_kv_release(self.handle, unit, kind)
+
+    def export(self, unit, kind):
+        """(K, V) of a segment as numpy uint16 bf16 bits [n, H, 128]."""
+        import numpy as np
+        n = ws_segment_tokens(self.handle, unit, kind)
+        k = np.empty((n, self.num_heads, 128), dtype=np.uint16)
+        v = np.empty_like(k)
+        ws_cache_export(self.handle, unit, kind, k.ctypes.data, v.ctypes.data)
+        return k, v
+
+    def info(self):
+        return ws_cache_info(self.handle)
+
+    def check(self):
+        return ws_cache_check(self.handle)
+
+    def set_option(self, opt, value):
+        ws_cache_set_option(self.handle, opt, value)
+
+
+def mask_spec(q_unit, min_visible_unit=INT32_MIN, kinds=(WS_KIND_COND, WS_KIND_VIDEO)):
+    m = ws_mask_spec()
+    m.q_unit, m.min_visible_unit = q_unit, min_visible_unit
+    m.kind_mask = sum(1 << k for k in kinds)
+    return m
