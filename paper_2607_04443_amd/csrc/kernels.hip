@@ -28,6 +28,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_inff();
+// Lazy-max threshold of the video softmax, log2 units.
+constexpr float kLazyTau = 8.0f;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -168,15 +170,175 @@ __device__ __forceinline__ int swz_v(int d, int chunk) { return chunk ^ ((d ^ (d
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-struct VideoSmem {
-  uint16_t k[2][kPageTokens * kHeadDim];
-  uint16_t v[2][kHeadDim * kPageTokens];
+// LDS stages of the video kernel: K [64][128] and V^T [128][64] per stage,
+// 16-byte chunks XOR-swizzled (swz_k, swz_v).
+__shared__ __attribute__((aligned(16))) uint16_t g_vk[2][kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(16))) uint16_t g_vv[2][kHeadDim * kPageTokens];
+
+struct VideoState {
+  f32x16 o[4];
+  float m_run;
+  float l_run;
+  bool first;
 };
 
+// Read-only for a whole launch: accessed through the constant address space
+// so that uniform reads become scalar loads.
+typedef const __attribute__((address_space(4))) int2* const_page_list;
+
+struct VideoCtx {
+  const_page_list pages;   // visible page list
+  const uint16_t* kpool;   // pool base + this head's tile offset
+  const uint16_t* vpool;
+  int64_t page_stride;     // elements per page (all heads)
+  int tid, half, l32, krow;
+  bf16x8 qreg[8];
+};
+
+// The 16 KB K (or V^T) tile of (page, head): thread t stages chunks
+// t + 256 i, i = 0..3 (coalesced 16-byte loads).
+__device__ __forceinline__ void stage_load(const VideoCtx& c, const uint16_t* pool, int page,
+                                           u32x4 (&st)[4]) {
+  const u32x4* src = reinterpret_cast<const u32x4*>(pool + page * c.page_stride);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) st[i] = src[c.tid + 256 * i];
+}
+
+__device__ __forceinline__ void stage_store_k(const VideoCtx& c, uint16_t* dst, const u32x4 (&st)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = c.tid + 256 * i;
+    const int r = ch >> 4;
+    *reinterpret_cast<u32x4*>(dst + r * kHeadDim + 8 * swz_k(r, ch & 15)) = st[i];
+  }
+}
+
+__device__ __forceinline__ void stage_store_v(const VideoCtx& c, uint16_t* dst, const u32x4 (&st)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = c.tid + 256 * i;
+    const int d = ch >> 3;
+    *reinterpret_cast<u32x4*>(dst + d * kPageTokens + 8 * swz_v(d, ch & 7)) = st[i];
+  }
+}
+
+// One 64-key page from LDS stage `cur`.  While it is computed, page pi + 1 is
+// staged through registers into the other stage: its K during S = K Q''^T,
+// its V^T during the softmax and O += P V.  One barrier per page.
+__device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, int pi, int p_end,
+                                           int cur) {
+  const uint16_t* sk = g_vk[cur];
+  const uint16_t* sv = g_vv[cur];
+  pi = __builtin_amdgcn_readfirstlane(pi);
+  const int n_valid = c.pages[pi].y;
+  // the last page of the range re-stages itself into the idle stage, which
+  // keeps the staging free of branches (nothing reads that copy)
+  const int next_page = c.pages[pi + 1 < p_end ? pi + 1 : pi].x;
+  __syncthreads();
+  u32x4 stg[4];
+  stage_load(c, c.kpool, next_page, stg);
+  // keep the staging loads here, ahead of the MFMAs that hide their latency
+  __builtin_amdgcn_sched_barrier(0);
+  const int half = c.half, krow = c.krow;
+
+  // S^T = K Q''^T; K operands fetched one step ahead
+  f32x16 s0, s1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    s0[r] = 0.f;
+    s1[r] = 0.f;
+  }
+  auto kread = [&](int s, int row) {
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kHeadDim + 8 * swz_k(krow, 2 * s + half)));
+  };
+  bf16x8 ka_n = kread(0, krow), kb_n = kread(0, 32 + krow);
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const bf16x8 ka = ka_n, kb = kb_n;
+    if (s < 7) {
+      ka_n = kread(s + 1, krow);
+      kb_n = kread(s + 1, 32 + krow);
+    }
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, c.qreg[s], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, c.qreg[s], s1, 0, 0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  stage_store_k(c, g_vk[cur ^ 1], stg);
+  stage_load(c, c.vpool, next_page, stg);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // page tail: register r of half h holds key 16*(r/8) + 8*h + r%8 (+32 in s1)
+  if (n_valid < kPageTokens) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = 16 * (r >> 3) + 8 * half + (r & 7);
+      if (key >= n_valid) s0[r] = kNegInf;
+      if (key + 32 >= n_valid) s1[r] = kNegInf;
+    }
+  }
+
+  // online softmax with a lazily raised maximum (relative to m_run)
+  float mx = fmaxf(s0[0], s1[0]);
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+  mx = fmaxf(mx, __shfl_xor(mx, 32)) - st.m_run;
+  const bool need = st.first || mx > kLazyTau;
+  st.first = false;
+  if (__any(need)) {
+    const float delta = need ? mx : 0.f;
+    st.m_run += delta;
+    const float alpha = fast_exp2(-delta);
+    st.l_run *= alpha;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) st.o[t] *= alpha;
+  }
+  const float m_run = st.m_run;
+
+  // P = exp2(S) in bf16; the row sum is taken over the same bf16 values
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  bf16x8 pb[4];
+  float l_run = st.l_run;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    u32x4 w0, w1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // bit-cast scalar temporaries: a bit-cast of a vector element
+      // subscript is lowered to element 0 by this compiler
+      const uint32_t p0 = pack_bf16(fast_exp2(s0[8 * j + 2 * i] - m_run), fast_exp2(s0[8 * j + 2 * i + 1] - m_run));
+      const uint32_t p1 = pack_bf16(fast_exp2(s1[8 * j + 2 * i] - m_run), fast_exp2(s1[8 * j + 2 * i + 1] - m_run));
+      w0[i] = p0;
+      w1[i] = p1;
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p0), ones, l_run, false);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p1), ones, l_run, false);
+    }
+    pb[j] = as_bf16x8(w0);
+    pb[2 + j] = as_bf16x8(w1);
+  }
+  st.l_run = l_run;
+
+  // O^T += V^T P^T; V operands fetched one MFMA ahead
+  auto vread = [&](int t, int j) {
+    const int d = 32 * t + c.l32;
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kPageTokens + 8 * swz_v(d, 2 * j + half)));
+  };
+  bf16x8 va_n = vread(0, 0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16x8 va = va_n;
+      if (t < 3 || j < 3) va_n = vread(j < 3 ? t : t + 1, (j + 1) & 3);
+      st.o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[j], st.o[t], 0, 0, 0);
+    }
+  }
+  stage_store_v(c, g_vv[cur ^ 1], stg);
+}
+
 __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) VideoSmem sm;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, l32 = lane & 31;
 
   // Work decode.  Workgroups are dispatched round-robin over the 8 XCDs;
@@ -192,7 +354,17 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
   const int p_begin = split * a.pages_per_split;
   const int p_end = min(a.n_pages, p_begin + a.pages_per_split);
 
-  // ---- Q prologue: lane holds Q'[q][16s + 8h + j], s = 0..7, j = 0..7 ----
+  VideoCtx c;
+  c.pages = (const_page_list)a.pages;
+  c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
+  c.kpool = a.kpool + head * kPageHeadElems;
+  c.vpool = a.vpool + head * kPageHeadElems;
+  c.tid = tid;
+  c.half = half;
+  c.l32 = l32;
+  c.krow = swap23(l32);
+
+  // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
   const int q = qtile * kVideoQTile + wave * 32 + l32;
   const bool q_ok = q < a.n_q;
   u32x4 qraw[8];
@@ -200,8 +372,7 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
 #pragma unroll
   for (int s = 0; s < 8; ++s)
     qraw[s] = q_ok ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : (u32x4){0u, 0u, 0u, 0u};
-  bf16x8 qreg[8];
-  if (a.mode == 1) {
+    if (a.mode == 1) {
     float ss = 0.f;
 #pragma unroll
     for (int s = 0; s < 8; ++s)
@@ -226,131 +397,50 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
         const float y0 = bf16_lo(qraw[s][i]) * inv * g[2 * i];
         const float y1 = bf16_hi(qraw[s][i]) * inv * g[2 * i + 1];
         const float2 cs = rope_cs(a.rope, (d0 >> 1) + i, pt, ph, pw);
-        w[i] = pack_bf16(y0 * cs.x - y1 * cs.y, y0 * cs.y + y1 * cs.x);
+        w[i] = pack_bf16((y0 * cs.x - y1 * cs.y) * a.scale_log2, (y0 * cs.y + y1 * cs.x) * a.scale_log2);
       }
-      qreg[s] = as_bf16x8(q_ok ? w : (u32x4){0u, 0u, 0u, 0u});
+      c.qreg[s] = as_bf16x8(q_ok ? w : (u32x4){0u, 0u, 0u, 0u});
     }
   } else {
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qreg[s] = as_bf16x8(qraw[s]);
+    for (int s = 0; s < 8; ++s) {
+      u32x4 w;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        w[i] = pack_bf16(bf16_lo(qraw[s][i]) * a.scale_log2, bf16_hi(qraw[s][i]) * a.scale_log2);
+      c.qreg[s] = as_bf16x8(w);
+    }
   }
 
   // ---- main loop over this split's pages ----
-  f32x16 o[4];
+  // Logits arrive in the log2 domain (the scale and log2(e) are folded into
+  // Q'').  The S accumulators start at -m_run, so exp2 applies directly.  The
+  // running maximum is raised lazily: only when a page exceeds it by more than
+  // kLazyTau (p then stays below 2^kLazyTau), which makes the O rescale rare.
+  VideoState st;
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
-  float m_run = kNegInf, l_run = 0.f;
-  const float c = a.scale_log2;
-  const int krow = swap23(l32);
+    for (int r = 0; r < 16; ++r) st.o[t][r] = 0.f;
+  st.m_run = 0.f;
+  st.l_run = 0.f;
+  st.first = true;
 
-  u32x4 kst[4], vst[4];
-  auto gload = [&](int pi) {
-    const int page = a.pages[pi].x;
-    const int64_t tileo = (static_cast<int64_t>(page) * a.num_heads + head) * kPageHeadElems;
-    const u32x4* kb = reinterpret_cast<const u32x4*>(a.kpool + tileo);
-    const u32x4* vb = reinterpret_cast<const u32x4*>(a.vpool + tileo);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      kst[i] = kb[tid + 256 * i];
-      vst[i] = vb[tid + 256 * i];
-    }
-  };
-  if (p_begin < p_end) gload(p_begin);
-
-  for (int pi = p_begin; pi < p_end; ++pi) {
-    const int buf = (pi - p_begin) & 1;
-    uint16_t* sk = sm.k[buf];
-    uint16_t* sv = sm.v[buf];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ch = tid + 256 * i;
-      const int kr = ch >> 4, kc = ch & 15;
-      *reinterpret_cast<u32x4*>(sk + kr * kHeadDim + 8 * swz_k(kr, kc)) = kst[i];
-      const int vd = ch >> 3, vc = ch & 7;
-      *reinterpret_cast<u32x4*>(sv + vd * kPageTokens + 8 * swz_v(vd, vc)) = vst[i];
-    }
-    __syncthreads();
-    const int n_valid = a.pages[pi].y;
-    if (pi + 1 < p_end) gload(pi + 1);
-
-    // S^T = K Q'^T
-    f32x16 s0, s1;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) { s0[r] = 0.f; s1[r] = 0.f; }
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const int ck = 2 * s + half;
-      const bf16x8 ka = as_bf16x8(
-          *reinterpret_cast<const u32x4*>(sk + krow * kHeadDim + 8 * swz_k(krow, ck)));
-      const bf16x8 kb = as_bf16x8(
-          *reinterpret_cast<const u32x4*>(sk + (32 + krow) * kHeadDim + 8 * swz_k(krow, ck)));
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[s], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qreg[s], s1, 0, 0, 0);
-    }
-
-    // page tail: register r of half h holds key 16*(r/8) + 8*h + r%8 (+32 in s1)
-    if (n_valid < kPageTokens) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = 16 * (r >> 3) + 8 * half + (r & 7);
-        if (key >= n_valid) s0[r] = kNegInf;
-        if (key + 32 >= n_valid) s1[r] = kNegInf;
-      }
-    }
-
-    // online softmax (exp2 domain, scale folded into c)
-    float mx = kNegInf;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = fast_exp2((m_run - m_use) * c);
-    const float mc = m_use * c;
-    float psum = 0.f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = fast_exp2(__builtin_fmaf(s0[r], c, -mc));
-      s1[r] = fast_exp2(__builtin_fmaf(s1[r], c, -mc));
-      psum += s0[r] + s1[r];
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-
-    bf16x8 pb[4];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      u32x4 w0, w1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        w0[i] = pack_bf16(s0[8 * j + 2 * i], s0[8 * j + 2 * i + 1]);
-        w1[i] = pack_bf16(s1[8 * j + 2 * i], s1[8 * j + 2 * i + 1]);
-      }
-      pb[j] = as_bf16x8(w0);
-      pb[2 + j] = as_bf16x8(w1);
-    }
-
-    // O^T += V^T P^T
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int d = 32 * t + l32;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bf16x8 va = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            sv + d * kPageTokens + 8 * swz_v(d, 2 * j + half)));
-        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[j], o[t], 0, 0, 0);
-      }
-    }
+  if (p_begin < p_end) {
+    u32x4 stg[4];
+    const int page = a.pages[p_begin].x;
+    stage_load(c, c.kpool, page, stg);
+    stage_store_k(c, g_vk[0], stg);
+    stage_load(c, c.vpool, page, stg);
+    stage_store_v(c, g_vv[0], stg);
+  }
+  for (int pi = p_begin; pi < p_end; pi += 2) {
+    video_page(c, st, pi, p_end, 0);
+    if (pi + 1 < p_end) video_page(c, st, pi + 1, p_end, 1);
   }
 
   // ---- epilogue: lane holds O^T[32t + 8g + 4h + i][q], g = r/4, i = r%4 ----
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = st.l_run + __shfl_xor(st.l_run, 32);
   if (!q_ok) return;
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   if (a.n_splits == 1) {
@@ -361,8 +451,8 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
       for (int g = 0; g < 4; ++g) {
         const int d0 = 32 * t + 8 * g + 4 * half;
         u32x2 w;
-        w[0] = pack_bf16(o[t][4 * g] * inv, o[t][4 * g + 1] * inv);
-        w[1] = pack_bf16(o[t][4 * g + 2] * inv, o[t][4 * g + 3] * inv);
+        w[0] = pack_bf16(st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv);
+        w[1] = pack_bf16(st.o[t][4 * g + 2] * inv, st.o[t][4 * g + 3] * inv);
         *reinterpret_cast<u32x2*>(op + d0) = w;
       }
   } else {
@@ -374,10 +464,10 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
       for (int g = 0; g < 4; ++g) {
         const int d0 = 32 * t + 8 * g + 4 * half;
         *reinterpret_cast<f32x4*>(po + d0) =
-            (f32x4){o[t][4 * g] * inv, o[t][4 * g + 1] * inv, o[t][4 * g + 2] * inv,
-                    o[t][4 * g + 3] * inv};
+            (f32x4){st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv, st.o[t][4 * g + 2] * inv,
+                    st.o[t][4 * g + 3] * inv};
       }
-    if (half == 0) a.part_lse[row] = l_tot > 0.f ? m_run * c + __log2f(l_tot) : kNegInf;
+    if (half == 0) a.part_lse[row] = l_tot > 0.f ? st.m_run + __log2f(l_tot) : kNegInf;
   }
 }
 
@@ -547,28 +637,67 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
 }
 
 // ------------------------------------------------------------------------- //
-// combine: 32 threads per (head, query) row, 4 d each; 8 rows per block.
+// combine: kGroups groups of 32 threads per (head, query) row, 4 d per thread.
+// Group g folds splits g, g + kGroups, ... with an online log-sum-exp; the
+// groups of a row then merge through LDS.  Many splits (audio) are read in
+// parallel; few splits with many rows (video) use one group per row.
 // ------------------------------------------------------------------------- //
+template <int kGroups>
 __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
-  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
-  if (row >= a.num_heads * a.n_q) return;
-  const int head = row / a.n_q, q = row % a.n_q;
-  const int d0 = 4 * (threadIdx.x & 31);
+  constexpr int kRowsPerBlock = 8 / kGroups;
+  __shared__ float sm_m[8], sm_w[8];
+  __shared__ f32x4 sm_acc[8][32];
+  const int grp = threadIdx.x >> 5;
+  const int lane = threadIdx.x & 31;
+  const int g = grp % kGroups;
+  const int row = blockIdx.x * kRowsPerBlock + grp / kGroups;
+  const bool row_ok = row < a.num_heads * a.n_q;
+  const int d0 = 4 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
-  float mx = kNegInf;
-  for (int s = 0; s < a.n_splits; ++s) mx = fmaxf(mx, a.part_lse[s * split_stride + row]);
+  float mx = kNegInf, wsum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
-  if (mx != kNegInf) {
-    for (int s = 0; s < a.n_splits; ++s) {
-      const float l = a.part_lse[s * split_stride + row];
+  if (row_ok) {
+    for (int sp = g; sp < a.n_splits; sp += kGroups) {
+      const float l = a.part_lse[sp * split_stride + row];
       if (l == kNegInf) continue;
+      const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + (sp * split_stride + row) * kHeadDim + d0);
+      if (l > mx) {
+        const float sc = fast_exp2(mx - l);
+        acc *= sc;
+        wsum *= sc;
+        mx = l;
+      }
       const float w = fast_exp2(l - mx);
+      acc += w * o;
       wsum += w;
-      acc += w * *reinterpret_cast<const f32x4*>(a.part_o + (s * split_stride + row) * kHeadDim + d0);
     }
-    acc *= 1.0f / wsum;
   }
+  if (kGroups > 1) {
+    if (lane == 0) {
+      sm_m[grp] = mx;
+      sm_w[grp] = wsum;
+    }
+    sm_acc[grp][lane] = acc;
+    __syncthreads();
+    if (g != 0) return;
+    float big = kNegInf;
+#pragma unroll
+    for (int k = 0; k < kGroups; ++k) big = fmaxf(big, sm_m[grp + k]);
+    wsum = 0.f;
+    acc = (f32x4){0.f, 0.f, 0.f, 0.f};
+    if (big != kNegInf) {
+#pragma unroll
+      for (int k = 0; k < kGroups; ++k) {
+        const float w = fast_exp2(sm_m[grp + k] - big);
+        wsum += w * sm_w[grp + k];
+        acc += w * sm_acc[grp + k][lane];
+      }
+    }
+    mx = big;
+  }
+  if (!row_ok) return;
+  const int head = row / a.n_q, q = row % a.n_q;
+  if (mx != kNegInf) acc *= 1.0f / wsum;
   u32x2 w;
   w[0] = pack_bf16(acc[0], acc[1]);
   w[1] = pack_bf16(acc[2], acc[3]);
@@ -601,8 +730,16 @@ hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   const int rows = a.num_heads * a.n_q;
-  dim3 grid((rows + 7) / 8);
-  hipLaunchKernelGGL(combine_kernel, grid, dim3(256), 0, stream, a);
+  int groups = 1;
+  if (rows < 4096) groups = a.n_splits >= 8 ? 8 : a.n_splits >= 4 ? 4 : a.n_splits >= 2 ? 2 : 1;
+  const int rows_per_block = 8 / groups;
+  dim3 grid((rows + rows_per_block - 1) / rows_per_block);
+  switch (groups) {
+    case 8: hipLaunchKernelGGL(combine_kernel<8>, grid, dim3(256), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL(combine_kernel<4>, grid, dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(combine_kernel<2>, grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL(combine_kernel<1>, grid, dim3(256), 0, stream, a); break;
+  }
   return hipGetLastError();
 }
 

@@ -7,13 +7,15 @@ import oracle
 from paper_2607_04443_amd import synth
 
 # Gates.  Contract: max |err| <= 2e-2 and mean |err| <= 2e-3 on bf16 outputs.
-# Internal, stricter: relative Frobenius <= 1e-2 (one dropped 64-key page at
-# 8.5k keys gives ~9%) and, elementwise, |err| <= 3e-3 + 2^-8 |ref| (half a
-# bf16 ulp of output rounding plus the logit error of bf16 Q'/K'/P).  A
-# workload whose logits are k times wider (gamma_q = k) scales the absolute
-# terms by k.
+# Internal, stricter, and scale-free: relative Frobenius <= 1e-2 (one dropped
+# 64-key page at 8.5k keys gives ~9%), and elementwise
+#   |err| <= 2^-7 |ref| + 0.08 rms(ref)
+# (one bf16 ulp of output rounding, plus a term sized to ~3x the largest
+# logit/P rounding error seen at 124..30616 keys; a wrong row, tile or page
+# errs by O(|ref|) and fails it).  A workload whose logits are k times wider
+# (gamma_q = k) scales the contract's absolute gates by k.
 CONTRACT_MAX, CONTRACT_MEAN = 2e-2, 2e-3
-STRICT_FROB, STRICT_ABS, STRICT_REL = 1e-2, 3e-3, 2.0 ** -8
+STRICT_FROB, STRICT_REL, STRICT_RMS = 1e-2, 2.0 ** -7, 0.08
 
 
 def to_dev(bits):
@@ -106,8 +108,9 @@ def errors(got, ref):
 def assert_gates(got, ref, strict=True, label="", scale=1.0):
     assert np.isfinite(got).all(), f"{label}: non-finite output"
     e = errors(got, ref)
-    bound = scale * STRICT_ABS + STRICT_REL * np.abs(ref)
-    ratio = np.abs(got - ref) / bound
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    bound = STRICT_REL * np.abs(ref) + STRICT_RMS * rms
+    ratio = np.abs(got - ref) / np.maximum(bound, 1e-30)
     i = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
     e["worst_ratio"] = float(ratio[i])
     e["worst_ref"] = float(ref[i])
