@@ -187,6 +187,7 @@ struct VideoState {
 typedef const __attribute__((address_space(4))) int2* const_page_list;
 
 struct VideoCtx {
+  bool active;             // the wave has at least one real query row
   const_page_list pages;   // visible page list
   const uint16_t* kpool;   // pool base + this head's tile offset
   const uint16_t* vpool;
@@ -241,6 +242,15 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, krow = c.krow;
 
+  if (!c.active) {
+    // all 32 query rows of this wave are padding: stage only
+    __builtin_amdgcn_sched_barrier(0);
+    stage_store_k(c, g_vk[cur ^ 1], stg);
+    stage_load(c, c.vpool, next_page, stg);
+    stage_store_v(c, g_vv[cur ^ 1], stg);
+    return;
+  }
+
   // S^T = K Q''^T; K operands fetched one step ahead
   f32x16 s0, s1;
 #pragma unroll
@@ -277,10 +287,17 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
     }
   }
 
-  // online softmax with a lazily raised maximum (relative to m_run)
-  float mx = fmaxf(s0[0], s1[0]);
+  // online softmax with a lazily raised maximum (relative to m_run); the row
+  // maximum is a v_max3 tree over the lane's 32 logits and its partner's
+  float t[11];
 #pragma unroll
-  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+  for (int i = 0; i < 5; ++i) {
+    t[i] = fmaxf(s0[3 * i], fmaxf(s0[3 * i + 1], s0[3 * i + 2]));
+    t[5 + i] = fmaxf(s1[3 * i], fmaxf(s1[3 * i + 1], s1[3 * i + 2]));
+  }
+  t[10] = fmaxf(s0[15], s1[15]);
+  float mx = fmaxf(fmaxf(t[0], fmaxf(t[1], t[2])), fmaxf(t[3], fmaxf(t[4], t[5])));
+  mx = fmaxf(mx, fmaxf(fmaxf(t[6], fmaxf(t[7], t[8])), fmaxf(t[9], t[10])));
   mx = fmaxf(mx, __shfl_xor(mx, 32)) - st.m_run;
   const bool need = st.first || mx > kLazyTau;
   st.first = false;
@@ -290,48 +307,44 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
     const float alpha = fast_exp2(-delta);
     st.l_run *= alpha;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) st.o[t] *= alpha;
+    for (int t4 = 0; t4 < 4; ++t4) st.o[t4] *= alpha;
   }
   const float m_run = st.m_run;
 
-  // P = exp2(S) in bf16; the row sum is taken over the same bf16 values
+  // P = exp2(S - m) in bf16, 16 keys at a time, each chunk feeding the four
+  // O^T tiles right away (independent accumulators) so the exponentials of
+  // chunk jc + 1 issue while the MFMAs of chunk jc run.  The row sum is taken
+  // over the same bf16 values the MFMAs consume.
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-  bf16x8 pb[4];
   float l_run = st.l_run;
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    u32x4 w0, w1;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      // bit-cast scalar temporaries: a bit-cast of a vector element
-      // subscript is lowered to element 0 by this compiler
-      const uint32_t p0 = pack_bf16(fast_exp2(s0[8 * j + 2 * i] - m_run), fast_exp2(s0[8 * j + 2 * i + 1] - m_run));
-      const uint32_t p1 = pack_bf16(fast_exp2(s1[8 * j + 2 * i] - m_run), fast_exp2(s1[8 * j + 2 * i + 1] - m_run));
-      w0[i] = p0;
-      w1[i] = p1;
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p0), ones, l_run, false);
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p1), ones, l_run, false);
-    }
-    pb[j] = as_bf16x8(w0);
-    pb[2 + j] = as_bf16x8(w1);
-  }
-  st.l_run = l_run;
-
-  // O^T += V^T P^T; V operands fetched one MFMA ahead
-  auto vread = [&](int t, int j) {
-    const int d = 32 * t + c.l32;
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kPageTokens + 8 * swz_v(d, 2 * j + half)));
+  auto vread = [&](int t4, int jc) {
+    const int d = 32 * t4 + c.l32;
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kPageTokens + 8 * swz_v(d, 2 * jc + half)));
   };
   bf16x8 va_n = vread(0, 0);
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
+  for (int jc = 0; jc < 4; ++jc) {
+    const f32x16& sc = jc < 2 ? s0 : s1;
+    const int base = 8 * (jc & 1);
+    u32x4 w;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int i = 0; i < 4; ++i) {
+      // bit-cast a scalar temporary: a bit-cast of a vector element
+      // subscript is lowered to element 0 by this compiler
+      const uint32_t pk = pack_bf16(fast_exp2(sc[base + 2 * i] - m_run),
+                                    fast_exp2(sc[base + 2 * i + 1] - m_run));
+      w[i] = pk;
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), ones, l_run, false);
+    }
+    const bf16x8 pbj = as_bf16x8(w);
+#pragma unroll
+    for (int t4 = 0; t4 < 4; ++t4) {
       const bf16x8 va = va_n;
-      if (t < 3 || j < 3) va_n = vread(j < 3 ? t : t + 1, (j + 1) & 3);
-      st.o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[j], st.o[t], 0, 0, 0);
+      if (jc < 3 || t4 < 3) va_n = vread(t4 < 3 ? t4 + 1 : 0, t4 < 3 ? jc : jc + 1);
+      st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pbj, st.o[t4], 0, 0, 0);
     }
   }
+  st.l_run = l_run;
   stage_store_v(c, g_vv[cur ^ 1], stg);
 }
 
@@ -360,6 +373,7 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
   c.kpool = a.kpool + head * kPageHeadElems;
   c.vpool = a.vpool + head * kPageHeadElems;
   c.tid = tid;
+  c.active = qtile * kVideoQTile + wave * 32 < a.n_q;
   c.half = half;
   c.l32 = l32;
   c.krow = swap23(l32);
