@@ -129,13 +129,18 @@ typedef struct ws_cache_stats {
  * results beyond floating-point summation order. */
 typedef enum ws_option {
   WS_OPT_VIDEO_KV_SPLITS = 0,  /* key-range splits of the video kernel (1..8) */
-  WS_OPT_AUDIO_KV_SPLITS = 1   /* key-range splits of the audio kernel (1..512) */
+  WS_OPT_AUDIO_KV_SPLITS = 1,  /* key-range splits of the audio kernel (1..512) */
+  /* Softmax shift of the video kernel: 0 = automatic (a query row's logit
+   * bound |q''| * max |k| when it is at most 40 in log2 units, else a lazily
+   * raised running maximum), 1 = always the running maximum. */
+  WS_OPT_VIDEO_RUNNING_MAX = 2
 } ws_option;
 
 /* Creates a cache: allocates the K and V page pools (2 * max_pages * H * 64 *
- * 128 * 2 bytes), the rotary cos/sin tables (built in double precision on the
- * host, stored as fp32), page-list arenas and split-KV workspaces, and clears
- * the pools to zero.  Uses the current HIP device.  Synchronous.
+ * 128 * 2 bytes), a per-(page, head) table of key-norm maxima (max_pages * H
+ * floats, written by ws_kv_append with each page), the rotary cos/sin tables
+ * (built in double precision on the host, stored as fp32), page-list arenas
+ * and split-KV workspaces, and clears the pools to zero.  Uses the current HIP device.  Synchronous.
  * On success *out owns all of it until ws_cache_destroy. */
 WS_API ws_status ws_cache_create(const ws_cache_config* cfg, ws_cache** out);
 
@@ -156,7 +161,8 @@ WS_API ws_status ws_cache_reset(ws_cache* cache);
  *         t < n_tokens, h < num_heads, d < 128.
  * NORM_ROPE keys: K' = RoPE(RMSNorm(K) * gamma, positions), computed in fp32,
  * rounded to bf16.  Values are always stored as given.  Positions outside
- * [0, rope_max_pos) are clamped and flagged (ws_cache_check). */
+ * [0, rope_max_pos) are clamped and flagged (ws_cache_check).  Each written
+ * page also records, per head, the largest squared norm of its stored keys. */
 WS_API ws_status ws_kv_append(ws_cache* cache, const void* k, const void* v, int64_t tok_stride,
                        int64_t head_stride, const ws_append_desc* desc, void* hip_stream);
 
@@ -179,7 +185,11 @@ WS_API ws_status ws_kv_release(ws_cache* cache, int32_t unit, ws_kind kind);
  *   out[i] = sum_j softmax_j(scale * <Q'_i, K'_j>) V_j over the visible keys.
  *   q:   device bf16 [n_q][H][128] with strides (q_tok_stride, q_head_stride).
  *   out: device bf16 [n_q][H][128] with strides (out_tok_stride, out_head_stride).
- * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 128-query tiles, 64-key pages. */
+ * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 128-query tiles, 64-key pages.
+ * The softmax shift of a query row is its logit bound |Q''_i| * max |K'_j|
+ * (Cauchy-Schwarz over the pages of one key range) when that bound is at most
+ * 40 in log2 units, else a lazily raised running maximum
+ * (WS_OPT_VIDEO_RUNNING_MAX forces the latter); both give the same softmax. */
 WS_API ws_status ws_unit_attention(const void* q, int64_t q_tok_stride, int64_t q_head_stride,
                             int32_t n_q, const ws_query_desc* qdesc, ws_cache* cache,
                             const ws_mask_spec* mask, void* out, int64_t out_tok_stride,

@@ -30,6 +30,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr float kNegInf = -__builtin_inff();
 // Lazy-max threshold of the video softmax, log2 units.
 constexpr float kLazyTau = 8.0f;
+// Largest logit bound (log2 units) used as a fixed softmax shift.
+constexpr float kShiftBoundMax = 40.0f;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -69,6 +71,7 @@ __device__ __forceinline__ void load_pos(const RopeTables& r, const int32_t* pos
 template <int kMode>
 __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPageTokens][kHeadDim + 8];
+  __shared__ float wave_norm2[4];
   const int head = blockIdx.y;
   const int page = a.pages[blockIdx.x];
   const int tok0 = (a.first_page + blockIdx.x) * kPageTokens;
@@ -78,8 +81,10 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
   const int t = threadIdx.x;
 
   // K: 16 threads per token row, 8 consecutive d each; 16 rows per pass.
+  // Alongside, the largest squared norm of the stored rows of the tile.
   const int c = t & 15;
   const int rr = t >> 4;
+  float norm2 = 0.f;
   float g[8];
   if (kMode == 1) {
     const float4 g0 = *reinterpret_cast<const float4*>(a.gamma + 8 * c);
@@ -124,7 +129,18 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
       if (!valid) y = (u32x4){0u, 0u, 0u, 0u};
     }
     *reinterpret_cast<u32x4*>(kdst + slot * kHeadDim + 8 * c) = y;
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ss += bf16_lo(y[i]) * bf16_lo(y[i]) + bf16_hi(y[i]) * bf16_hi(y[i]);
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    ss += __shfl_xor(ss, 4);
+    ss += __shfl_xor(ss, 8);
+    norm2 = fmaxf(norm2, ss);
   }
+  norm2 = fmaxf(norm2, __shfl_xor(norm2, 16));
+  norm2 = fmaxf(norm2, __shfl_xor(norm2, 32));
+  if ((t & 63) == 0) wave_norm2[t >> 6] = norm2;
 
   // V: stage [slot][d] in LDS, write [d][slot].
 #pragma unroll
@@ -149,6 +165,9 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
              (static_cast<uint32_t>(vt[8 * tc + 2 * j + 1][d]) << 16);
     *reinterpret_cast<u32x4*>(vdst + d * kPageTokens + 8 * tc) = y;
   }
+  if (t == 0)
+    a.knorm2[static_cast<int64_t>(page) * a.num_heads + head] =
+        fmaxf(fmaxf(wave_norm2[0], wave_norm2[1]), fmaxf(wave_norm2[2], wave_norm2[3]));
 }
 
 // ------------------------------------------------------------------------- //
@@ -164,16 +183,19 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
 // directly the B operands (eight consecutive keys) of the P*V MFMAs.
 // ------------------------------------------------------------------------- //
 __device__ __forceinline__ int swap23(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
-// LDS chunk swizzles (16-byte chunks): conflict-free MFMA operand reads.
-__device__ __forceinline__ int swz_k(int row, int chunk) { return chunk ^ swap23(row & 15); }
-__device__ __forceinline__ int swz_v(int d, int chunk) { return chunk ^ ((d ^ (d >> 3)) & 7); }
+// LDS stages of the video kernel, rows padded by one 16-byte chunk:
+//   K    [64 rows][136]: key r is stored at row swap23(r), so lane i of either
+//        half reads row i (+32 for the second tile) and the eight lanes of a
+//        ds_read_b128 pass hit eight distinct 16-byte bank groups;
+//   V^T  [128 d][72].
+// With padding instead of an XOR swizzle every operand read of a page is one
+// base register plus an immediate offset.
+constexpr int kKRow = kHeadDim + 8;
+constexpr int kVRow = kPageTokens + 8;
+__shared__ __attribute__((aligned(16))) uint16_t g_vk[2][kPageTokens * kKRow];
+__shared__ __attribute__((aligned(16))) uint16_t g_vv[2][kHeadDim * kVRow];
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-// LDS stages of the video kernel: K [64][128] and V^T [128][64] per stage,
-// 16-byte chunks XOR-swizzled (swz_k, swz_v).
-__shared__ __attribute__((aligned(16))) uint16_t g_vk[2][kPageTokens * kHeadDim];
-__shared__ __attribute__((aligned(16))) uint16_t g_vv[2][kHeadDim * kPageTokens];
 
 struct VideoState {
   f32x16 o[4];
@@ -205,27 +227,115 @@ __device__ __forceinline__ void stage_load(const VideoCtx& c, const uint16_t* po
   for (int i = 0; i < 4; ++i) st[i] = src[c.tid + 256 * i];
 }
 
+// Chunk t + 256 i of the K tile is row 16 i + t/16, 16-byte column t%16;
+// swap23 leaves bits 4-5 of the row alone, so the four stores are one base
+// plus immediate offsets.
 __device__ __forceinline__ void stage_store_k(const VideoCtx& c, uint16_t* dst, const u32x4 (&st)[4]) {
+  uint16_t* base = dst + swap23(c.tid >> 4) * kKRow + 8 * (c.tid & 15);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ch = c.tid + 256 * i;
-    const int r = ch >> 4;
-    *reinterpret_cast<u32x4*>(dst + r * kHeadDim + 8 * swz_k(r, ch & 15)) = st[i];
-  }
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(base + 16 * i * kKRow) = st[i];
 }
 
+// Chunk t + 256 i of the V^T tile is row (d) 32 i + t/8, column t%8.
 __device__ __forceinline__ void stage_store_v(const VideoCtx& c, uint16_t* dst, const u32x4 (&st)[4]) {
+  uint16_t* base = dst + (c.tid >> 3) * kVRow + 8 * (c.tid & 7);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(base + 32 * i * kVRow) = st[i];
+}
+
+// max over lanes l and l ^ 32 (v_permlane32_swap: no LDS round trip)
+__device__ __forceinline__ float pair_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// v_max3 tree over one lane's 16 logits of a 32-key tile
+__device__ __forceinline__ float max16(const f32x16& s) {
+  const float a = fmaxf(s[0], fmaxf(s[1], s[2]));
+  const float b = fmaxf(s[3], fmaxf(s[4], s[5]));
+  const float c = fmaxf(s[6], fmaxf(s[7], s[8]));
+  const float d = fmaxf(s[9], fmaxf(s[10], s[11]));
+  const float e = fmaxf(s[12], fmaxf(s[13], s[14]));
+  return fmaxf(fmaxf(a, fmaxf(b, c)), fmaxf(d, fmaxf(e, s[15])));
+}
+
+// P = exp2(s) of a 32-key tile as bf16: pa holds the lane's first eight keys,
+// pb the next eight (the B operands of two P*V MFMAs).  Returns the lane's
+// row sum over the same bf16 values the MFMAs consume.
+__device__ __forceinline__ float exp_tile(const f32x16& s, u32x4& pa, u32x4& pb) {
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  float la = 0.f, lb = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int ch = c.tid + 256 * i;
-    const int d = ch >> 3;
-    *reinterpret_cast<u32x4*>(dst + d * kPageTokens + 8 * swz_v(d, ch & 7)) = st[i];
+    // bit-cast scalar temporaries: a bit-cast of a vector element subscript
+    // is lowered to element 0 by this compiler
+    const uint32_t x = pack_bf16(fast_exp2(s[2 * i]), fast_exp2(s[2 * i + 1]));
+    const uint32_t y = pack_bf16(fast_exp2(s[8 + 2 * i]), fast_exp2(s[9 + 2 * i]));
+    pa[i] = x;
+    pb[i] = y;
+    la = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, x), ones, la, false);
+    lb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, y), ones, lb, false);
+  }
+  return la + lb;
+}
+
+__device__ __forceinline__ void scale_o(VideoState& st, float alpha) {
+#pragma unroll
+  for (int t4 = 0; t4 < 4; ++t4) st.o[t4] *= alpha;
+}
+
+// Issue pattern of a 32-key step: each MFMA followed by an operand read and a
+// share of the softmax VALU work, so that one wave keeps its matrix pipe busy
+// while it computes the exponentials of the neighbouring tile.
+// kLead operand reads go first, so that every MFMA finds its operand read
+// two MFMAs earlier.
+template <int kLead>
+__device__ __forceinline__ void interleave_mfma_valu() {
+  if (kLead > 0) __builtin_amdgcn_sched_group_barrier(0x100, kLead, 0);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
   }
 }
 
-// One 64-key page from LDS stage `cur`.  While it is computed, page pi + 1 is
-// staged through registers into the other stage: its K during S = K Q''^T,
-// its V^T during the softmax and O += P V.  One barrier per page.
+// Empty asm statements that make a value live in a register at this point:
+// they keep the compiler from sinking the speculative softmax past the rare
+// rescale branch, and a scalar page-list load from drifting next to its use.
+__device__ __forceinline__ void pin_sgpr(int x) { asm volatile("" ::"s"(x)); }
+__device__ __forceinline__ void pin_vgpr(u32x4& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin_vgpr(float& x) { asm volatile("" : "+v"(x)); }
+
+// A page for a wave whose 32 query rows are all padding (ragged last query
+// tile): it only takes its share of staging page pi + 1.
+__device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi, int p_end, int cur) {
+  pi = __builtin_amdgcn_readfirstlane(pi);
+  const int next_page = c.pages[pi + 1 < p_end ? pi + 1 : pi].x;
+  __syncthreads();
+  u32x4 stg[4];
+  stage_load(c, c.kpool, next_page, stg);
+  stage_store_k(c, g_vk[cur ^ 1], stg);
+  stage_load(c, c.vpool, next_page, stg);
+  stage_store_v(c, g_vv[cur ^ 1], stg);
+}
+
+// One 64-key page from LDS stage `cur`, as two 32-key tiles (keys 0-31 in
+// s0, 32-63 in s1).  Order of issue:
+//   S tile 0 | S tile 1 + softmax of tile 0 | P*V tile 0 + softmax of tile 1
+//   | P*V tile 1
+// The S accumulators start at -m_run (or -inf past the page's valid tokens),
+// so they hold the exp2 argument directly.
+//   kLazy = false: m_run is a fixed upper bound of the row's logits (from the
+//     key norms), so there is no running maximum and nothing to rescale.
+//   kLazy = true: m_run is a running maximum raised lazily.  The
+//     exponentials are taken speculatively against the current m_run; when a
+//     tile raises it by more than kLazyTau (rare after the first tile), a
+//     branch outside the interleaved regions rescales O and l and recomputes
+//     that tile's P.
+// While the page is computed, page pi + 1 is staged through registers into
+// the other stage: its K after S, its V^T after P*V.  One barrier per page.
+template <bool kLazy>
 __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, int pi, int p_end,
                                            int cur) {
   const uint16_t* sk = g_vk[cur];
@@ -235,6 +345,9 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   // the last page of the range re-stages itself into the idle stage, which
   // keeps the staging free of branches (nothing reads that copy)
   const int next_page = c.pages[pi + 1 < p_end ? pi + 1 : pi].x;
+  // both scalars are loaded before the barrier: a scalar load left for later
+  // would share lgkmcnt with the LDS operand reads
+  pin_sgpr(n_valid);
   __syncthreads();
   u32x4 stg[4];
   stage_load(c, c.kpool, next_page, stg);
@@ -242,109 +355,135 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, krow = c.krow;
 
-  if (!c.active) {
-    // all 32 query rows of this wave are padding: stage only
-    __builtin_amdgcn_sched_barrier(0);
-    stage_store_k(c, g_vk[cur ^ 1], stg);
-    stage_load(c, c.vpool, next_page, stg);
-    stage_store_v(c, g_vv[cur ^ 1], stg);
-    return;
-  }
-
-  // S^T = K Q''^T; K operands fetched one step ahead
+  const float neg_m = -st.m_run;
   f32x16 s0, s1;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    s0[r] = 0.f;
-    s1[r] = 0.f;
+    s0[r] = neg_m;
+    s1[r] = neg_m;
   }
-  auto kread = [&](int s, int row) {
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kHeadDim + 8 * swz_k(krow, 2 * s + half)));
+  // page tail: register r of half h holds key 16*(r/8) + 8*h + r%8 (+32 in
+  // s1); keys at or past n_valid become -inf
+  const bool tail = n_valid < kPageTokens;
+  auto mask_tail = [&](f32x16& sc, int key0) {
+    const int lim = n_valid - key0 - 8 * half;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (16 * (r >> 3) + (r & 7) >= lim) sc[r] = kNegInf;
   };
-  bf16x8 ka_n = kread(0, krow), kb_n = kread(0, 32 + krow);
+
+  // K operands are read two MFMAs ahead
+  auto kread = [&](int s, int row) {
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kKRow + 8 * (2 * s + half)));
+  };
+  bf16x8 k0 = kread(0, krow), k1 = kread(1, krow);
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
-    const bf16x8 ka = ka_n, kb = kb_n;
-    if (s < 7) {
-      ka_n = kread(s + 1, krow);
-      kb_n = kread(s + 1, 32 + krow);
-    }
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, c.qreg[s], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, c.qreg[s], s1, 0, 0, 0);
+    const bf16x8 k = k0;
+    k0 = k1;
+    k1 = kread((s + 2) & 7, s + 2 < 8 ? krow : 32 + krow);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, c.qreg[s], s0, 0, 0, 0);
   }
+  __builtin_amdgcn_sched_barrier(0);
+  if (tail) mask_tail(s0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // S tile 1; softmax of tile 0 in its shadow
+  u32x4 p0a, p0b;
+  float mx0 = 0.f, l0;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const bf16x8 k = k0;
+    k0 = k1;
+    if (s < 6) k1 = kread(s + 2, 32 + krow);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, c.qreg[s], s1, 0, 0, 0);
+    if (s == 0) {
+      if constexpr (kLazy) mx0 = pair_max(max16(s0));
+      l0 = exp_tile(s0, p0a, p0b);
+    }
+  }
+  // d0: shift of the running maximum taken at tile 0 (0 for most rows)
+  const bool need0 = kLazy && (st.first || mx0 > kLazyTau);
+  float d0 = need0 ? mx0 : 0.f;
+  pin_vgpr(p0a);
+  pin_vgpr(p0b);
+  pin_vgpr(l0);
+  if constexpr (kLazy) pin_vgpr(d0);
+  interleave_mfma_valu<0>();
   __builtin_amdgcn_sched_barrier(0);
   stage_store_k(c, g_vk[cur ^ 1], stg);
   stage_load(c, c.vpool, next_page, stg);
   __builtin_amdgcn_sched_barrier(0);
 
-  // page tail: register r of half h holds key 16*(r/8) + 8*h + r%8 (+32 in s1)
-  if (n_valid < kPageTokens) {
+  if constexpr (kLazy) {
+    if (__any(need0)) {
+      const float alpha = fast_exp2(-d0);
+      st.m_run += d0;
+      st.l_run *= alpha;
+      scale_o(st, alpha);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = 16 * (r >> 3) + 8 * half + (r & 7);
-      if (key >= n_valid) s0[r] = kNegInf;
-      if (key + 32 >= n_valid) s1[r] = kNegInf;
+      for (int r = 0; r < 16; ++r) s0[r] -= d0;
+      l0 = exp_tile(s0, p0a, p0b);
     }
+    st.first = false;
   }
+  st.l_run += l0;
+  if (tail) mask_tail(s1, 32);
+  __builtin_amdgcn_sched_barrier(0);
 
-  // online softmax with a lazily raised maximum (relative to m_run); the row
-  // maximum is a v_max3 tree over the lane's 32 logits and its partner's
-  float t[11];
-#pragma unroll
-  for (int i = 0; i < 5; ++i) {
-    t[i] = fmaxf(s0[3 * i], fmaxf(s0[3 * i + 1], s0[3 * i + 2]));
-    t[5 + i] = fmaxf(s1[3 * i], fmaxf(s1[3 * i + 1], s1[3 * i + 2]));
-  }
-  t[10] = fmaxf(s0[15], s1[15]);
-  float mx = fmaxf(fmaxf(t[0], fmaxf(t[1], t[2])), fmaxf(t[3], fmaxf(t[4], t[5])));
-  mx = fmaxf(mx, fmaxf(fmaxf(t[6], fmaxf(t[7], t[8])), fmaxf(t[9], t[10])));
-  mx = fmaxf(mx, __shfl_xor(mx, 32)) - st.m_run;
-  const bool need = st.first || mx > kLazyTau;
-  st.first = false;
-  if (__any(need)) {
-    const float delta = need ? mx : 0.f;
-    st.m_run += delta;
-    const float alpha = fast_exp2(-delta);
-    st.l_run *= alpha;
-#pragma unroll
-    for (int t4 = 0; t4 < 4; ++t4) st.o[t4] *= alpha;
-  }
-  const float m_run = st.m_run;
-
-  // P = exp2(S - m) in bf16, 16 keys at a time, each chunk feeding the four
-  // O^T tiles right away (independent accumulators) so the exponentials of
-  // chunk jc + 1 issue while the MFMAs of chunk jc run.  The row sum is taken
-  // over the same bf16 values the MFMAs consume.
-  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-  float l_run = st.l_run;
+  // O^T += V^T P^T for tile 0; softmax of tile 1 in its shadow
   auto vread = [&](int t4, int jc) {
     const int d = 32 * t4 + c.l32;
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kPageTokens + 8 * swz_v(d, 2 * jc + half)));
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kVRow + 8 * (2 * jc + half)));
   };
-  bf16x8 va_n = vread(0, 0);
+  bf16x8 v0 = vread(0, 0), v1 = vread(1, 0);
+  u32x4 p1a, p1b;
+  float mx1 = 0.f, l1;
 #pragma unroll
-  for (int jc = 0; jc < 4; ++jc) {
-    const f32x16& sc = jc < 2 ? s0 : s1;
-    const int base = 8 * (jc & 1);
-    u32x4 w;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      // bit-cast a scalar temporary: a bit-cast of a vector element
-      // subscript is lowered to element 0 by this compiler
-      const uint32_t pk = pack_bf16(fast_exp2(sc[base + 2 * i] - m_run),
-                                    fast_exp2(sc[base + 2 * i + 1] - m_run));
-      w[i] = pk;
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), ones, l_run, false);
-    }
-    const bf16x8 pbj = as_bf16x8(w);
-#pragma unroll
-    for (int t4 = 0; t4 < 4; ++t4) {
-      const bf16x8 va = va_n;
-      if (jc < 3 || t4 < 3) va_n = vread(t4 < 3 ? t4 + 1 : 0, t4 < 3 ? jc : jc + 1);
-      st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pbj, st.o[t4], 0, 0, 0);
+  for (int j = 0; j < 8; ++j) {
+    const bf16x8 v = v0;
+    v0 = v1;
+    v1 = vread((j + 2) & 3, (j + 2) >> 2);
+    const int t4 = j & 3;
+    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(j < 4 ? p0a : p0b), st.o[t4], 0, 0, 0);
+    if (j == 0) {
+      if constexpr (kLazy) mx1 = pair_max(max16(s1));
+      l1 = exp_tile(s1, p1a, p1b);
     }
   }
-  st.l_run = l_run;
+  // d1: shift of tile 1 relative to the page's starting maximum
+  const bool need1 = kLazy && mx1 - d0 > kLazyTau;
+  float d1 = need1 ? mx1 : d0;
+  pin_vgpr(p1a);
+  pin_vgpr(p1b);
+  pin_vgpr(l1);
+  if constexpr (kLazy) pin_vgpr(d1);
+  interleave_mfma_valu<2>();
+  __builtin_amdgcn_sched_barrier(0);
+
+  if constexpr (kLazy) {
+    if (__any(d1 != 0.f)) {
+      const float e = d1 - d0;
+      const float alpha = fast_exp2(-e);
+      st.m_run += e;
+      st.l_run *= alpha;
+      scale_o(st, alpha);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s1[r] -= d1;
+      l1 = exp_tile(s1, p1a, p1b);
+    }
+  }
+  st.l_run += l1;
+
+  // O^T += V^T P^T for tile 1
+#pragma unroll
+  for (int j = 8; j < 16; ++j) {
+    const bf16x8 v = v0;
+    v0 = v1;
+    if (j < 14) v1 = vread((j + 2) & 3, (j + 2) >> 2);
+    const int t4 = j & 3;
+    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(j < 12 ? p1a : p1b), st.o[t4], 0, 0, 0);
+  }
   stage_store_v(c, g_vv[cur ^ 1], stg);
 }
 
@@ -376,7 +515,7 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
   c.active = qtile * kVideoQTile + wave * 32 < a.n_q;
   c.half = half;
   c.l32 = l32;
-  c.krow = swap23(l32);
+  c.krow = l32;  // LDS row l32 holds key swap23(l32)
 
   // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
   const int q = qtile * kVideoQTile + wave * 32 + l32;
@@ -426,17 +565,40 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
     }
   }
 
-  // ---- main loop over this split's pages ----
+  // ---- softmax shift ----
   // Logits arrive in the log2 domain (the scale and log2(e) are folded into
-  // Q'').  The S accumulators start at -m_run, so exp2 applies directly.  The
-  // running maximum is raised lazily: only when a page exceeds it by more than
-  // kLazyTau (p then stays below 2^kLazyTau), which makes the O rescale rare.
+  // Q'').  By Cauchy-Schwarz every logit of row q is at most
+  // B_q = |Q''_q| * max |k| over the split's pages (knorm2 holds the squared
+  // norms of the stored keys).  Softmax is shift invariant, so B_q serves as
+  // the exp2 shift as it stands: p = exp2(s - B_q) <= 1, with no running
+  // maximum and no rescale of O.  The row's largest p is at least 2^(-2 B_q),
+  // so for B_q <= kShiftBoundMax every weight above 2^-46 of the row maximum
+  // stays a normal bf16/fp32 number.  Otherwise the running maximum is raised
+  // lazily: only when a 32-key tile exceeds it by more than kLazyTau
+  // (p then stays below 2^kLazyTau), which makes the O rescale rare.
+  float kn2 = 0.f;
+  for (int pi = p_begin + lane; pi < p_end; pi += 64)
+    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(a.pages[pi].x) * a.num_heads + head]);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) kn2 = fmaxf(kn2, __shfl_xor(kn2, o));
+  float qn2 = 0.f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const u32x4 w = __builtin_bit_cast(u32x4, c.qreg[s]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) qn2 += bf16_lo(w[i]) * bf16_lo(w[i]) + bf16_hi(w[i]) * bf16_hi(w[i]);
+  }
+  qn2 += __shfl_xor(qn2, 32);
+  const float bound = sqrtf(qn2 * kn2);
+  const bool fixed_shift = a.fixed_shift != 0 && __all(bound <= kShiftBoundMax);
+
+  // ---- main loop over this split's pages ----
   VideoState st;
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) st.o[t][r] = 0.f;
-  st.m_run = 0.f;
+  st.m_run = fixed_shift ? bound : 0.f;
   st.l_run = 0.f;
   st.first = true;
 
@@ -448,9 +610,21 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
     stage_load(c, c.vpool, page, stg);
     stage_store_v(c, g_vv[0], stg);
   }
-  for (int pi = p_begin; pi < p_end; pi += 2) {
-    video_page(c, st, pi, p_end, 0);
-    if (pi + 1 < p_end) video_page(c, st, pi + 1, p_end, 1);
+  if (c.active && fixed_shift) {
+    for (int pi = p_begin; pi < p_end; pi += 2) {
+      video_page<false>(c, st, pi, p_end, 0);
+      if (pi + 1 < p_end) video_page<false>(c, st, pi + 1, p_end, 1);
+    }
+  } else if (c.active) {
+    for (int pi = p_begin; pi < p_end; pi += 2) {
+      video_page<true>(c, st, pi, p_end, 0);
+      if (pi + 1 < p_end) video_page<true>(c, st, pi + 1, p_end, 1);
+    }
+  } else {
+    for (int pi = p_begin; pi < p_end; pi += 2) {
+      video_page_stage_only(c, pi, p_end, 0);
+      if (pi + 1 < p_end) video_page_stage_only(c, pi + 1, p_end, 1);
+    }
   }
 
   // ---- epilogue: lane holds O^T[32t + 8g + 4h + i][q], g = r/4, i = r%4 ----

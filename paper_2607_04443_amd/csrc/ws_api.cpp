@@ -78,6 +78,8 @@ struct ws_cache {
   int64_t part_rows = 0;  // capacity in (split, head, query) rows
   int32_t opt_video_splits = 0;
   int32_t opt_audio_splits = 0;
+  int32_t opt_running_max = 0;
+  float* knorm2 = nullptr;  // [max_pages][H] squared key-norm maxima
   std::vector<ws::PageRef> scratch_list;
 
   ws_cache(int32_t page_tokens, int32_t max_pages) : pt(page_tokens, max_pages) {}
@@ -208,6 +210,8 @@ void free_all(ws_cache* c) {
   if (c->arena_host) (void)hipHostFree(c->arena_host);
   if (c->part_o) (void)hipFree(c->part_o);
   if (c->part_lse) (void)hipFree(c->part_lse);
+  if (c->knorm2) (void)hipFree(c->knorm2);
+  c->knorm2 = nullptr;
   c->kpool = c->vpool = nullptr;
   c->rope_dev = nullptr;
   c->flags_dev = nullptr;
@@ -256,6 +260,11 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
   if ((e = hipMalloc(&c->vpool, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMalloc(V pool)"));
   if ((e = hipMemset(c->kpool, 0, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
   if ((e = hipMemset(c->vpool, 0, pool_elems * 2)) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
+  const size_t norm_elems = static_cast<size_t>(cfg->max_pages) * cfg->num_heads;
+  if ((e = hipMalloc(&c->knorm2, norm_elems * sizeof(float))) != hipSuccess)
+    return bail(hip_fail(e, "hipMalloc(key norms)"));
+  if ((e = hipMemset(c->knorm2, 0, norm_elems * sizeof(float))) != hipSuccess)
+    return bail(hip_fail(e, "hipMemset"));
   if (ws_status st = fill_rope(c); st != WS_OK) return bail(st);
   if ((e = hipMalloc(&c->flags_dev, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMalloc"));
   if ((e = hipMemset(c->flags_dev, 0, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
@@ -341,6 +350,8 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   a.rope = c->rope;
   a.kpool = c->kpool;
   a.vpool = c->vpool;
+  a.knorm2 = c->knorm2;
+  a.fixed_shift = c->opt_running_max ? 0 : 1;
   a.pages = plist;
   a.n_pages = n_pages;
   a.out = static_cast<uint16_t*>(out);
@@ -451,6 +462,7 @@ ws_status ws_kv_append(ws_cache* c, const void* k, const void* v, int64_t tok_st
   a.num_heads = H;
   a.kpool = c->kpool;
   a.vpool = c->vpool;
+  a.knorm2 = c->knorm2;
   a.rope = c->rope;
   a.flags = c->flags_dev;
   const int n_pages = static_cast<int>(seg->pages.size());
@@ -572,6 +584,10 @@ ws_status ws_cache_set_option(ws_cache* c, ws_option opt, int32_t value) {
     case WS_OPT_AUDIO_KV_SPLITS:
       if (value < 0 || value > kMaxAudioSplits) return fail(WS_ERR_INVALID_ARG, "audio splits out of range");
       c->opt_audio_splits = value;
+      return WS_OK;
+    case WS_OPT_VIDEO_RUNNING_MAX:
+      if (value < 0 || value > 1) return fail(WS_ERR_INVALID_ARG, "running-max option must be 0 or 1");
+      c->opt_running_max = value;
       return WS_OK;
   }
   return fail(WS_ERR_INVALID_ARG, "unknown option %d", static_cast<int>(opt));

@@ -7,6 +7,8 @@
 //           MFMA operand (eight consecutive keys of one d) is one 16-byte load
 // Slots past a segment's last token hold zeros, so masked keys never carry
 // non-finite values into the P*V product.
+// Key norms: knorm2[page][head] holds the largest squared L2 norm of the
+// stored (bf16) keys of that tile; kv_append writes it with the tile.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -43,6 +45,7 @@ struct AppendArgs {
   int32_t num_heads;
   uint16_t* kpool;
   uint16_t* vpool;
+  float* knorm2;
   RopeTables rope;
   uint32_t* flags;
   static constexpr int kMaxAppendPages = 192;
@@ -63,6 +66,8 @@ struct AttnArgs {
   RopeTables rope;
   const uint16_t* kpool;
   const uint16_t* vpool;
+  const float* knorm2;
+  int32_t fixed_shift;   // 1: softmax shift from the key-norm bound when it is small enough
   const int2* pages;     // visible pages: (page id, valid tokens)
   int32_t n_pages;
   int32_t n_splits;      // key-range splits (1: write bf16 output directly)

@@ -32,7 +32,7 @@ STATUS_NAMES = {0: "WS_OK", 1: "WS_ERR_INVALID_ARG", 2: "WS_ERR_SHAPE", 3: "WS_E
                 7: "WS_ERR_HIP"}
 WS_KIND_COND, WS_KIND_VIDEO, WS_KIND_AUDIO = 0, 1, 2
 WS_APPEND_RAW, WS_APPEND_NORM_ROPE = 0, 1
-WS_OPT_VIDEO_KV_SPLITS, WS_OPT_AUDIO_KV_SPLITS = 0, 1
+WS_OPT_VIDEO_KV_SPLITS, WS_OPT_AUDIO_KV_SPLITS, WS_OPT_VIDEO_RUNNING_MAX = 0, 1, 2
 INT32_MIN = -(2 ** 31)
 
 

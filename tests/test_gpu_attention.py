@@ -239,3 +239,90 @@ def test_masked_segment_equals_deleted_segment(ws):
     finally:
         A.close()
         B.close()
+
+
+@pytest.mark.parametrize("name", ["v01", "tiny"])
+def test_video_running_max_path(ws, name):
+    """The lazily raised running maximum (forced by option) against the
+    oracle, and against the default key-norm-bound shift on the same cache:
+    the two shifts give the same softmax."""
+    wl = synth.make_workload(TINY if name == "tiny" else name)
+    L = Loaded(ws, wl)
+    try:
+        st = wl.steps[0]
+        kinds = ALL_KINDS if name == "tiny" else VIDEO_KINDS
+        fixed = L.run("video", st.q_video, st.q_video_pos, wl.current_unit, kinds)
+        L.cache.set_option(ws.WS_OPT_VIDEO_RUNNING_MAX, 1)
+        for splits in (1, 3):
+            L.cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, splits)
+            lazy = L.run("video", st.q_video, st.q_video_pos, wl.current_unit, kinds)
+            ref = L.oracle(st.q_video, st.q_video_pos, wl.current_unit, kinds)
+            assert_gates(lazy, ref, label=f"running max, splits={splits}")
+        assert_gates(fixed, lazy, label="bound shift vs running max")
+    finally:
+        L.close()
+
+
+def _raw_cond_workload(name, H, k, v):
+    cfg = synth.Config(name, 20, H, (1, 1), k.shape[0], 0)
+    wl = synth.make_workload(cfg)
+    wl.cached[0].k, wl.cached[0].v = k, v
+    return wl
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+def test_video_large_key_norm_falls_back(ws, splits):
+    """A page with a few long keys (norm 40 along one axis) lifts that key
+    range's logit bound above 40, so its waves fall back to the running
+    maximum while the other ranges keep the bound shift; the merged result
+    must match the oracle.  The queries are short along those axes, so the
+    long keys' logits stay ordinary (about 1.3 sigma in log2 units) and the
+    bf16 rounding of the queries does not dominate the comparison."""
+    rng = np.random.default_rng(21)
+    H, n_keys, n_q = 3, 64 * 9 + 5, 150
+    k = synth.normal_bf16(rng, (n_keys, H, 128))
+    v = synth.normal_bf16(rng, (n_keys, H, 128))
+    axes = []
+    for j in range(64 * 6 + 3, 64 * 6 + 9):
+        row = np.zeros((H, 128), np.float32)
+        row[:, (7 * j) % 128] = 40.0
+        axes.append((7 * j) % 128)
+        k[j] = synth.bf16_bits(row)
+    wl = _raw_cond_workload("longkeys", H, k, v)
+    L = Loaded(ws, wl)
+    try:
+        L.cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, splits)
+        qf = rng.standard_normal((n_q, H, 128)).astype(np.float32)
+        qf[:, :, axes] *= 0.25
+        q = synth.bf16_bits(qf)
+        pos = np.zeros((n_q, 3), np.int32)
+        got = L.run("video", q, pos, 0, (synth.KIND_COND,), mode=ws.WS_APPEND_RAW)
+        ref = L.oracle(q, pos, 0, (synth.KIND_COND,), mode=oracle.MODE_RAW)
+        assert_gates(got, ref, label=f"long keys, splits={splits}")
+    finally:
+        L.close()
+
+
+def test_video_tight_bound_shift(ws):
+    """Each query's dominant RAW key is 2x its own direction, so the logit
+    bound |q''| |k| is attained (about 33 in log2 units, under the fallback
+    limit): the bound shift then works at its tightest."""
+    rng = np.random.default_rng(22)
+    H, n_keys, n_q = 2, 64 * 7 + 30, 140
+    k = synth.normal_bf16(rng, (n_keys, H, 128))
+    v = synth.normal_bf16(rng, (n_keys, H, 128))
+    qf = rng.standard_normal((n_q, H, 128)).astype(np.float32)
+    qf /= np.sqrt((qf * qf).mean(-1, keepdims=True))
+    q = synth.bf16_bits(qf)
+    needle = (np.arange(n_q) * 29 + 3) % n_keys
+    for i, j in enumerate(needle):
+        k[j] = synth.bf16_bits(2.0 * synth.bf16_to_f32(q[i]))
+    wl = _raw_cond_workload("tight", H, k, v)
+    L = Loaded(ws, wl)
+    try:
+        pos = np.zeros((n_q, 3), np.int32)
+        got = L.run("video", q, pos, 0, (synth.KIND_COND,), mode=ws.WS_APPEND_RAW)
+        ref = L.oracle(q, pos, 0, (synth.KIND_COND,), mode=oracle.MODE_RAW)
+        assert_gates(got, ref, label="tight bound")
+    finally:
+        L.close()
