@@ -171,7 +171,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
 }
 
 // ------------------------------------------------------------------------- //
-// unit_attn (video): 4 waves x 32 queries, 64-key pages through LDS.
+// unit_attn (video): 8 waves x 32 queries, 64-key pages through LDS.
 //
 // Per wave and page, with lane l = 32*h + i (h = half, i = query column):
 //   S^T[key][q] = K[key][:] . Q'[q][:]   2 x (32x32) tiles, 8 MFMAs of k=16 each
@@ -183,17 +183,21 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
 // directly the B operands (eight consecutive keys) of the P*V MFMAs.
 // ------------------------------------------------------------------------- //
 __device__ __forceinline__ int swap23(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
-// LDS stages of the video kernel, rows padded by one 16-byte chunk:
-//   K    [64 rows][136]: key r is stored at row swap23(r), so lane i of either
-//        half reads row i (+32 for the second tile) and the eight lanes of a
-//        ds_read_b128 pass hit eight distinct 16-byte bank groups;
-//   V^T  [128 d][72].
-// With padding instead of an XOR swizzle every operand read of a page is one
-// base register plus an immediate offset.
-constexpr int kKRow = kHeadDim + 8;
-constexpr int kVRow = kPageTokens + 8;
-__shared__ __attribute__((aligned(16))) uint16_t g_vk[2][kPageTokens * kKRow];
-__shared__ __attribute__((aligned(16))) uint16_t g_vv[2][kHeadDim * kVRow];
+// LDS stages of the video kernel (three pages in flight), filled by direct
+// global->LDS loads (global_load_lds_dwordx4: lane l of a wave writes 16
+// bytes at base + 16 l).
+//   K    [64 rows][16 chunks]: row R holds key swap23(R); its logical chunk c
+//        (dims 8c..8c+7) sits at position c ^ (R & 15).  Lane i of either
+//        half then reads row i (+32 for the second tile), and the 16 lanes
+//        of a ds_read_b128 pass hit 16 distinct 16-byte bank groups.
+//   V^T  [128 d][8 chunks]: logical chunk c (keys 8c..8c+7) of row d sits at
+//        position c ^ ((d >> 1) & 7).
+__shared__ __attribute__((aligned(1024))) uint16_t g_k0[kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k1[kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k2[kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v0[kHeadDim * kPageTokens];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v1[kHeadDim * kPageTokens];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v2[kHeadDim * kPageTokens];
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -214,34 +218,59 @@ struct VideoCtx {
   const uint16_t* kpool;   // pool base + this head's tile offset
   const uint16_t* vpool;
   int64_t page_stride;     // elements per page (all heads)
-  int tid, half, l32, krow;
+  int wave, half, l32;
+  uint32_t dma_k, dma_v;   // this lane's source byte offsets within a tile (block i = 0)
   bf16x8 qreg[8];
 };
 
-// The 16 KB K (or V^T) tile of (page, head): thread t stages chunks
-// t + 256 i, i = 0..3 (coalesced 16-byte loads).
-__device__ __forceinline__ void stage_load(const VideoCtx& c, const uint16_t* pool, int page,
-                                           u32x4 (&st)[4]) {
-  const u32x4* src = reinterpret_cast<const u32x4*>(pool + page * c.page_stride);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) st[i] = src[c.tid + 256 * i];
+// LDS byte offset of a pointer into a __shared__ object.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p));
 }
 
-// Chunk t + 256 i of the K tile is row 16 i + t/16, 16-byte column t%16;
-// swap23 leaves bits 4-5 of the row alone, so the four stores are one base
-// plus immediate offsets.
-__device__ __forceinline__ void stage_store_k(const VideoCtx& c, uint16_t* dst, const u32x4 (&st)[4]) {
-  uint16_t* base = dst + swap23(c.tid >> 4) * kKRow + 8 * (c.tid & 15);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(base + 16 * i * kKRow) = st[i];
+// One direct load: each lane's 16 bytes at sbase + voff go to LDS at
+// lds + 16 * lane.  Written as inline asm: with the compiler's own LDS-DMA
+// intrinsic in flight, every later LDS read waits for lgkmcnt(0), which
+// serializes the MFMA operand reads.  M0 is restored afterwards; completion
+// is tracked by the explicit vmcnt wait in wait_dma.
+__device__ __forceinline__ void dma16(const uint16_t* sbase, uint32_t voff, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(sbase), "s"(lds)
+      : "memory");
 }
 
-// Chunk t + 256 i of the V^T tile is row (d) 32 i + t/8, column t%8.
-__device__ __forceinline__ void stage_store_v(const VideoCtx& c, uint16_t* dst, const u32x4 (&st)[4]) {
-  uint16_t* base = dst + (c.tid >> 3) * kVRow + 8 * (c.tid & 7);
+// Issues the direct loads of page `page` (K and V^T tiles of this head) into
+// the stage (k_dst, v_dst): per wave two 1 KB blocks of each, block
+// b = 8 i + wave.  Block b of K is rows 4b..4b+3, lane l at row
+// R = 32 i + 4 wave + l/16, position l%16; block b of V^T is rows
+// d = 64 i + 8 wave + l/8, position l%8.  In both, the lane's source offset
+// changes with i only by 4096 elements (8 KB).
+__device__ __forceinline__ void stage_dma(const VideoCtx& c, int page, uint16_t* k_dst, uint16_t* v_dst) {
+  const uint16_t* kp = c.kpool + page * c.page_stride;
+  const uint16_t* vp = c.vpool + page * c.page_stride;
+  const uint32_t kl = lds_offset(k_dst) + 1024 * c.wave, vl = lds_offset(v_dst) + 1024 * c.wave;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(base + 32 * i * kVRow) = st[i];
+  for (int i = 0; i < 2; ++i) {
+    dma16(kp + 4096 * i, c.dma_k, kl + 8192 * i);
+    dma16(vp + 4096 * i, c.dma_v, vl + 8192 * i);
+  }
 }
+constexpr int kDmaPerPage = 4;  // direct loads per wave and page
+
+// Waits for this wave's direct loads of the page after next's predecessor:
+// everything but the kDmaPerPage loads issued last (loads retire in order).
+// The barrier that follows then makes every wave's share visible.
+__device__ __forceinline__ void wait_dma_all_but_last_page() {
+  static_assert(kDmaPerPage == 4, "vmcnt encoding below");
+  __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt(4), expcnt(7), lgkmcnt(15)
+}
+__device__ __forceinline__ void wait_dma_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 // max over lanes l and l ^ 32 (v_permlane32_swap: no LDS round trip)
 __device__ __forceinline__ float pair_max(float v) {
@@ -284,22 +313,6 @@ __device__ __forceinline__ void scale_o(VideoState& st, float alpha) {
   for (int t4 = 0; t4 < 4; ++t4) st.o[t4] *= alpha;
 }
 
-// Issue pattern of a 32-key step: each MFMA followed by an operand read and a
-// share of the softmax VALU work, so that one wave keeps its matrix pipe busy
-// while it computes the exponentials of the neighbouring tile.
-// kLead operand reads go first, so that every MFMA finds its operand read
-// two MFMAs earlier.
-template <int kLead>
-__device__ __forceinline__ void interleave_mfma_valu() {
-  if (kLead > 0) __builtin_amdgcn_sched_group_barrier(0x100, kLead, 0);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-    __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
-  }
-}
-
 // Empty asm statements that make a value live in a register at this point:
 // they keep the compiler from sinking the speculative softmax past the rare
 // rescale branch, and a scalar page-list load from drifting next to its use.
@@ -307,23 +320,33 @@ __device__ __forceinline__ void pin_sgpr(int x) { asm volatile("" ::"s"(x)); }
 __device__ __forceinline__ void pin_vgpr(u32x4& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ void pin_vgpr(float& x) { asm volatile("" : "+v"(x)); }
 
+template <int kStage>
+__device__ __forceinline__ uint16_t* stage_k() { return kStage == 0 ? g_k0 : kStage == 1 ? g_k1 : g_k2; }
+template <int kStage>
+__device__ __forceinline__ uint16_t* stage_v() { return kStage == 0 ? g_v0 : kStage == 1 ? g_v1 : g_v2; }
+
+// Page list index of the page staged two pages ahead of pi (the range's
+// last page re-stages itself into the idle stage: nothing reads that copy).
+__device__ __forceinline__ int ahead2(int pi, int p_end) { return pi + 2 < p_end ? pi + 2 : p_end - 1; }
+
 // A page for a wave whose 32 query rows are all padding (ragged last query
-// tile): it only takes its share of staging page pi + 1.
-__device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi, int p_end, int cur) {
+// tile): it only issues its share of the loads of page pi + 2.
+template <int kCur>
+__device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi, int p_end) {
   pi = __builtin_amdgcn_readfirstlane(pi);
-  const int next_page = c.pages[pi + 1 < p_end ? pi + 1 : pi].x;
+  const int ahead = c.pages[ahead2(pi, p_end)].x;
   __syncthreads();
-  u32x4 stg[4];
-  stage_load(c, c.kpool, next_page, stg);
-  stage_store_k(c, g_vk[cur ^ 1], stg);
-  stage_load(c, c.vpool, next_page, stg);
-  stage_store_v(c, g_vv[cur ^ 1], stg);
+  stage_dma(c, ahead, stage_k<(kCur + 2) % 3>(), stage_v<(kCur + 2) % 3>());
+  wait_dma_all_but_last_page();
 }
 
-// One 64-key page from LDS stage `cur`, as two 32-key tiles (keys 0-31 in
-// s0, 32-63 in s1).  Order of issue:
-//   S tile 0 | S tile 1 + softmax of tile 0 | P*V tile 0 + softmax of tile 1
-//   | P*V tile 1
+// One 64-key page from LDS stage kCur, as two 32-key tiles (keys 0-31 in s0,
+// 32-63 in s1), scheduled by hand in 32 steps of one MFMA each:
+//   A: S tile 0                      B: S tile 1 + exp of tile 0
+//   D: P*V tile 0 + exp of tile 1    F: P*V tile 1
+// Each step issues the LDS operand read four steps ahead, its MFMA, and its
+// share of the softmax VALU work (two exponentials, one pack, one dot2), and
+// ends in a scheduling fence, so the emitted order is the program order.
 // The S accumulators start at -m_run (or -inf past the page's valid tokens),
 // so they hold the exp2 argument directly.
 //   kLazy = false: m_run is a fixed upper bound of the row's logits (from the
@@ -331,29 +354,25 @@ __device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi,
 //   kLazy = true: m_run is a running maximum raised lazily.  The
 //     exponentials are taken speculatively against the current m_run; when a
 //     tile raises it by more than kLazyTau (rare after the first tile), a
-//     branch outside the interleaved regions rescales O and l and recomputes
-//     that tile's P.
-// While the page is computed, page pi + 1 is staged through registers into
-// the other stage: its K after S, its V^T after P*V.  One barrier per page.
-template <bool kLazy>
-__device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, int pi, int p_end,
-                                           int cur) {
-  const uint16_t* sk = g_vk[cur];
-  const uint16_t* sv = g_vv[cur];
+//     branch between the phases rescales O and l and recomputes that tile's P.
+// Right after the page's barrier, the direct loads of page pi + 2 into the
+// stage freed by page pi - 1 are issued; at the end of the page each wave
+// waits for its loads of page pi + 1 (issued one page earlier), so every
+// load has two pages to land.  One barrier per page.
+template <bool kLazy, int kCur>
+__device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, int pi, int p_end) {
+  const uint16_t* sk = stage_k<kCur>();
+  const uint16_t* sv = stage_v<kCur>();
   pi = __builtin_amdgcn_readfirstlane(pi);
   const int n_valid = c.pages[pi].y;
-  // the last page of the range re-stages itself into the idle stage, which
-  // keeps the staging free of branches (nothing reads that copy)
-  const int next_page = c.pages[pi + 1 < p_end ? pi + 1 : pi].x;
+  const int ahead = c.pages[ahead2(pi, p_end)].x;
   // both scalars are loaded before the barrier: a scalar load left for later
   // would share lgkmcnt with the LDS operand reads
   pin_sgpr(n_valid);
   __syncthreads();
-  u32x4 stg[4];
-  stage_load(c, c.kpool, next_page, stg);
-  // keep the staging loads here, ahead of the MFMAs that hide their latency
+  stage_dma(c, ahead, stage_k<(kCur + 2) % 3>(), stage_v<(kCur + 2) % 3>());
   __builtin_amdgcn_sched_barrier(0);
-  const int half = c.half, krow = c.krow;
+  const int half = c.half, l32 = c.l32;
 
   const float neg_m = -st.m_run;
   f32x16 s0, s1;
@@ -371,50 +390,70 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
     for (int r = 0; r < 16; ++r)
       if (16 * (r >> 3) + (r & 7) >= lim) sc[r] = kNegInf;
   };
-
-  // K operands are read two MFMAs ahead
-  auto kread = [&](int s, int row) {
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kKRow + 8 * (2 * s + half)));
+  // operand of S step n (n < 8: tile 0, else tile 1) and of P*V step n
+  // (d tile n % 4, key chunk n / 4)
+  auto kread = [&](int n) {
+    const int row = n < 8 ? l32 : 32 + l32;
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kHeadDim + 8 * ((2 * (n & 7) + half) ^ (l32 & 15))));
   };
-  bf16x8 k0 = kread(0, krow), k1 = kread(1, krow);
+  auto vread = [&](int n) {
+    const int d = 32 * (n & 3) + l32;
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kPageTokens + 8 * ((2 * (n >> 2) + half) ^ ((l32 >> 1) & 7))));
+  };
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  // two exponentials of tile register pair n, packed to bf16 (word n of P),
+  // added to the row sum
+  auto exp_pair = [&](const f32x16& sc, int n, float& l) {
+    // bit-cast a scalar temporary: a bit-cast of a vector element subscript
+    // is lowered to element 0 by this compiler
+    const uint32_t w = pack_bf16(fast_exp2(sc[2 * n]), fast_exp2(sc[2 * n + 1]));
+    l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, l, false);
+    return w;
+  };
+
+  // Operand reads run kAhead MFMA steps ahead of their use, through a ring of
+  // kAhead + 1 registers: S steps 0-15 (kread), then P*V steps 0-15 (vread).
+  constexpr int kAhead = 4;
+  auto oread = [&](int n) { return n < 16 ? kread(n) : vread(n - 16); };
+  bf16x8 ring[kAhead + 1];
 #pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    const bf16x8 k = k0;
-    k0 = k1;
-    k1 = kread((s + 2) & 7, s + 2 < 8 ? krow : 32 + krow);
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, c.qreg[s], s0, 0, 0, 0);
-  }
+  for (int n = 0; n < kAhead; ++n) ring[n] = oread(n);
+  auto next_operand = [&](int n) {  // operand of step n; issues the read of step n + kAhead
+    if (n + kAhead < 32) ring[(n + kAhead) % (kAhead + 1)] = oread(n + kAhead);
+    return ring[n % (kAhead + 1)];
+  };
+
+  // ---- A: S tile 0 ----
   __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int n = 0; n < 8; ++n) {
+    const bf16x8 k = next_operand(n);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, c.qreg[n], s0, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   if (tail) mask_tail(s0, 0);
   __builtin_amdgcn_sched_barrier(0);
 
-  // S tile 1; softmax of tile 0 in its shadow
+  // ---- B: S tile 1, exponentials of tile 0 ----
   u32x4 p0a, p0b;
-  float mx0 = 0.f, l0;
+  float l0 = 0.f, mx0 = 0.f;
 #pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    const bf16x8 k = k0;
-    k0 = k1;
-    if (s < 6) k1 = kread(s + 2, 32 + krow);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, c.qreg[s], s1, 0, 0, 0);
-    if (s == 0) {
-      if constexpr (kLazy) mx0 = pair_max(max16(s0));
-      l0 = exp_tile(s0, p0a, p0b);
-    }
+  for (int n = 0; n < 8; ++n) {
+    const bf16x8 k = next_operand(8 + n);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, c.qreg[n], s1, 0, 0, 0);
+    if (kLazy && n == 0) mx0 = pair_max(max16(s0));
+    const uint32_t w = exp_pair(s0, n, l0);
+    if (n < 4) p0a[n] = w; else p0b[n - 4] = w;
+    __builtin_amdgcn_sched_barrier(0);
   }
   // d0: shift of the running maximum taken at tile 0 (0 for most rows)
   const bool need0 = kLazy && (st.first || mx0 > kLazyTau);
-  float d0 = need0 ? mx0 : 0.f;
+  const float d0 = need0 ? mx0 : 0.f;
+  // keep the exponentials in the MFMA shadow they were scheduled in (the
+  // compiler would otherwise sink them past the branches below)
   pin_vgpr(p0a);
   pin_vgpr(p0b);
   pin_vgpr(l0);
-  if constexpr (kLazy) pin_vgpr(d0);
-  interleave_mfma_valu<0>();
-  __builtin_amdgcn_sched_barrier(0);
-  stage_store_k(c, g_vk[cur ^ 1], stg);
-  stage_load(c, c.vpool, next_page, stg);
-  __builtin_amdgcn_sched_barrier(0);
-
   if constexpr (kLazy) {
     if (__any(need0)) {
       const float alpha = fast_exp2(-d0);
@@ -431,36 +470,25 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   if (tail) mask_tail(s1, 32);
   __builtin_amdgcn_sched_barrier(0);
 
-  // O^T += V^T P^T for tile 0; softmax of tile 1 in its shadow
-  auto vread = [&](int t4, int jc) {
-    const int d = 32 * t4 + c.l32;
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kVRow + 8 * (2 * jc + half)));
-  };
-  bf16x8 v0 = vread(0, 0), v1 = vread(1, 0);
+  // ---- D: P*V tile 0, exponentials of tile 1 ----
   u32x4 p1a, p1b;
-  float mx1 = 0.f, l1;
+  float l1 = 0.f, mx1 = 0.f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const bf16x8 v = v0;
-    v0 = v1;
-    v1 = vread((j + 2) & 3, (j + 2) >> 2);
-    const int t4 = j & 3;
-    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(j < 4 ? p0a : p0b), st.o[t4], 0, 0, 0);
-    if (j == 0) {
-      if constexpr (kLazy) mx1 = pair_max(max16(s1));
-      l1 = exp_tile(s1, p1a, p1b);
-    }
+  for (int n = 0; n < 8; ++n) {
+    const bf16x8 v = next_operand(16 + n);
+    const int t4 = n & 3;
+    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(n < 4 ? p0a : p0b), st.o[t4], 0, 0, 0);
+    if (kLazy && n == 0) mx1 = pair_max(max16(s1));
+    const uint32_t w = exp_pair(s1, n, l1);
+    if (n < 4) p1a[n] = w; else p1b[n - 4] = w;
+    __builtin_amdgcn_sched_barrier(0);
   }
   // d1: shift of tile 1 relative to the page's starting maximum
   const bool need1 = kLazy && mx1 - d0 > kLazyTau;
-  float d1 = need1 ? mx1 : d0;
+  const float d1 = need1 ? mx1 : d0;
   pin_vgpr(p1a);
   pin_vgpr(p1b);
   pin_vgpr(l1);
-  if constexpr (kLazy) pin_vgpr(d1);
-  interleave_mfma_valu<2>();
-  __builtin_amdgcn_sched_barrier(0);
-
   if constexpr (kLazy) {
     if (__any(d1 != 0.f)) {
       const float e = d1 - d0;
@@ -474,20 +502,20 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
     }
   }
   st.l_run += l1;
+  __builtin_amdgcn_sched_barrier(0);
 
-  // O^T += V^T P^T for tile 1
+  // ---- F: P*V tile 1 ----
 #pragma unroll
-  for (int j = 8; j < 16; ++j) {
-    const bf16x8 v = v0;
-    v0 = v1;
-    if (j < 14) v1 = vread((j + 2) & 3, (j + 2) >> 2);
-    const int t4 = j & 3;
-    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(j < 12 ? p1a : p1b), st.o[t4], 0, 0, 0);
+  for (int n = 8; n < 16; ++n) {
+    const bf16x8 v = next_operand(16 + n);
+    const int t4 = n & 3;
+    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(n < 12 ? p1a : p1b), st.o[t4], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  stage_store_v(c, g_vv[cur ^ 1], stg);
+  wait_dma_all_but_last_page();
 }
 
-__global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
+__global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -511,11 +539,16 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
   c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
   c.kpool = a.kpool + head * kPageHeadElems;
   c.vpool = a.vpool + head * kPageHeadElems;
-  c.tid = tid;
   c.active = qtile * kVideoQTile + wave * 32 < a.n_q;
+  c.wave = wave;
   c.half = half;
   c.l32 = l32;
-  c.krow = l32;  // LDS row l32 holds key swap23(l32)
+  {
+    const int r0 = 4 * wave + (lane >> 4);  // K row of block i = 0
+    c.dma_k = 2 * (swap23(r0) * kHeadDim + 8 * ((lane & 15) ^ (r0 & 15)));
+    const int d0 = 8 * wave + (lane >> 3);  // V^T row of block i = 0
+    c.dma_v = 2 * (d0 * kPageTokens + 8 * ((lane & 7) ^ ((d0 >> 1) & 7)));
+  }
 
   // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
   const int q = qtile * kVideoQTile + wave * 32 + l32;
@@ -603,29 +636,31 @@ __global__ __launch_bounds__(256, 2) void unit_attn_kernel(const AttnArgs a) {
   st.first = true;
 
   if (p_begin < p_end) {
-    u32x4 stg[4];
-    const int page = a.pages[p_begin].x;
-    stage_load(c, c.kpool, page, stg);
-    stage_store_k(c, g_vk[0], stg);
-    stage_load(c, c.vpool, page, stg);
-    stage_store_v(c, g_vv[0], stg);
+    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[p_begin].x), g_k0, g_v0);
+    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 1, p_end - 1)].x), g_k1, g_v1);
+    wait_dma_all_but_last_page();
   }
   if (c.active && fixed_shift) {
-    for (int pi = p_begin; pi < p_end; pi += 2) {
-      video_page<false>(c, st, pi, p_end, 0);
-      if (pi + 1 < p_end) video_page<false>(c, st, pi + 1, p_end, 1);
+    for (int pi = p_begin; pi < p_end; pi += 3) {
+      video_page<false, 0>(c, st, pi, p_end);
+      if (pi + 1 < p_end) video_page<false, 1>(c, st, pi + 1, p_end);
+      if (pi + 2 < p_end) video_page<false, 2>(c, st, pi + 2, p_end);
     }
   } else if (c.active) {
-    for (int pi = p_begin; pi < p_end; pi += 2) {
-      video_page<true>(c, st, pi, p_end, 0);
-      if (pi + 1 < p_end) video_page<true>(c, st, pi + 1, p_end, 1);
+    for (int pi = p_begin; pi < p_end; pi += 3) {
+      video_page<true, 0>(c, st, pi, p_end);
+      if (pi + 1 < p_end) video_page<true, 1>(c, st, pi + 1, p_end);
+      if (pi + 2 < p_end) video_page<true, 2>(c, st, pi + 2, p_end);
     }
   } else {
-    for (int pi = p_begin; pi < p_end; pi += 2) {
-      video_page_stage_only(c, pi, p_end, 0);
-      if (pi + 1 < p_end) video_page_stage_only(c, pi + 1, p_end, 1);
+    for (int pi = p_begin; pi < p_end; pi += 3) {
+      video_page_stage_only<0>(c, pi, p_end);
+      if (pi + 1 < p_end) video_page_stage_only<1>(c, pi + 1, p_end);
+      if (pi + 2 < p_end) video_page_stage_only<2>(c, pi + 2, p_end);
     }
   }
+  // no direct load may still be writing this workgroup's LDS when it exits
+  wait_dma_all();
 
   // ---- epilogue: lane holds O^T[32t + 8g + 4h + i][q], g = r/4, i = r%4 ----
   const float l_tot = st.l_run + __shfl_xor(st.l_run, 32);
@@ -905,7 +940,7 @@ hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
 
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream) {
   dim3 grid(a.n_qtiles * a.num_heads * a.n_splits);
-  hipLaunchKernelGGL(unit_attn_kernel, grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(unit_attn_kernel, grid, dim3(kVideoWaves * 64), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -93,13 +93,14 @@ struct CombineArgs {
 };
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
-// Video path: 128-query tiles on 4 waves, 32x32x16 bf16 MFMA, LDS-staged pages.
+// Video path: 256-query tiles on 8 waves, 32x32x16 bf16 MFMA, LDS-staged pages.
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
 // Audio path: one wave per (head, key range), 16x16x32 bf16 MFMA, no LDS.
 hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 
-constexpr int kVideoQTile = 128;
+constexpr int kVideoQTile = 256;
+constexpr int kVideoWaves = kVideoQTile / 32;
 constexpr int kAudioQTile = 16;
 
 }  // namespace ws
