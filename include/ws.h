@@ -223,6 +223,30 @@ WS_API ws_status ws_cache_check(ws_cache* cache, uint32_t* flags);
 /* Sets a tuning knob (see ws_option); value 0 restores the automatic choice. */
 WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t value);
 
+/* Launch timing of the attention entry points (for benchmarks and
+ * profilers).  While enabled, every ws_unit_attention / ws_audio_attention
+ * call records three HIP events on its own stream: before its attention
+ * kernel, between that kernel and the split-KV merge kernel, and after the
+ * merge.  The cache keeps the events of the last `capacity` calls in a ring
+ * (older calls are overwritten); recording adds no synchronization. */
+typedef struct ws_call_timing {
+  int32_t path;      /* 0 = ws_unit_attention (video), 1 = ws_audio_attention */
+  int32_t n_splits;  /* key-range splits of the call (1 = video without merge) */
+  float attn_us;     /* attention kernel, microseconds */
+  float merge_us;    /* merge kernel, microseconds (0 when there is none) */
+} ws_call_timing;
+
+/* capacity > 0 (at most 65536) enables timing with a ring of that many calls
+ * (creating 3 * capacity HIP events on the cache's device) and clears it;
+ * capacity = 0 disables timing and destroys the events. */
+WS_API ws_status ws_cache_timing_enable(ws_cache* cache, int32_t capacity);
+
+/* Waits for the recorded calls, copies up to `max` of them into out[] (host
+ * array owned by the caller, oldest call first), stores the count in *n and
+ * clears the ring.  WS_ERR_INVALID_ARG if timing is not enabled. */
+WS_API ws_status ws_cache_timing_read(ws_cache* cache, ws_call_timing* out, int32_t max,
+                                      int32_t* n);
+
 /* Thread-local message for the last non-OK status ("" if none). */
 WS_API const char* ws_last_error(void);
 

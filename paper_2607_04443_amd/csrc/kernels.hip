@@ -183,21 +183,25 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
 // directly the B operands (eight consecutive keys) of the P*V MFMAs.
 // ------------------------------------------------------------------------- //
 __device__ __forceinline__ int swap23(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
-// LDS stages of the video kernel (three pages in flight), filled by direct
-// global->LDS loads (global_load_lds_dwordx4: lane l of a wave writes 16
-// bytes at base + 16 l).
+// LDS stages of the video kernel (a ring of four pages: the previous page,
+// whose V^T the pipelined schedule still reads, the current page, and the
+// next two in flight), filled by direct global->LDS loads
+// (global_load_lds_dwordx4: lane l of a wave writes 16 bytes at base + 16 l).
 //   K    [64 rows][16 chunks]: row R holds key swap23(R); its logical chunk c
 //        (dims 8c..8c+7) sits at position c ^ (R & 15).  Lane i of either
 //        half then reads row i (+32 for the second tile), and the 16 lanes
 //        of a ds_read_b128 pass hit 16 distinct 16-byte bank groups.
 //   V^T  [128 d][8 chunks]: logical chunk c (keys 8c..8c+7) of row d sits at
 //        position c ^ ((d >> 1) & 7).
+constexpr int kStages = 4;
 __shared__ __attribute__((aligned(1024))) uint16_t g_k0[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_k1[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_k2[kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k3[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v0[kHeadDim * kPageTokens];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v1[kHeadDim * kPageTokens];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v2[kHeadDim * kPageTokens];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v3[kHeadDim * kPageTokens];
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -321,9 +325,16 @@ __device__ __forceinline__ void pin_vgpr(u32x4& x) { asm volatile("" : "+v"(x));
 __device__ __forceinline__ void pin_vgpr(float& x) { asm volatile("" : "+v"(x)); }
 
 template <int kStage>
-__device__ __forceinline__ uint16_t* stage_k() { return kStage == 0 ? g_k0 : kStage == 1 ? g_k1 : g_k2; }
+__device__ __forceinline__ uint16_t* stage_k() {
+  return kStage == 0 ? g_k0 : kStage == 1 ? g_k1 : kStage == 2 ? g_k2 : g_k3;
+}
 template <int kStage>
-__device__ __forceinline__ uint16_t* stage_v() { return kStage == 0 ? g_v0 : kStage == 1 ? g_v1 : g_v2; }
+__device__ __forceinline__ uint16_t* stage_v() {
+  return kStage == 0 ? g_v0 : kStage == 1 ? g_v1 : kStage == 2 ? g_v2 : g_v3;
+}
+__device__ __forceinline__ const uint16_t* stage_v_at(int stage) {
+  return stage == 0 ? g_v0 : stage == 1 ? g_v1 : stage == 2 ? g_v2 : g_v3;
+}
 
 // Page list index of the page staged two pages ahead of pi (the range's
 // last page re-stages itself into the idle stage: nothing reads that copy).
@@ -336,7 +347,7 @@ __device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi,
   pi = __builtin_amdgcn_readfirstlane(pi);
   const int ahead = c.pages[ahead2(pi, p_end)].x;
   __syncthreads();
-  stage_dma(c, ahead, stage_k<(kCur + 2) % 3>(), stage_v<(kCur + 2) % 3>());
+  stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
   wait_dma_all_but_last_page();
 }
 
@@ -370,7 +381,7 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   // would share lgkmcnt with the LDS operand reads
   pin_sgpr(n_valid);
   __syncthreads();
-  stage_dma(c, ahead, stage_k<(kCur + 2) % 3>(), stage_v<(kCur + 2) % 3>());
+  stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, l32 = c.l32;
 
@@ -515,6 +526,170 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   wait_dma_all_but_last_page();
 }
 
+// Fixed-shift pages, software-pipelined across pages so that every group of
+// eight MFMAs carries eight exponentials (the softmax VALU then runs in the
+// shadow of the matrix pipe throughout, instead of piling up in two phases).
+// Iteration p (page p from LDS stage kCur, V^T of page p-1 from the stage
+// before it), 32 MFMA steps with operand reads four steps ahead:
+//   steps  0- 7  S tile 0 of p                 exp: tile 1 of p-1, keys 0-15
+//   steps  8-11  P*V of p-1, key chunk 2       exp: tile 1 of p-1, keys 16-31
+//   steps 12-15  S tile 1 of p, k-steps 0-3      (same)
+//   steps 16-19  P*V of p-1, key chunk 3       exp: tile 0 of p, keys 0-15
+//   steps 20-23  S tile 1 of p, k-steps 4-7      (same)
+//   steps 24-27  P*V of p, key chunk 0         exp: tile 0 of p, keys 16-31
+//   steps 28-31  P*V of p, key chunk 1
+// ("keys 0-15" of a tile are its accumulator registers 0-7 in both lane
+// halves, i.e. key chunk 0 or 2 of the page.)  The first page of a range
+// (kFirst) has no page p-1: steps 0-7 S tile 0, 8-15 S tile 1 with the
+// exponentials of tile 0 keys 0-15, 16-23 P*V chunks 0-1 with those of keys
+// 16-31.  Tile 1 of the last page is finished by video_flush.
+struct PipeState {
+  f32x16 s1;      // S tile 1 of the previous page (exp2 argument, masked)
+};
+
+template <int kCur, bool kFirst>
+__device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, PipeState& ps, int pi,
+                                           int p_end) {
+  constexpr int kPrev = (kCur + kStages - 1) % kStages;
+  const uint16_t* sk = stage_k<kCur>();
+  const uint16_t* sv = stage_v<kCur>();
+  const uint16_t* svp = stage_v<kPrev>();
+  pi = __builtin_amdgcn_readfirstlane(pi);
+  const int n_valid = c.pages[pi].y;
+  const int ahead = c.pages[ahead2(pi, p_end)].x;
+  pin_sgpr(n_valid);
+  __syncthreads();
+  stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
+  __builtin_amdgcn_sched_barrier(0);
+  const int half = c.half, l32 = c.l32;
+  const bool tail = n_valid < kPageTokens;
+  auto mask_tail = [&](f32x16& sc, int key0) {
+    const int lim = n_valid - key0 - 8 * half;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (16 * (r >> 3) + (r & 7) >= lim) sc[r] = kNegInf;
+  };
+  auto kread = [&](int n) {  // S k-step n % 8 of tile n / 8
+    const int row = n < 8 ? l32 : 32 + l32;
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kHeadDim + 8 * ((2 * (n & 7) + half) ^ (l32 & 15))));
+  };
+  auto vread = [&](const uint16_t* v, int t4, int jc) {  // d tile t4, key chunk jc
+    const int d = 32 * t4 + l32;
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(v + d * kPageTokens + 8 * ((2 * jc + half) ^ ((l32 >> 1) & 7))));
+  };
+  constexpr int kSteps = kFirst ? 24 : 32;
+  auto oread = [&](int o) {
+    if (kFirst) return o < 16 ? kread(o) : vread(sv, (o - 16) & 3, (o - 16) >> 2);
+    if (o < 8) return kread(o);
+    if (o < 12) return vread(svp, o - 8, 2);
+    if (o < 16) return kread(8 + o - 12);
+    if (o < 20) return vread(svp, o - 16, 3);
+    if (o < 24) return kread(12 + o - 20);
+    return vread(sv, (o - 24) & 3, (o - 24) >> 2);
+  };
+  constexpr int kAhead = 4;
+  bf16x8 ring[kAhead + 1];
+#pragma unroll
+  for (int o = 0; o < kAhead; ++o) ring[o] = oread(o);
+  __builtin_amdgcn_sched_barrier(0);
+
+  const float neg_m = -st.m_run;
+  f32x16 s0, s1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    s0[r] = neg_m;
+    s1[r] = neg_m;
+  }
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  float l = 0.f;
+  // P words: w[0..3] keys 0-15 of a tile (chunk 0 or 2), w[4..7] keys 16-31
+  u32x4 pp2, pp3, p0, p1;  // tile 1 of p-1 (chunks 2, 3); tile 0 of p (chunks 0, 1)
+  float e_lo = 0.f;        // first exponential of a pair, waiting for its partner
+  auto exp_one = [&](const f32x16& sc, int r, u32x4& dst, int word) {
+    const float e = fast_exp2(sc[r]);
+    if ((r & 1) == 0) {
+      e_lo = e;
+    } else {
+      // bit-cast a scalar temporary: a bit-cast of a vector element subscript
+      // is lowered to element 0 by this compiler
+      const uint32_t w = pack_bf16(e_lo, e);
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, l, false);
+      dst[word] = w;
+    }
+  };
+
+#pragma unroll
+  for (int o = 0; o < kSteps; ++o) {
+    if (o + kAhead < kSteps) ring[(o + kAhead) % (kAhead + 1)] = oread(o + kAhead);
+    const bf16x8 a = ring[o % (kAhead + 1)];
+    if (kFirst) {
+      if (o < 8) {
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], s0, 0, 0, 0);
+      } else if (o < 16) {
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 8], s1, 0, 0, 0);
+        exp_one(s0, o - 8, p0, (o - 8) >> 1);
+      } else if (o < 20) {
+        st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p0), st.o[o - 16], 0, 0, 0);
+        exp_one(s0, 8 + 2 * (o - 16), p1, o - 16);
+        exp_one(s0, 9 + 2 * (o - 16), p1, o - 16);
+      } else {
+        st.o[o - 20] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p1), st.o[o - 20], 0, 0, 0);
+      }
+    } else {
+      if (o < 8) {
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], s0, 0, 0, 0);
+        exp_one(ps.s1, o, pp2, o >> 1);
+      } else if (o < 12) {
+        st.o[o - 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp2), st.o[o - 8], 0, 0, 0);
+        exp_one(ps.s1, 8 + o - 8, pp3, (o - 8) >> 1);
+      } else if (o < 16) {
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 12], s1, 0, 0, 0);
+        exp_one(ps.s1, 8 + o - 8, pp3, (o - 8) >> 1);
+      } else if (o < 20) {
+        st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp3), st.o[o - 16], 0, 0, 0);
+        exp_one(s0, o - 16, p0, (o - 16) >> 1);
+      } else if (o < 24) {
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[4 + o - 20], s1, 0, 0, 0);
+        exp_one(s0, o - 16, p0, (o - 16) >> 1);
+      } else if (o < 28) {
+        st.o[o - 24] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p0), st.o[o - 24], 0, 0, 0);
+        exp_one(s0, 8 + 2 * (o - 24), p1, o - 24);
+        exp_one(s0, 9 + 2 * (o - 24), p1, o - 24);
+      } else {
+        st.o[o - 28] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p1), st.o[o - 28], 0, 0, 0);
+      }
+    }
+    // the tile-0 exponentials start after step 7 (kFirst) or 15: mask the
+    // page tail first (waits for the S tile 0 MFMAs on tail pages only)
+    if (o == 7) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (tail) mask_tail(s0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  st.l_run += l;
+  if (tail) mask_tail(s1, 32);
+  ps.s1 = s1;
+  wait_dma_all_but_last_page();
+}
+
+// Finishes tile 1 of the range's last page (V^T in LDS stage `stage`).
+__device__ __forceinline__ void video_flush(const VideoCtx& c, VideoState& st, const PipeState& ps,
+                                            int stage) {
+  const uint16_t* sv = stage_v_at(stage);
+  const int half = c.half, l32 = c.l32;
+  u32x4 pa, pb;
+  st.l_run += exp_tile(ps.s1, pa, pb);
+#pragma unroll
+  for (int n = 0; n < 8; ++n) {
+    const int t4 = n & 3, jc = 2 + (n >> 2);
+    const int d = 32 * t4 + l32;
+    const bf16x8 v =
+        as_bf16x8(*reinterpret_cast<const u32x4*>(sv + d * kPageTokens + 8 * ((2 * jc + half) ^ ((l32 >> 1) & 7))));
+    st.o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, as_bf16x8(n < 4 ? pa : pb), st.o[t4], 0, 0, 0);
+  }
+}
+
 __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -641,22 +816,30 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
     wait_dma_all_but_last_page();
   }
   if (c.active && fixed_shift) {
-    for (int pi = p_begin; pi < p_end; pi += 3) {
-      video_page<false, 0>(c, st, pi, p_end);
-      if (pi + 1 < p_end) video_page<false, 1>(c, st, pi + 1, p_end);
-      if (pi + 2 < p_end) video_page<false, 2>(c, st, pi + 2, p_end);
+    if (p_begin < p_end) {
+      PipeState ps;
+      video_iter<0, true>(c, st, ps, p_begin, p_end);
+      for (int pi = p_begin + 1; pi < p_end; pi += 4) {
+        video_iter<1, false>(c, st, ps, pi, p_end);
+        if (pi + 1 < p_end) video_iter<2, false>(c, st, ps, pi + 1, p_end);
+        if (pi + 2 < p_end) video_iter<3, false>(c, st, ps, pi + 2, p_end);
+        if (pi + 3 < p_end) video_iter<0, false>(c, st, ps, pi + 3, p_end);
+      }
+      video_flush(c, st, ps, (p_end - 1 - p_begin) % kStages);
     }
   } else if (c.active) {
-    for (int pi = p_begin; pi < p_end; pi += 3) {
+    for (int pi = p_begin; pi < p_end; pi += 4) {
       video_page<true, 0>(c, st, pi, p_end);
       if (pi + 1 < p_end) video_page<true, 1>(c, st, pi + 1, p_end);
       if (pi + 2 < p_end) video_page<true, 2>(c, st, pi + 2, p_end);
+      if (pi + 3 < p_end) video_page<true, 3>(c, st, pi + 3, p_end);
     }
   } else {
-    for (int pi = p_begin; pi < p_end; pi += 3) {
+    for (int pi = p_begin; pi < p_end; pi += 4) {
       video_page_stage_only<0>(c, pi, p_end);
       if (pi + 1 < p_end) video_page_stage_only<1>(c, pi + 1, p_end);
       if (pi + 2 < p_end) video_page_stage_only<2>(c, pi + 2, p_end);
+      if (pi + 3 < p_end) video_page_stage_only<3>(c, pi + 3, p_end);
     }
   }
   // no direct load may still be writing this workgroup's LDS when it exits

@@ -47,6 +47,14 @@ constexpr int kMaxVideoSplits = 8;
 constexpr int kMaxAudioSplits = 512;
 constexpr int kMaxAudioQ = 64;
 
+struct TimingRing {
+  int32_t cap = 0;
+  int32_t next = 0;   // slot of the next call
+  int32_t count = 0;  // recorded calls, <= cap
+  std::vector<hipEvent_t> ev;  // 3 per slot
+  std::vector<ws_call_timing> meta;
+};
+
 struct ListCacheEntry {
   bool valid = false;
   ws::MaskSpec mask{};
@@ -81,6 +89,7 @@ struct ws_cache {
   int32_t opt_running_max = 0;
   float* knorm2 = nullptr;  // [max_pages][H] squared key-norm maxima
   std::vector<ws::PageRef> scratch_list;
+  TimingRing timing;
 
   ws_cache(int32_t page_tokens, int32_t max_pages) : pt(page_tokens, max_pages) {}
 };
@@ -201,7 +210,13 @@ ws_status fill_rope(ws_cache* c) {
   return WS_OK;
 }
 
+void timing_free(ws_cache* c) {
+  for (hipEvent_t e : c->timing.ev) (void)hipEventDestroy(e);
+  c->timing = TimingRing{};
+}
+
 void free_all(ws_cache* c) {
+  timing_free(c);
   if (c->kpool) (void)hipFree(c->kpool);
   if (c->vpool) (void)hipFree(c->vpool);
   if (c->rope_dev) (void)hipFree(c->rope_dev);
@@ -286,18 +301,24 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
 
 int choose_video_splits(const ws_cache* c, int n_items, int n_pages) {
   if (c->opt_video_splits > 0) return c->opt_video_splits;
-  // Few work items (small head counts / unit sizes): split until the grid
-  // fills two workgroups per CU, keeping >= 4 pages per split.
-  if (n_items < c->num_cus) {
-    int s = 1;
-    while (s < kMaxVideoSplits && static_cast<int64_t>(n_items) * s < 2LL * c->num_cus &&
-           n_pages >= 4 * (s + 1))
-      ++s;
-    return s;
+  // One workgroup per CU: a split count s runs in ceil(items * s / CUs)
+  // rounds of ceil(pages / s) pages each, plus a fixed per-item cost (query
+  // prologue, pipeline fill, partial write-back and merge) worth about ten
+  // pages (measured on MI355X for 1..33 history units of 920 tokens x 40
+  // heads).  Pick the s with the smallest estimate.
+  constexpr int64_t kItemCostPages = 10;
+  int best = 1;
+  int64_t best_cost = -1;
+  for (int s = 1; s <= kMaxVideoSplits; ++s) {
+    const int64_t rounds = (static_cast<int64_t>(n_items) * s + c->num_cus - 1) / c->num_cus;
+    const int64_t cost = rounds * ((n_pages + s - 1) / s + kItemCostPages);
+    if (best_cost < 0 || cost < best_cost) {
+      best = s;
+      best_cost = cost;
+    }
+    if (s >= n_pages) break;
   }
-  // Many items: up to 4 splits of >= 32 pages each (measured best on MI355X
-  // for 1..33 history units of 920 tokens x 40 heads).
-  return std::max(1, std::min(4, n_pages / 32));
+  return best;
 }
 
 int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
@@ -373,8 +394,15 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   a.n_splits = splits;
   a.pages_per_split = pps;
 
+  TimingRing& tr = c->timing;
+  const int slot = tr.cap > 0 ? tr.next : -1;
+  if (slot >= 0) {
+    tr.meta[slot] = ws_call_timing{audio ? 1 : 0, splits, 0.f, 0.f};
+    WS_HIP(hipEventRecord(tr.ev[3 * slot], stream));
+  }
   hipError_t e = audio ? ws::launch_audio_attention(a, stream) : ws::launch_unit_attention(a, stream);
   if (e != hipSuccess) return hip_fail(e, audio ? "audio_attn launch" : "unit_attn launch");
+  if (slot >= 0) WS_HIP(hipEventRecord(tr.ev[3 * slot + 1], stream));
   if (audio || splits > 1) {
     ws::CombineArgs cb{};
     cb.part_o = c->part_o;
@@ -387,6 +415,11 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
     cb.out_head_stride = out_head_stride;
     e = ws::launch_combine(cb, stream);
     if (e != hipSuccess) return hip_fail(e, "combine launch");
+  }
+  if (slot >= 0) {
+    WS_HIP(hipEventRecord(tr.ev[3 * slot + 2], stream));
+    tr.next = (tr.next + 1) % tr.cap;
+    tr.count = std::min(tr.count + 1, tr.cap);
   }
   return WS_OK;
 }
@@ -591,6 +624,49 @@ ws_status ws_cache_set_option(ws_cache* c, ws_option opt, int32_t value) {
       return WS_OK;
   }
   return fail(WS_ERR_INVALID_ARG, "unknown option %d", static_cast<int>(opt));
+}
+
+ws_status ws_cache_timing_enable(ws_cache* c, int32_t capacity) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  if (capacity < 0 || capacity > 65536) return fail(WS_ERR_INVALID_ARG, "timing capacity out of range");
+  if (ws_status st = check_device(c); st != WS_OK) return st;
+  timing_free(c);
+  if (capacity == 0) return WS_OK;
+  TimingRing& tr = c->timing;
+  tr.ev.reserve(3 * static_cast<size_t>(capacity));
+  for (int i = 0; i < 3 * capacity; ++i) {
+    hipEvent_t e;
+    hipError_t he = hipEventCreate(&e);
+    if (he != hipSuccess) {
+      timing_free(c);
+      return hip_fail(he, "hipEventCreate");
+    }
+    tr.ev.push_back(e);
+  }
+  tr.meta.assign(static_cast<size_t>(capacity), ws_call_timing{});
+  tr.cap = capacity;
+  return WS_OK;
+}
+
+ws_status ws_cache_timing_read(ws_cache* c, ws_call_timing* out, int32_t max, int32_t* n) {
+  if (!c || !n || (max > 0 && !out)) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  TimingRing& tr = c->timing;
+  if (tr.cap == 0) return fail(WS_ERR_INVALID_ARG, "timing is not enabled");
+  const int32_t count = std::min(tr.count, std::max(max, 0));
+  const int32_t first = (tr.next - tr.count + tr.cap) % tr.cap;
+  for (int32_t i = 0; i < count; ++i) {
+    const int32_t slot = (first + i) % tr.cap;
+    WS_HIP(hipEventSynchronize(tr.ev[3 * slot + 2]));
+    float a_ms = 0.f, m_ms = 0.f;
+    WS_HIP(hipEventElapsedTime(&a_ms, tr.ev[3 * slot], tr.ev[3 * slot + 1]));
+    WS_HIP(hipEventElapsedTime(&m_ms, tr.ev[3 * slot + 1], tr.ev[3 * slot + 2]));
+    out[i] = tr.meta[slot];
+    out[i].attn_us = 1e3f * a_ms;
+    out[i].merge_us = 1e3f * m_ms;
+  }
+  *n = count;
+  tr.count = 0;
+  return WS_OK;
 }
 
 const char* ws_last_error(void) { return g_last_error.c_str(); }

@@ -69,6 +69,11 @@ class ws_cache_stats(ctypes.Structure):
                 ("n_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class ws_call_timing(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("n_splits", ctypes.c_int32),
+                ("attn_us", ctypes.c_float), ("merge_us", ctypes.c_float)]
+
+
 _vp, _i32, _i64, _u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
 _P = ctypes.POINTER
 _SIGS = {
@@ -88,6 +93,8 @@ _SIGS = {
     "ws_cache_info": [_vp, _P(ws_cache_stats)],
     "ws_cache_check": [_vp, _P(_u32)],
     "ws_cache_set_option": [_vp, _i32, _i32],
+    "ws_cache_timing_enable": [_vp, _i32],
+    "ws_cache_timing_read": [_vp, _P(ws_call_timing), _i32, _P(_i32)],
 }
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -181,6 +188,17 @@ def ws_cache_check(cache) -> int:
 
 def ws_cache_set_option(cache, opt, value):
     _check(_lib.ws_cache_set_option(cache, opt, value), "ws_cache_set_option")
+
+
+def ws_cache_timing_enable(cache, capacity):
+    _check(_lib.ws_cache_timing_enable(cache, capacity), "ws_cache_timing_enable")
+
+
+def ws_cache_timing_read(cache, max_calls):
+    buf = (ws_call_timing * max(max_calls, 1))()
+    n = _i32()
+    _check(_lib.ws_cache_timing_read(cache, buf, max_calls, ctypes.byref(n)), "ws_cache_timing_read")
+    return [buf[i] for i in range(n.value)]
 
 
 def ws_last_error() -> str:
@@ -295,6 +313,17 @@ class Cache:
 
     def set_option(self, opt, value):
         ws_cache_set_option(self.handle, opt, value)
+
+    def timing_enable(self, capacity):
+        ws_cache_timing_enable(self.handle, capacity)
+        self._timing_cap = capacity
+
+    def timing_read(self):
+        """Per-call launch timing recorded since the last read, oldest first:
+        dicts with path ('video'/'audio'), n_splits, attn_us, merge_us."""
+        out = ws_cache_timing_read(self.handle, getattr(self, "_timing_cap", 0))
+        return [dict(path="audio" if t.path else "video", n_splits=t.n_splits, attn_us=t.attn_us,
+                     merge_us=t.merge_us) for t in out]
 
 
 def mask_spec(q_unit, min_visible_unit=INT32_MIN, kinds=(WS_KIND_COND, WS_KIND_VIDEO)):

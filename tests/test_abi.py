@@ -72,6 +72,7 @@ int main(void) {
   P(ws_query_desc, softmax_scale)
   S(ws_mask_spec) P(ws_mask_spec, kind_mask)
   S(ws_cache_stats)
+  S(ws_call_timing) P(ws_call_timing, n_splits) P(ws_call_timing, attn_us) P(ws_call_timing, merge_us)
   printf("enum %zu\n", sizeof(ws_kind));
   return 0;
 }
@@ -93,7 +94,8 @@ def test_struct_layouts_match_c(tmp_path):
     assert c["enum"] == 4
     for name, typ in (("ws_cache_config", ws.ws_cache_config),
                       ("ws_append_desc", ws.ws_append_desc), ("ws_query_desc", ws.ws_query_desc),
-                      ("ws_mask_spec", ws.ws_mask_spec), ("ws_cache_stats", ws.ws_cache_stats)):
+                      ("ws_mask_spec", ws.ws_mask_spec), ("ws_cache_stats", ws.ws_cache_stats),
+                      ("ws_call_timing", ws.ws_call_timing)):
         assert ctypes.sizeof(typ) == c[name], name
         for key, off in c.items():
             if key.startswith(name + "."):

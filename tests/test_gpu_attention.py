@@ -326,3 +326,34 @@ def test_video_tight_bound_shift(ws):
         assert_gates(got, ref, label="tight bound")
     finally:
         L.close()
+
+
+def test_launch_timing_ring(ws):
+    """ws_cache_timing_*: one record per attention call, oldest first, with
+    the attention kernel and the merge timed separately; disabled -> error."""
+    wl = synth.make_workload(TINY)
+    L = Loaded(ws, wl)
+    try:
+        st = wl.steps[0]
+        with pytest.raises(ws.WsError):
+            L.cache.timing_read()
+        L.cache.timing_enable(4)
+        L.cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, 3)
+        L.run("video", st.q_video, st.q_video_pos, wl.current_unit, ALL_KINDS)
+        L.cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, 1)
+        L.run("video", st.q_video, st.q_video_pos, wl.current_unit, ALL_KINDS)
+        L.run("audio", st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+        rec = L.cache.timing_read()
+        assert [r["path"] for r in rec] == ["video", "video", "audio"]
+        assert [r["n_splits"] for r in rec][:2] == [3, 1]
+        assert all(r["attn_us"] > 0 for r in rec)
+        assert rec[0]["merge_us"] > 0 and rec[2]["merge_us"] > 0
+        assert L.cache.timing_read() == []
+        for _ in range(6):  # ring of 4 keeps the last 4
+            L.run("audio", st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+        assert len(L.cache.timing_read()) == 4
+        L.cache.timing_enable(0)
+        with pytest.raises(ws.WsError):
+            L.cache.timing_read()
+    finally:
+        L.close()
