@@ -14,6 +14,8 @@
 // The attention is the performer's per-step attention over its K/V cache
 // (Wan-Streamer v0.2, Sec. 3); block-causal visibility (Fig. 1 caption) is
 // resolved on the host into the list of visible pages.
+#include <type_traits>
+
 #include "ws_kernels.hpp"
 
 namespace ws {
@@ -21,6 +23,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -238,6 +241,13 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 // serializes the MFMA operand reads.  M0 is restored afterwards; completion
 // is tracked by the explicit vmcnt wait in wait_dma.
 __device__ __forceinline__ void dma16(const uint16_t* sbase, uint32_t voff, uint32_t lds) {
+  // both are wave-uniform by construction; make that visible to the compiler
+  // (readfirstlane returns int: widen through uint32_t, never sign-extend)
+  lds = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(lds));
+  const uint64_t b = reinterpret_cast<uint64_t>(sbase);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+  sbase = reinterpret_cast<const uint16_t*>((static_cast<uint64_t>(hi) << 32) | lo);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -878,29 +888,106 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
 }
 
 // ------------------------------------------------------------------------- //
-// audio_attn: one wave per (head, q-tile of 16, key range); 4 waves per block.
-//
-// Lane l = 16*g + i (g = 0..3, i = query column).  16x16x32 MFMAs:
-//   S^T tile t (16 keys) = K Q'^T, 4 d-steps of 32;
-//   O^T d-tile u' (16 d) += V^T P^T, 2 key-steps of 32 per page.
-// A-row m of S-tile t reads key 32*(t/2) + 8*(m/4) + 4*(t%2) + m%4, so that
-// register r of lane group g in S-tiles 2u and 2u+1 holds keys 32u + 8g + r and
-// 32u + 8g + 4 + r: exactly the eight consecutive keys the P*V B operand of
-// key-step u needs from that lane.  Rows and chunks past the page's valid
-// tokens are not loaded (no HBM traffic for the partly filled pages).
+// audio_attn: the few audio queries, memory-bound.  A workgroup of 4 waves
+// takes one (head, 16-query tile, key range) and streams its pages through a
+// 4-stage LDS ring with direct global->LDS loads issued three pages ahead; each
+// wave computes 16 keys of every page.  With lane l = 16 g + i (i = query
+// column):
+//   S^T (16 keys x 16 queries) = K Q'^T   4 x v_mfma_f32_16x16x32_bf16
+//   O^T (128 d x 16 queries) += V^T P^T   8 x v_mfma_f32_16x16x16_bf16
+// The S accumulator register r of lane group g holds key 4g + r of the
+// wave's 16, which is exactly the B operand (keys 4g..4g+3) of the P*V MFMA.
+// The four waves' softmax states merge through LDS at the end.
+//   LDS stage: K [64 keys][16 chunks], chunk c of key R at position
+//   c ^ (R & 15); V^T chunk-major [8 key chunks][128 d][16 B].
+// Each wave issues exactly 8 direct loads per page (a page is 32 blocks of
+// 1 KB); blocks past a page's valid tokens read a zero block instead of the
+// pool, so partly filled pages cost only their valid rows in HBM traffic.
 // ------------------------------------------------------------------------- //
+constexpr int kAStages = 4;
+__shared__ __attribute__((aligned(1024))) uint16_t g_ak[kAStages][kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(1024))) uint16_t g_av[kAStages][kHeadDim * kPageTokens];
+
+struct AudioCtx {
+  const_page_list pages;
+  const uint16_t* kpool;   // pool base + this head's tile offset
+  const uint16_t* vpool;
+  const uint16_t* zeros;   // 1 KB of zeros
+  int64_t page_stride;
+  int wave, lane;
+  uint32_t k_off, v_off;   // lane source byte offsets of K block 0 / V block 0
+};
+
+// Direct loads of page `page` (n_valid tokens) into stage `st`: wave w takes
+// blocks j = w + 4 i (i = 0..7); j < 16 are K blocks (keys 4j..4j+3), j >= 16
+// are V^T blocks (key chunk (j-16)/2, d half (j-16)%2).
+__device__ __forceinline__ void audio_dma(const AudioCtx& c, int page, int n_valid, int st) {
+  const uint16_t* kt = c.kpool + page * c.page_stride;
+  const uint16_t* vt = c.vpool + page * c.page_stride;
+  const uint32_t kl = lds_offset(g_ak[st]), vl = lds_offset(g_av[st]);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = c.wave + 4 * i;  // wave-uniform; j < 16 exactly when i < 4
+    if (i < 4) {
+      const bool ok = 4 * j < n_valid;
+      // K block j: rows 4j..4j+3; the lane offset k_off is that of block 0
+      dma16(ok ? kt + j * 4 * kHeadDim : c.zeros, ok ? c.k_off : 16u * c.lane, kl + 1024 * j);
+    } else {
+      const int jj = j - 16, chunk = jj >> 1, half = jj & 1;
+      const bool ok = 8 * chunk < n_valid;
+      dma16(ok ? vt + half * 64 * kPageTokens + 8 * chunk : c.zeros, ok ? c.v_off : 16u * c.lane,
+            vl + 2048 * chunk + 1024 * half);
+    }
+  }
+}
+constexpr int kAudioDmaPerPage = 8;
+// vmcnt(16): this wave's loads of the next two pages may stay in flight
+__device__ __forceinline__ void wait_audio_dma_page() {
+  static_assert(kAudioDmaPerPage * (kAStages - 2) == 16, "vmcnt encoding below");
+  __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt = 16: bits [15:14] = 1, [3:0] = 0
+}
+
+// Page list index of the page staged kAStages - 1 pages ahead of pi.
+__device__ __forceinline__ int audio_ahead(int pi, int p_end) {
+  return pi + kAStages - 1 < p_end ? pi + kAStages - 1 : p_end - 1;
+}
+
 __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, i16 = lane & 15;
-  const int wid = blockIdx.x * 4 + wave;
-  const int n_work = a.num_heads * a.n_qtiles * a.n_splits;
-  if (wid >= n_work) return;
-  const int split = wid % a.n_splits;
-  const int rest = wid / a.n_splits;
+  const int bid = blockIdx.x;
+  const int split = bid % a.n_splits;
+  const int rest = bid / a.n_splits;
   const int qtile = rest % a.n_qtiles;
   const int head = rest / a.n_qtiles;
   const int p_begin = split * a.pages_per_split;
   const int p_end = min(a.n_pages, p_begin + a.pages_per_split);
+
+  AudioCtx c;
+  c.pages = (const_page_list)a.pages;
+  c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
+  c.kpool = a.kpool + head * kPageHeadElems;
+  c.vpool = a.vpool + head * kPageHeadElems;
+  c.zeros = a.zeros;
+  c.wave = wave;
+  c.lane = lane;
+  {
+    // K blocks of this wave are j = wave + 4 i: row R = 4 j + lane/16 has
+    // R & 15 = 4 wave + lane/16 for every i
+    const int r = lane >> 4;
+    c.k_off = 2u * (r * kHeadDim + 8 * ((lane & 15) ^ (4 * wave + r)));
+    c.v_off = 2u * (lane * kPageTokens);  // d = 64 half + lane, key chunk 0
+  }
+
+  // start streaming the first pages before anything else
+  if (p_begin < p_end) {
+#pragma unroll
+    for (int k = 0; k < kAStages - 1; ++k) {
+      const int pk = min(p_begin + k, p_end - 1);
+      audio_dma(c, c.pages[pk].x, c.pages[pk].y, k);
+    }
+  }
 
   // Q prologue: lane holds Q'[q][32s + 8g + j], s = 0..3
   const int q = qtile * kAudioQTile + i16;
@@ -949,97 +1036,161 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
   f32x4 o[8];
 #pragma unroll
   for (int u = 0; u < 8; ++u) o[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  float m_run = kNegInf, l_run = 0.f;
-  const float c = a.scale_log2;
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  const float sc = a.scale_log2;
+  const int key0 = 16 * wave;  // this wave's keys within a page
 
-  for (int pi = p_begin; pi < p_end; ++pi) {
-    const int2 pr = a.pages[pi];
-    const int n_valid = pr.y;
-    const int64_t tileo = (static_cast<int64_t>(pr.x) * a.num_heads + head) * kPageHeadElems;
-    const uint16_t* kb = a.kpool + tileo;
-    const uint16_t* vb = a.vpool + tileo;
-    u32x4 kr[4][4], vr[2][8];
+  // Softmax shift: as in the video kernel, the logit bound |Q'_q| max|k| *
+  // scale (log2 units) over the range's pages when it is at most
+  // kShiftBoundMax for all 16 queries (then no maximum is tracked and the
+  // page loop has no cross-lane work), else the running maximum.
+  float kn2 = 0.f;
+  for (int pi = p_begin + lane; pi < p_end; pi += 64)
+    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(a.pages[pi].x) * a.num_heads + head]);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int key = 32 * (t >> 1) + 8 * (i16 >> 2) + 4 * (t & 1) + (i16 & 3);
+  for (int off = 1; off < 64; off <<= 1) kn2 = fmaxf(kn2, __shfl_xor(kn2, off));
+  float qn2 = 0.f;
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-        kr[t][s] = key < n_valid
-                       ? *reinterpret_cast<const u32x4*>(kb + key * kHeadDim + 32 * s + 8 * g)
-                       : zero4;
-    }
+  for (int s = 0; s < 4; ++s) {
+    const u32x4 w = __builtin_bit_cast(u32x4, qreg[s]);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const bool chunk_ok = 32 * u + 8 * g < n_valid;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
-        vr[u][dt] = chunk_ok ? *reinterpret_cast<const u32x4*>(
-                                   vb + (16 * dt + i16) * kPageTokens + 32 * u + 8 * g)
-                             : zero4;
-    }
-    f32x4 st[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      st[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[t][s]), qreg[s], st[t], 0, 0,
-                                                        0);
-    }
-    // register r of group g in tile t holds key 32*(t/2) + 8*g + 4*(t%2) + r
-    float mx = kNegInf;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = 32 * (t >> 1) + 8 * g + 4 * (t & 1) + r;
-        if (key >= n_valid) st[t][r] = kNegInf;
-        mx = fmaxf(mx, st[t][r]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = fast_exp2((m_run - m_use) * c);
-    const float mc = m_use * c;
-    float psum = 0.f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        st[t][r] = fast_exp2(__builtin_fmaf(st[t][r], c, -mc));
-        psum += st[t][r];
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) o[u] *= alpha;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      u32x4 w;
-      w[0] = pack_bf16(st[2 * u][0], st[2 * u][1]);
-      w[1] = pack_bf16(st[2 * u][2], st[2 * u][3]);
-      w[2] = pack_bf16(st[2 * u + 1][0], st[2 * u + 1][1]);
-      w[3] = pack_bf16(st[2 * u + 1][2], st[2 * u + 1][3]);
-      const bf16x8 pbv = as_bf16x8(w);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[u][dt]), pbv, o[dt], 0, 0, 0);
-    }
+    for (int i = 0; i < 4; ++i) qn2 += bf16_lo(w[i]) * bf16_lo(w[i]) + bf16_hi(w[i]) * bf16_hi(w[i]);
   }
+  qn2 += __shfl_xor(qn2, 16);
+  qn2 += __shfl_xor(qn2, 32);
+  const float bound = sqrtf(qn2 * kn2) * sc;
+  const bool fixed_shift = a.fixed_shift != 0 && __all(bound <= kShiftBoundMax);
+  // m_run is kept in logit units (times sc gives the exp2 shift)
+  float m_run = fixed_shift ? bound / sc : kNegInf, l_run = 0.f;
+  if (fixed_shift && sc == 0.f) m_run = 0.f;
 
-  // lane holds O^T[16*dt + 4*g + r][q]; row sums are spread over the 4 groups
-  float l_tot = l_run + __shfl_xor(l_run, 16);
-  l_tot += __shfl_xor(l_tot, 32);
-  if (!q_ok) return;
-  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-  const int64_t row = (static_cast<int64_t>(split) * a.num_heads + head) * a.n_q + q;
-  float* po = a.part_o + row * kHeadDim;
+  if (p_begin < p_end) wait_audio_dma_page();
+  auto page_loop = [&](auto fixed_tag) {
+    constexpr bool kFixed = decltype(fixed_tag)::value;
+  // page-list entries are read one page ahead of their use
+  int n_valid_next = p_begin < p_end ? c.pages[p_begin].y : 0;
+  int pa_next = audio_ahead(p_begin, p_end);
+  int ahead_page_next = p_begin < p_end ? c.pages[pa_next].x : 0;
+  int ahead_valid_next = p_begin < p_end ? c.pages[pa_next].y : 0;
+  for (int pi = p_begin, st = 0; pi < p_end; ++pi, st = st == kAStages - 1 ? 0 : st + 1) {
+    const int n_valid = n_valid_next, ahead_page = ahead_page_next, ahead_valid = ahead_valid_next;
+    if (pi + 1 < p_end) {
+      const int pa2 = audio_ahead(pi + 1, p_end);
+      n_valid_next = c.pages[pi + 1].y;
+      ahead_page_next = c.pages[pa2].x;
+      ahead_valid_next = c.pages[pa2].y;
+    }
+    __syncthreads();
+    audio_dma(c, ahead_page, ahead_valid, st == 0 ? kAStages - 1 : st - 1);
+    const uint16_t* sk = g_ak[st];
+    const uint16_t* sv = g_av[st];
+
+    // S^T for keys key0 + 0..15
+    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+    const int krow = key0 + i16;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 k = as_bf16x8(*reinterpret_cast<const u32x4*>(sk + krow * kHeadDim + 8 * ((4 * s + g) ^ i16)));
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k, qreg[s], sacc, 0, 0, 0);
+    }
+    // V^T operands: d = 16 dt + i16, keys key0 + 4g..4g+3
+    u32x2 vr[8];
+    const int vchunk = (key0 >> 3) + (g >> 1);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt)
+      vr[dt] = *reinterpret_cast<const u32x2*>(sv + vchunk * 1024 + (16 * dt + i16) * 8 + 4 * (g & 1));
+
+    // softmax over this wave's keys (register r: key key0 + 4g + r)
+    if (n_valid < kPageTokens) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (key0 + 4 * g + r >= n_valid) sacc[r] = kNegInf;
+    }
+    float alpha = 1.f, mc = m_run * sc;
+    if constexpr (!kFixed) {
+      float mx = fmaxf(fmaxf(sacc[0], sacc[1]), fmaxf(sacc[2], sacc[3]));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
+      alpha = fast_exp2((m_run - m_use) * sc);
+      mc = m_use * sc;
+      m_run = m_new;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sacc[r] = fast_exp2(__builtin_fmaf(sacc[r], sc, -mc));
+    // P in bf16 for the MFMA; the row sum is taken over the same bf16 values
+    u32x2 pw;
+    pw[0] = pack_bf16(sacc[0], sacc[1]);
+    pw[1] = pack_bf16(sacc[2], sacc[3]);
+    {
+      const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+      const uint32_t w0 = pw[0], w1 = pw[1];  // scalar temporaries for the bit-casts
+      const float psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones,
+          __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, 0.f, false), false);
+      l_run = l_run * alpha + psum;
+    }
+    const bf16x4 pb = __builtin_bit_cast(bf16x4, pw);
+    if constexpr (!kFixed) {
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+    }
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt)
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vr[dt]), pb, o[dt], 0, 0, 0);
+    wait_audio_dma_page();
+  }
+  };
+  if (fixed_shift)
+    page_loop(std::true_type{});
+  else
+    page_loop(std::false_type{});
+  wait_dma_all();
+
+  // merge the four waves: lane holds O^T[16 dt + 4g + r][q] of its keys
+  float l_w = l_run + __shfl_xor(l_run, 16);
+  l_w += __shfl_xor(l_w, 32);
+  __syncthreads();  // the stages are free: reuse them for the merge
+  float* sm_o = reinterpret_cast<float*>(g_ak[0]);          // [wave][128 d][16 q]
+  float* sm_ml = reinterpret_cast<float*>(g_av[0]);         // [wave][2][16 q]
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
-    *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * g) = o[dt] * inv;
-  if (g == 0) a.part_lse[row] = l_tot > 0.f ? m_run * c + __log2f(l_tot) : kNegInf;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sm_o[(wave * kHeadDim + 16 * dt + 4 * g + r) * 16 + i16] = o[dt][r];
+  if (g == 0) {
+    sm_ml[(wave * 2 + 0) * 16 + i16] = m_run;
+    sm_ml[(wave * 2 + 1) * 16 + i16] = l_w;
+  }
+  __syncthreads();
+  // thread t: query t % 16, d = 8 (t / 16) .. + 8
+  const int qi = tid & 15, d0 = 8 * (tid >> 4);
+  float mw[4], big = kNegInf;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    mw[w] = sm_ml[(w * 2) * 16 + qi];
+    big = fmaxf(big, mw[w]);
+  }
+  float ew[4], l_tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    ew[w] = big == kNegInf ? 0.f : fast_exp2((mw[w] - big) * sc);
+    l_tot += ew[w] * sm_ml[(w * 2 + 1) * 16 + qi];
+  }
+  const int qq = qtile * kAudioQTile + qi;
+  if (qq >= a.n_q) return;
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  const int64_t row = (static_cast<int64_t>(split) * a.num_heads + head) * a.n_q + qq;
+  float* po = a.part_o + row * kHeadDim + d0;
+  f32x4 out0, out1;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) v += ew[w] * sm_o[(w * kHeadDim + d0 + k) * 16 + qi];
+    if (k < 4) out0[k] = v * inv; else out1[k - 4] = v * inv;
+  }
+  *reinterpret_cast<f32x4*>(po) = out0;
+  *reinterpret_cast<f32x4*>(po + 4) = out1;
+  if (tid < 16) a.part_lse[row] = l_tot > 0.f ? big * sc + __log2f(l_tot) : kNegInf;
 }
 
 // ------------------------------------------------------------------------- //
@@ -1128,8 +1279,7 @@ hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
-  const int waves = a.num_heads * a.n_qtiles * a.n_splits;
-  dim3 grid((waves + 3) / 4);
+  dim3 grid(a.num_heads * a.n_qtiles * a.n_splits);
   hipLaunchKernelGGL(audio_attn_kernel, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }

@@ -88,6 +88,7 @@ struct ws_cache {
   int32_t opt_audio_splits = 0;
   int32_t opt_running_max = 0;
   float* knorm2 = nullptr;  // [max_pages][H] squared key-norm maxima
+  uint16_t* zeros = nullptr;  // 1 KB of zeros (direct-load source of empty blocks)
   std::vector<ws::PageRef> scratch_list;
   TimingRing timing;
 
@@ -226,7 +227,9 @@ void free_all(ws_cache* c) {
   if (c->part_o) (void)hipFree(c->part_o);
   if (c->part_lse) (void)hipFree(c->part_lse);
   if (c->knorm2) (void)hipFree(c->knorm2);
+  if (c->zeros) (void)hipFree(c->zeros);
   c->knorm2 = nullptr;
+  c->zeros = nullptr;
   c->kpool = c->vpool = nullptr;
   c->rope_dev = nullptr;
   c->flags_dev = nullptr;
@@ -280,6 +283,8 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
     return bail(hip_fail(e, "hipMalloc(key norms)"));
   if ((e = hipMemset(c->knorm2, 0, norm_elems * sizeof(float))) != hipSuccess)
     return bail(hip_fail(e, "hipMemset"));
+  if ((e = hipMalloc(&c->zeros, 1024)) != hipSuccess) return bail(hip_fail(e, "hipMalloc(zeros)"));
+  if ((e = hipMemset(c->zeros, 0, 1024)) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
   if (ws_status st = fill_rope(c); st != WS_OK) return bail(st);
   if ((e = hipMalloc(&c->flags_dev, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMalloc"));
   if ((e = hipMemset(c->flags_dev, 0, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
@@ -323,9 +328,10 @@ int choose_video_splits(const ws_cache* c, int n_items, int n_pages) {
 
 int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
   if (c->opt_audio_splits > 0) return c->opt_audio_splits;
-  // enough independent waves to keep HBM busy: ~8 per CU, >= 2 pages per wave
-  const int target = (8 * c->num_cus + n_items - 1) / n_items;
-  return std::max(1, std::min({target, std::max(1, n_pages / 2), kMaxAudioSplits}));
+  // one workgroup (96 KB of LDS) per CU: as many key ranges as fill the CUs
+  // once, each streaming its pages two ahead
+  const int target = std::max(1, c->num_cus / std::max(n_items, 1));
+  return std::max(1, std::min({target, n_pages, kMaxAudioSplits}));
 }
 
 ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
@@ -372,6 +378,7 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   a.kpool = c->kpool;
   a.vpool = c->vpool;
   a.knorm2 = c->knorm2;
+  a.zeros = c->zeros;
   a.fixed_shift = c->opt_running_max ? 0 : 1;
   a.pages = plist;
   a.n_pages = n_pages;

@@ -69,6 +69,7 @@ struct AttnArgs {
   const float* knorm2;
   int32_t fixed_shift;   // 1: softmax shift from the key-norm bound when it is small enough
   const int2* pages;     // visible pages: (page id, valid tokens)
+  const uint16_t* zeros; // 1 KB of zeros (direct-load source for empty blocks)
   int32_t n_pages;
   int32_t n_splits;      // key-range splits (1: write bf16 output directly)
   int32_t pages_per_split;
@@ -95,7 +96,8 @@ struct CombineArgs {
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 // Video path: 256-query tiles on 8 waves, 32x32x16 bf16 MFMA, LDS-staged pages.
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
-// Audio path: one wave per (head, key range), 16x16x32 bf16 MFMA, no LDS.
+// Audio path: 4 waves per (head, 16-query tile, key range), pages streamed
+// through LDS, 16x16x32 / 16x16x16 bf16 MFMA.
 hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 

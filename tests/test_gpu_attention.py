@@ -259,6 +259,10 @@ def test_video_running_max_path(ws, name):
             ref = L.oracle(st.q_video, st.q_video_pos, wl.current_unit, kinds)
             assert_gates(lazy, ref, label=f"running max, splits={splits}")
         assert_gates(fixed, lazy, label="bound shift vs running max")
+        if st.q_audio is not None:  # the audio kernel follows the same option
+            got = L.run("audio", st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+            ref = L.oracle(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+            assert_gates(got, ref, label="audio, running max")
     finally:
         L.close()
 
@@ -299,6 +303,9 @@ def test_video_large_key_norm_falls_back(ws, splits):
         got = L.run("video", q, pos, 0, (synth.KIND_COND,), mode=ws.WS_APPEND_RAW)
         ref = L.oracle(q, pos, 0, (synth.KIND_COND,), mode=oracle.MODE_RAW)
         assert_gates(got, ref, label=f"long keys, splits={splits}")
+        L.cache.set_option(ws.WS_OPT_AUDIO_KV_SPLITS, splits)
+        got = L.run("audio", q[:40], pos[:40], 0, (synth.KIND_COND,), mode=ws.WS_APPEND_RAW)
+        assert_gates(got, ref[:40], label=f"audio, long keys, splits={splits}")
     finally:
         L.close()
 
