@@ -8,6 +8,7 @@ Sec. 2.1 history commit):
   1. the thinker's 256-token conditioning slice is written into the cache
      (stored as given, in place of the previous unit's slice);
   2. unit u's 920 video and 4 audio K/V are appended (RMS-norm + rotary on K);
+     steps 1 and 2 are one batched append (a single kernel launch);
   3. video attention: 920 queries (norm + rotary fused) over 256 + 9 x 920 =
      8536 keys;
   4. audio attention: 4 queries over cond + 9 x (920 + 4) = 8572 keys;
@@ -145,10 +146,12 @@ def main():
         e = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if timed else None
         if timed:
             e[0].record(stream)
-        cache.append(0, ws.WS_KIND_COND, s["ck"], s["cv"], ws.WS_APPEND_RAW)
-        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
-        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma,
-                     eps)
+        cache.append_many([
+            dict(unit=0, kind=ws.WS_KIND_COND, k=s["ck"], v=s["cv"], mode=ws.WS_APPEND_RAW),
+            dict(unit=u, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"], mode=ws.WS_APPEND_NORM_ROPE,
+                 positions=vpos[u], gamma=gamma, eps=eps),
+            dict(unit=u, kind=ws.WS_KIND_AUDIO, k=s["ka"], v=s["va"], mode=ws.WS_APPEND_NORM_ROPE,
+                 positions=apos[u], gamma=gamma, eps=eps)])
         if timed:
             e[1].record(stream)
             e[2].record(stream)

@@ -99,6 +99,18 @@ typedef struct ws_append_desc {
   float eps;                 /* RMS-norm epsilon (>= 0); NORM_ROPE only */
 } ws_append_desc;
 
+/* One segment of a batched append (ws_kv_append_many): the K/V buffers and
+ * strides of ws_kv_append plus its descriptor. */
+typedef struct ws_append_item {
+  const void* k;
+  const void* v;
+  int64_t tok_stride;
+  int64_t head_stride;
+  ws_append_desc desc;
+} ws_append_item;
+
+#define WS_MAX_APPEND_ITEMS 16
+
 typedef struct ws_query_desc {
   ws_append_mode mode;       /* NORM_ROPE: RMS-norm + rotary on Q; RAW: Q used as given */
   const int32_t* positions;  /* device int32 [n_q][3]; NORM_ROPE only */
@@ -166,6 +178,18 @@ WS_API ws_status ws_cache_reset(ws_cache* cache);
 WS_API ws_status ws_kv_append(ws_cache* cache, const void* k, const void* v, int64_t tok_stride,
                        int64_t head_stride, const ws_append_desc* desc, void* hip_stream);
 
+/* ws_kv_append for n (1..WS_MAX_APPEND_ITEMS) segments at once, e.g. a
+ * denoising step's video and audio K/V together with a thinker slice (Sec. 3):
+ * the writes of all items share kernel launches (one launch per 4 items and 192
+ * pages).  Each item obeys the rules of ws_kv_append and is stored exactly as a
+ * separate ws_kv_append of it would store it.  All items are checked before any
+ * page is taken, and if one item fails (bad argument, two items naming the same
+ * (unit, kind), WS_ERR_OUT_OF_PAGES, WS_ERR_COMMITTED, WS_ERR_SHAPE) the
+ * segments this call created are released again and nothing is launched.
+ * items: host array of n entries, read before the call returns. */
+WS_API ws_status ws_kv_append_many(ws_cache* cache, int32_t n, const ws_append_item* items,
+                                   void* hip_stream);
+
 /* Marks the VIDEO and AUDIO segments of `unit` as committed history
  * (Sec. 2.1); they can no longer be rewritten.  Host-only. */
 WS_API ws_status ws_unit_commit(ws_cache* cache, int32_t unit);
@@ -185,7 +209,7 @@ WS_API ws_status ws_kv_release(ws_cache* cache, int32_t unit, ws_kind kind);
  *   out[i] = sum_j softmax_j(scale * <Q'_i, K'_j>) V_j over the visible keys.
  *   q:   device bf16 [n_q][H][128] with strides (q_tok_stride, q_head_stride).
  *   out: device bf16 [n_q][H][128] with strides (out_tok_stride, out_head_stride).
- * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 128-query tiles, 64-key pages.
+ * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 256-query tiles, 64-key pages.
  * The softmax shift of a query row is its logit bound |Q''_i| * max |K'_j|
  * (Cauchy-Schwarz over the pages of one key range) when that bound is at most
  * 40 in log2 units, else a lazily raised running maximum

@@ -55,6 +55,18 @@ __device__ __forceinline__ float2 rope_cs(const RopeTables& r, int p, int pt, in
   return r.tab[2][pw * r.pairs[2] + (p - p01)];
 }
 
+// Clamps a token's (t, h, w) into the table; flags a clamp.
+__device__ __forceinline__ void clamp_pos(const RopeTables& r, int t, int h, int w, uint32_t* flags,
+                                          int& pt, int& ph, int& pw) {
+  const int ct = min(max(t, 0), r.max_pos[0] - 1);
+  const int ch = min(max(h, 0), r.max_pos[1] - 1);
+  const int cw = min(max(w, 0), r.max_pos[2] - 1);
+  if ((ct != t) | (ch != h) | (cw != w)) atomicOr(flags, kFlagPositionClamped);
+  pt = ct;
+  ph = ch;
+  pw = cw;
+}
+
 // Loads a token's (t, h, w), clamped into the table; flags a clamp.
 __device__ __forceinline__ void load_pos(const RopeTables& r, const int32_t* positions, int tok,
                                          uint32_t* flags, int& pt, int& ph, int& pw) {
@@ -69,15 +81,21 @@ __device__ __forceinline__ void load_pos(const RopeTables& r, const int32_t* pos
 }
 
 // ------------------------------------------------------------------------- //
-// kv_append: grid (pages of this launch, heads), 256 threads.
+// kv_append: grid (pages of this launch, heads), 256 threads; the pages may
+// belong to up to AppendArgs::kMaxSegs segments.
 // ------------------------------------------------------------------------- //
-template <int kMode>
 __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPageTokens][kHeadDim + 8];
   __shared__ float wave_norm2[4];
   const int head = blockIdx.y;
   const int page = a.pages[blockIdx.x];
-  const int tok0 = (a.first_page + blockIdx.x) * kPageTokens;
+  const int si = a.blk_seg[blockIdx.x];
+  const uint16_t* src_k = a.seg[si].k;
+  const uint16_t* src_v = a.seg[si].v;
+  const int64_t tok_stride = a.seg[si].tok_stride, head_stride = a.seg[si].head_stride;
+  const int n_tokens = a.seg[si].n_tokens;
+  const int mode = a.seg[si].mode;
+  const int tok0 = a.blk_page[blockIdx.x] * kPageTokens;
   const int64_t tile = (static_cast<int64_t>(page) * a.num_heads + head) * kPageHeadElems;
   uint16_t* kdst = a.kpool + tile;
   uint16_t* vdst = a.vpool + tile;
@@ -89,22 +107,49 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
   const int rr = t >> 4;
   float norm2 = 0.f;
   float g[8];
-  if (kMode == 1) {
-    const float4 g0 = *reinterpret_cast<const float4*>(a.gamma + 8 * c);
-    const float4 g1 = *reinterpret_cast<const float4*>(a.gamma + 8 * c + 4);
+  float eps = 0.f;
+  const int32_t* positions = nullptr;
+  if (mode == 1) {
+    const float* gamma = a.seg[si].gamma;
+    eps = a.seg[si].eps;
+    positions = a.seg[si].positions;
+    const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * c);
+    const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * c + 4);
     g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
     g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
   }
+  // all loads of the tile are issued up front (K rows, V rows, positions)
+  u32x4 kx[4], vx[4];
+  int tpos[4][3];
+#pragma unroll
+  for (int pass = 0; pass < 4; ++pass) {
+    const int tok = tok0 + pass * 16 + rr;
+    kx[pass] = tok < n_tokens ? *reinterpret_cast<const u32x4*>(src_k + tok * tok_stride + head * head_stride + 8 * c)
+                              : (u32x4){0u, 0u, 0u, 0u};
+    if (mode == 1 && tok < n_tokens) {
+      tpos[pass][0] = positions[3 * tok + 0];
+      tpos[pass][1] = positions[3 * tok + 1];
+      tpos[pass][2] = positions[3 * tok + 2];
+    } else {
+      tpos[pass][0] = tpos[pass][1] = tpos[pass][2] = 0;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = t + 256 * i;
+    const int tok = tok0 + (ch >> 4);
+    vx[i] = tok < n_tokens ? *reinterpret_cast<const u32x4*>(src_v + tok * tok_stride + head * head_stride + 8 * (ch & 15))
+                           : (u32x4){0u, 0u, 0u, 0u};
+  }
+
 #pragma unroll
   for (int pass = 0; pass < 4; ++pass) {
     const int slot = pass * 16 + rr;
     const int tok = tok0 + slot;
-    const bool valid = tok < a.n_tokens;
-    u32x4 x = {0u, 0u, 0u, 0u};
-    if (valid)
-      x = *reinterpret_cast<const u32x4*>(a.k + tok * a.tok_stride + head * a.head_stride + 8 * c);
+    const bool valid = tok < n_tokens;
+    const u32x4 x = kx[pass];
     u32x4 y = x;
-    if (kMode == 1) {
+    if (mode == 1) {
       float f[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -119,9 +164,9 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
       ss += __shfl_xor(ss, 2);
       ss += __shfl_xor(ss, 4);
       ss += __shfl_xor(ss, 8);
-      const float inv = rsqrtf(ss * (1.0f / kHeadDim) + a.eps);
+      const float inv = rsqrtf(ss * (1.0f / kHeadDim) + eps);
       int pt = 0, ph = 0, pw = 0;
-      if (valid) load_pos(a.rope, a.positions, tok, a.flags, pt, ph, pw);
+      if (valid) clamp_pos(a.rope, tpos[pass][0], tpos[pass][1], tpos[pass][2], a.flags, pt, ph, pw);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float y0 = f[2 * i] * inv * g[2 * i];
@@ -149,12 +194,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int ch = t + 256 * i;
-    const int slot = ch >> 4, dc = ch & 15;
-    const int tok = tok0 + slot;
-    u32x4 x = {0u, 0u, 0u, 0u};
-    if (tok < a.n_tokens)
-      x = *reinterpret_cast<const u32x4*>(a.v + tok * a.tok_stride + head * a.head_stride + 8 * dc);
-    *reinterpret_cast<u32x4*>(&vt[slot][8 * dc]) = x;
+    *reinterpret_cast<u32x4*>(&vt[ch >> 4][8 * (ch & 15)]) = vx[i];
   }
   __syncthreads();
 #pragma unroll
@@ -1264,11 +1304,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
 }  // namespace
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_pages, a.num_heads);
-  if (a.mode == 1)
-    hipLaunchKernelGGL(kv_append_kernel<1>, grid, dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(kv_append_kernel<0>, grid, dim3(256), 0, stream, a);
+  dim3 grid(a.n_blocks, a.num_heads);
+  hipLaunchKernelGGL(kv_append_kernel, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

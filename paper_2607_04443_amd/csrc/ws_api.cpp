@@ -460,62 +460,130 @@ ws_status ws_cache_reset(ws_cache* cache) {
 
 ws_status ws_kv_append(ws_cache* c, const void* k, const void* v, int64_t tok_stride,
                        int64_t head_stride, const ws_append_desc* d, void* hip_stream) {
-  if (!c || !d) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (!d) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  const ws_append_item item{k, v, tok_stride, head_stride, *d};
+  return ws_kv_append_many(c, 1, &item, hip_stream);
+}
+
+ws_status ws_kv_append_many(ws_cache* c, int32_t n, const ws_append_item* items, void* hip_stream) {
+  if (!c || !items) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (n < 1 || n > WS_MAX_APPEND_ITEMS)
+    return fail(WS_ERR_INVALID_ARG, "append item count %d outside [1, %d]", n, WS_MAX_APPEND_ITEMS);
   if (ws_status st = check_device(c); st != WS_OK) return st;
-  if (ws_status st = check_kind(d->kind); st != WS_OK) return st;
-  if (d->mode != WS_APPEND_RAW && d->mode != WS_APPEND_NORM_ROPE)
-    return fail(WS_ERR_INVALID_ARG, "bad append mode %d", static_cast<int>(d->mode));
-  if (d->n_tokens < 1) return fail(WS_ERR_SHAPE, "n_tokens must be >= 1");
   const int H = c->cfg.num_heads;
-  if (ws_status st = check_strides("k", k, tok_stride, head_stride, d->n_tokens, H); st != WS_OK) return st;
-  if (ws_status st = check_strides("v", v, tok_stride, head_stride, d->n_tokens, H); st != WS_OK) return st;
-  if (d->mode == WS_APPEND_NORM_ROPE) {
-    if (!d->positions || !d->gamma) return fail(WS_ERR_INVALID_ARG, "NORM_ROPE needs positions and gamma");
-    if (!aligned16(d->gamma)) return fail(WS_ERR_INVALID_ARG, "gamma is not 16-byte aligned");
-    if (!(d->eps >= 0.f) || !std::isfinite(d->eps)) return fail(WS_ERR_INVALID_ARG, "bad eps");
+  // Every item is checked before any page is taken.
+  for (int i = 0; i < n; ++i) {
+    const ws_append_item& it = items[i];
+    const ws_append_desc* d = &it.desc;
+    if (ws_status st = check_kind(d->kind); st != WS_OK) return st;
+    if (d->mode != WS_APPEND_RAW && d->mode != WS_APPEND_NORM_ROPE)
+      return fail(WS_ERR_INVALID_ARG, "item %d: bad append mode %d", i, static_cast<int>(d->mode));
+    if (d->n_tokens < 1) return fail(WS_ERR_SHAPE, "item %d: n_tokens must be >= 1", i);
+    if (ws_status st = check_strides("k", it.k, it.tok_stride, it.head_stride, d->n_tokens, H); st != WS_OK)
+      return st;
+    if (ws_status st = check_strides("v", it.v, it.tok_stride, it.head_stride, d->n_tokens, H); st != WS_OK)
+      return st;
+    if (d->mode == WS_APPEND_NORM_ROPE) {
+      if (!d->positions || !d->gamma)
+        return fail(WS_ERR_INVALID_ARG, "item %d: NORM_ROPE needs positions and gamma", i);
+      if (!aligned16(d->gamma)) return fail(WS_ERR_INVALID_ARG, "item %d: gamma is not 16-byte aligned", i);
+      if (!(d->eps >= 0.f) || !std::isfinite(d->eps)) return fail(WS_ERR_INVALID_ARG, "item %d: bad eps", i);
+    }
+    for (int j = 0; j < i; ++j)
+      if (items[j].desc.unit == d->unit && items[j].desc.kind == d->kind)
+        return fail(WS_ERR_INVALID_ARG, "items %d and %d name the same unit %d kind %d", j, i, d->unit,
+                    static_cast<int>(d->kind));
   }
-  ws::Segment* seg = nullptr;
-  bool created = false;
-  switch (c->pt.acquire(d->unit, d->kind, d->n_tokens, &seg, &created)) {
-    case ws::PtStatus::ok: break;
-    case ws::PtStatus::out_of_pages:
-      return fail(WS_ERR_OUT_OF_PAGES, "pool has %d free pages, segment needs %d", c->pt.free_pages(),
-                  (d->n_tokens + ws::kPageTokens - 1) / ws::kPageTokens);
-    case ws::PtStatus::committed:
-      return fail(WS_ERR_COMMITTED, "unit %d kind %d is committed history", d->unit, static_cast<int>(d->kind));
-    case ws::PtStatus::shape:
-      return fail(WS_ERR_SHAPE, "rewrite of unit %d kind %d with %d tokens (segment has %d)", d->unit,
-                  static_cast<int>(d->kind), d->n_tokens, seg ? seg->n_tokens : -1);
-    default: return fail(WS_ERR_INVALID_ARG, "page table error");
+  // Pages: all items or none.  Page lists are copied out at once (the table's
+  // segment storage may move on the next creation).
+  std::vector<std::vector<int32_t>> pages(static_cast<size_t>(n));
+  std::vector<int> created_items;
+  auto roll_back = [&]() {
+    for (auto it = created_items.rbegin(); it != created_items.rend(); ++it)
+      c->pt.release(items[*it].desc.unit, items[*it].desc.kind);
+  };
+  for (int i = 0; i < n; ++i) {
+    const ws_append_desc* d = &items[i].desc;
+    ws::Segment* seg = nullptr;
+    bool created = false;
+    const ws::PtStatus st = c->pt.acquire(d->unit, d->kind, d->n_tokens, &seg, &created);
+    if (st != ws::PtStatus::ok) {
+      roll_back();
+      switch (st) {
+        case ws::PtStatus::out_of_pages:
+          return fail(WS_ERR_OUT_OF_PAGES, "item %d: pool has %d free pages, segment needs %d", i,
+                      c->pt.free_pages(), (d->n_tokens + ws::kPageTokens - 1) / ws::kPageTokens);
+        case ws::PtStatus::committed:
+          return fail(WS_ERR_COMMITTED, "item %d: unit %d kind %d is committed history", i, d->unit,
+                      static_cast<int>(d->kind));
+        case ws::PtStatus::shape:
+          return fail(WS_ERR_SHAPE, "item %d: rewrite of unit %d kind %d with %d tokens (segment has %d)", i,
+                      d->unit, static_cast<int>(d->kind), d->n_tokens, seg ? seg->n_tokens : -1);
+        default: return fail(WS_ERR_INVALID_ARG, "item %d: page table error", i);
+      }
+    }
+    if (created) created_items.push_back(i);
+    pages[static_cast<size_t>(i)] = seg->pages;
   }
+
+  // Launches of up to kMaxSegs segments and kMaxAppendPages pages each; a
+  // segment longer than that continues in the next launch.
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   ws::AppendArgs a{};
-  a.k = static_cast<const uint16_t*>(k);
-  a.v = static_cast<const uint16_t*>(v);
-  a.tok_stride = tok_stride;
-  a.head_stride = head_stride;
-  a.n_tokens = d->n_tokens;
-  a.mode = static_cast<int32_t>(d->mode);
-  a.positions = d->positions;
-  a.gamma = d->gamma;
-  a.eps = d->eps;
   a.num_heads = H;
   a.kpool = c->kpool;
   a.vpool = c->vpool;
   a.knorm2 = c->knorm2;
   a.rope = c->rope;
   a.flags = c->flags_dev;
-  const int n_pages = static_cast<int>(seg->pages.size());
-  for (int p0 = 0; p0 < n_pages; p0 += ws::AppendArgs::kMaxAppendPages) {
-    const int np = std::min(ws::AppendArgs::kMaxAppendPages, n_pages - p0);
-    a.first_page = p0;
-    a.n_pages = np;
-    for (int i = 0; i < np; ++i) a.pages[i] = seg->pages[static_cast<size_t>(p0 + i)];
-    hipError_t e = ws::launch_kv_append(a, stream);
-    if (e != hipSuccess) {
-      if (created && p0 == 0) c->pt.release(d->unit, d->kind);
-      return hip_fail(e, "kv_append launch");
+  int n_segs = 0;
+  auto flush = [&]() -> hipError_t {
+    if (a.n_blocks == 0) return hipSuccess;
+    const hipError_t e = ws::launch_kv_append(a, stream);
+    a.n_blocks = 0;
+    n_segs = 0;
+    return e;
+  };
+  for (int i = 0; i < n; ++i) {
+    const ws_append_item& it = items[i];
+    const std::vector<int32_t>& pl = pages[static_cast<size_t>(i)];
+    int slot = -1;
+    for (size_t p = 0; p < pl.size(); ++p) {
+      if (a.n_blocks == ws::AppendArgs::kMaxAppendPages) {
+        if (hipError_t e = flush(); e != hipSuccess) {
+          roll_back();
+          return hip_fail(e, "kv_append launch");
+        }
+        slot = -1;
+      }
+      if (slot < 0) {
+        if (n_segs == ws::AppendArgs::kMaxSegs) {
+          if (hipError_t e = flush(); e != hipSuccess) {
+            roll_back();
+            return hip_fail(e, "kv_append launch");
+          }
+        }
+        slot = n_segs++;
+        ws::AppendSeg& sg = a.seg[slot];
+        sg.k = static_cast<const uint16_t*>(it.k);
+        sg.v = static_cast<const uint16_t*>(it.v);
+        sg.tok_stride = it.tok_stride;
+        sg.head_stride = it.head_stride;
+        sg.n_tokens = it.desc.n_tokens;
+        sg.mode = static_cast<int32_t>(it.desc.mode);
+        sg.positions = it.desc.positions;
+        sg.gamma = it.desc.gamma;
+        sg.eps = it.desc.eps;
+      }
+      a.pages[a.n_blocks] = pl[p];
+      a.blk_page[a.n_blocks] = static_cast<int32_t>(p);
+      a.blk_seg[a.n_blocks] = static_cast<uint8_t>(slot);
+      ++a.n_blocks;
     }
+  }
+  if (hipError_t e = flush(); e != hipSuccess) {
+    roll_back();
+    return hip_fail(e, "kv_append launch");
   }
   return WS_OK;
 }

@@ -30,26 +30,35 @@ struct RopeTables {
   int32_t pairs[3];
 };
 
-struct AppendArgs {
+// One segment of an append launch.
+struct AppendSeg {
   const uint16_t* k;
   const uint16_t* v;
   int64_t tok_stride;
   int64_t head_stride;
   int32_t n_tokens;      // tokens of the whole segment
-  int32_t first_page;    // index (within the segment) of pages[0]
-  int32_t n_pages;       // pages handled by this launch (<= kMaxAppendPages)
   int32_t mode;          // 0 raw, 1 norm + rope
   const int32_t* positions;
   const float* gamma;
   float eps;
+};
+
+// Several segments in one launch: block x of the grid writes page pages[x],
+// which is page blk_page[x] of segment blk_seg[x].
+struct AppendArgs {
+  static constexpr int kMaxSegs = 4;
+  static constexpr int kMaxAppendPages = 192;
+  AppendSeg seg[kMaxSegs];
+  int32_t n_blocks;
   int32_t num_heads;
   uint16_t* kpool;
   uint16_t* vpool;
   float* knorm2;
   RopeTables rope;
   uint32_t* flags;
-  static constexpr int kMaxAppendPages = 192;
   int32_t pages[kMaxAppendPages];
+  int32_t blk_page[kMaxAppendPages];
+  uint8_t blk_seg[kMaxAppendPages];
 };
 
 struct AttnArgs {

@@ -53,6 +53,14 @@ class ws_append_desc(ctypes.Structure):
                 ("gamma", ctypes.c_void_p), ("eps", ctypes.c_float)]
 
 
+class ws_append_item(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("tok_stride", ctypes.c_int64),
+                ("head_stride", ctypes.c_int64), ("desc", ws_append_desc)]
+
+
+WS_MAX_APPEND_ITEMS = 16
+
+
 class ws_query_desc(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("positions", ctypes.c_void_p),
                 ("gamma", ctypes.c_void_p), ("eps", ctypes.c_float),
@@ -81,6 +89,7 @@ _SIGS = {
     "ws_cache_destroy": [_vp],
     "ws_cache_reset": [_vp],
     "ws_kv_append": [_vp, _vp, _vp, _i64, _i64, _P(ws_append_desc), _vp],
+    "ws_kv_append_many": [_vp, _i32, _P(ws_append_item), _vp],
     "ws_unit_commit": [_vp, _i32],
     "ws_kv_evict_before": [_vp, _i32],
     "ws_kv_release": [_vp, _i32, _i32],
@@ -136,6 +145,12 @@ def ws_cache_reset(cache):
 def ws_kv_append(cache, k, v, tok_stride, head_stride, desc: ws_append_desc, stream):
     _check(_lib.ws_kv_append(cache, k, v, tok_stride, head_stride, ctypes.byref(desc), stream),
            "ws_kv_append")
+
+
+def ws_kv_append_many(cache, items, stream):
+    """items: a sequence of ws_append_item."""
+    arr = (ws_append_item * len(items))(*items)
+    _check(_lib.ws_kv_append_many(cache, len(items), arr, stream), "ws_kv_append_many")
 
 
 def ws_unit_commit(cache, unit):
@@ -249,20 +264,32 @@ class Cache:
         except Exception:
             pass
 
-    def append(self, unit, kind, k, v, mode=WS_APPEND_RAW, positions=None, gamma=None, eps=1e-6,
-               stream=None):
+    @staticmethod
+    def _item(unit, kind, k, v, mode=WS_APPEND_RAW, positions=None, gamma=None, eps=1e-6):
         import torch
         _check_tensor("k", k, torch.bfloat16)
         _check_tensor("v", v, torch.bfloat16)
         if k.stride() != v.stride() or k.shape != v.shape:
             raise ValueError("k and v must share shape and strides")
-        d = ws_append_desc()
+        it = ws_append_item()
+        it.k, it.v = k.data_ptr(), v.data_ptr()
+        it.tok_stride, it.head_stride = k.stride(0), k.stride(1)
+        d = it.desc
         d.unit, d.kind, d.n_tokens, d.mode = unit, kind, k.shape[0], mode
         d.positions = positions.data_ptr() if positions is not None else None
         d.gamma = gamma.data_ptr() if gamma is not None else None
         d.eps = eps
-        ws_kv_append(self.handle, k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), d,
+        return it
+
+    def append(self, unit, kind, k, v, mode=WS_APPEND_RAW, positions=None, gamma=None, eps=1e-6,
+               stream=None):
+        it = self._item(unit, kind, k, v, mode, positions, gamma, eps)
+        ws_kv_append(self.handle, it.k, it.v, it.tok_stride, it.head_stride, it.desc,
                      _stream_handle(stream))
+
+    def append_many(self, items, stream=None):
+        """items: dicts with the keyword arguments of append (stream aside)."""
+        ws_kv_append_many(self.handle, [self._item(**x) for x in items], _stream_handle(stream))
 
     def _attn(self, fn, q, out, mask, mode, positions, gamma, eps, scale, stream):
         import torch

@@ -73,6 +73,9 @@ int main(void) {
   S(ws_mask_spec) P(ws_mask_spec, kind_mask)
   S(ws_cache_stats)
   S(ws_call_timing) P(ws_call_timing, n_splits) P(ws_call_timing, attn_us) P(ws_call_timing, merge_us)
+  S(ws_append_item) P(ws_append_item, v) P(ws_append_item, tok_stride) P(ws_append_item, head_stride)
+  P(ws_append_item, desc)
+  printf("max_items %d\n", WS_MAX_APPEND_ITEMS);
   printf("enum %zu\n", sizeof(ws_kind));
   return 0;
 }
@@ -92,10 +95,12 @@ def test_struct_layouts_match_c(tmp_path):
              .stdout.splitlines())
     c = {k: int(v) for k, v in c.items()}
     assert c["enum"] == 4
+    assert c["max_items"] == ws.WS_MAX_APPEND_ITEMS
     for name, typ in (("ws_cache_config", ws.ws_cache_config),
                       ("ws_append_desc", ws.ws_append_desc), ("ws_query_desc", ws.ws_query_desc),
                       ("ws_mask_spec", ws.ws_mask_spec), ("ws_cache_stats", ws.ws_cache_stats),
-                      ("ws_call_timing", ws.ws_call_timing)):
+                      ("ws_call_timing", ws.ws_call_timing),
+                      ("ws_append_item", ws.ws_append_item)):
         assert ctypes.sizeof(typ) == c[name], name
         for key, off in c.items():
             if key.startswith(name + "."):
