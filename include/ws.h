@@ -210,6 +210,8 @@ WS_API ws_status ws_kv_release(ws_cache* cache, int32_t unit, ws_kind kind);
  *   q:   device bf16 [n_q][H][128] with strides (q_tok_stride, q_head_stride).
  *   out: device bf16 [n_q][H][128] with strides (out_tok_stride, out_head_stride).
  * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 256-query tiles, 64-key pages.
+ * A head's keys may be split into ranges (split-KV), merged by log-sum-exp
+ * in a second kernel.
  * The softmax shift of a query row is its logit bound |Q''_i| * max |K'_j|
  * (Cauchy-Schwarz over the pages of one key range) when that bound is at most
  * 40 in log2 units, else a lazily raised running maximum

@@ -594,31 +594,23 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
 // exponentials of tile 0 keys 0-15, 16-23 P*V chunks 0-1 with those of keys
 // 16-31.  Tile 1 of the last page is finished by video_flush.
 struct PipeState {
-  f32x16 s1;      // S tile 1 of the previous page (exp2 argument, masked)
+  f32x16 s1;      // S tile 1 of the previous page (exp2 argument)
 };
 
 template <int kCur, bool kFirst>
-__device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, PipeState& ps, int pi,
-                                           int p_end) {
+__device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, PipeState& ps,
+                                           const f32x16& s_init, int pi, int p_end) {
   constexpr int kPrev = (kCur + kStages - 1) % kStages;
   const uint16_t* sk = stage_k<kCur>();
   const uint16_t* sv = stage_v<kCur>();
   const uint16_t* svp = stage_v<kPrev>();
   pi = __builtin_amdgcn_readfirstlane(pi);
-  const int n_valid = c.pages[pi].y;
   const int ahead = c.pages[ahead2(pi, p_end)].x;
-  pin_sgpr(n_valid);
+  pin_sgpr(ahead);
   __syncthreads();
   stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, l32 = c.l32;
-  const bool tail = n_valid < kPageTokens;
-  auto mask_tail = [&](f32x16& sc, int key0) {
-    const int lim = n_valid - key0 - 8 * half;
-#pragma unroll
-    for (int r = 0; r < 16; ++r)
-      if (16 * (r >> 3) + (r & 7) >= lim) sc[r] = kNegInf;
-  };
   auto kread = [&](int n) {  // S k-step n % 8 of tile n / 8
     const int row = n < 8 ? l32 : 32 + l32;
     return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kHeadDim + 8 * ((2 * (n & 7) + half) ^ (l32 & 15))));
@@ -643,13 +635,10 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
   for (int o = 0; o < kAhead; ++o) ring[o] = oread(o);
   __builtin_amdgcn_sched_barrier(0);
 
-  const float neg_m = -st.m_run;
+  // The first MFMA of each S tile takes its accumulator input from s_init
+  // (-m_run in every register), so the tiles start at the exp2 argument with
+  // no per-page register initialisation.
   f32x16 s0, s1;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    s0[r] = neg_m;
-    s1[r] = neg_m;
-  }
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
   float l = 0.f;
   // P words: w[0..3] keys 0-15 of a tile (chunk 0 or 2), w[4..7] keys 16-31
@@ -674,9 +663,9 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
     const bf16x8 a = ring[o % (kAhead + 1)];
     if (kFirst) {
       if (o < 8) {
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], s0, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
       } else if (o < 16) {
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 8], s1, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 8], o == 8 ? s_init : s1, 0, 0, 0);
         exp_one(s0, o - 8, p0, (o - 8) >> 1);
       } else if (o < 20) {
         st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p0), st.o[o - 16], 0, 0, 0);
@@ -687,13 +676,13 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
       }
     } else {
       if (o < 8) {
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], s0, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
         exp_one(ps.s1, o, pp2, o >> 1);
       } else if (o < 12) {
         st.o[o - 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp2), st.o[o - 8], 0, 0, 0);
         exp_one(ps.s1, 8 + o - 8, pp3, (o - 8) >> 1);
       } else if (o < 16) {
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 12], s1, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 12], o == 12 ? s_init : s1, 0, 0, 0);
         exp_one(ps.s1, 8 + o - 8, pp3, (o - 8) >> 1);
       } else if (o < 20) {
         st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp3), st.o[o - 16], 0, 0, 0);
@@ -709,16 +698,9 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
         st.o[o - 28] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p1), st.o[o - 28], 0, 0, 0);
       }
     }
-    // the tile-0 exponentials start after step 7 (kFirst) or 15: mask the
-    // page tail first (waits for the S tile 0 MFMAs on tail pages only)
-    if (o == 7) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (tail) mask_tail(s0, 0);
-    }
     __builtin_amdgcn_sched_barrier(0);
   }
   st.l_run += l;
-  if (tail) mask_tail(s1, 32);
   ps.s1 = s1;
   wait_dma_all_but_last_page();
 }
@@ -740,24 +722,21 @@ __device__ __forceinline__ void video_flush(const VideoCtx& c, VideoState& st, c
   }
 }
 
-__global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
+// The work of one video workgroup: query tile `qtile` of head `head` against
+// pages [p_begin, p_end) of the visible list, which is key range `seg` of the
+// n_seg ranges that split this head's pages.  With one range the output is
+// written in bf16; otherwise the softmax-normalised fp32 partial and its
+// log-sum-exp go to the split-KV workspace for the combine kernel.
+struct VideoSeg {
+  int head, p_begin, p_end, seg, n_seg;
+};
+
+__device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg& sg, int qtile) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, l32 = lane & 31;
-
-  // Work decode.  Workgroups are dispatched round-robin over the 8 XCDs;
-  // renumber so that each XCD owns a contiguous run of (head, q-tile, split)
-  // items, i.e. whole heads, whose K/V pages then stay in that XCD's L2.
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
-  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
-  const int split = item % a.n_splits;
-  const int rest = item / a.n_splits;
-  const int qtile = rest % a.n_qtiles;
-  const int head = rest / a.n_qtiles;
-  const int p_begin = split * a.pages_per_split;
-  const int p_end = min(a.n_pages, p_begin + a.pages_per_split);
+  const int head = sg.head, p_begin = sg.p_begin, p_end = sg.p_end;
 
   VideoCtx c;
   c.pages = (const_page_list)a.pages;
@@ -775,6 +754,13 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
     c.dma_v = 2 * (d0 * kPageTokens + 8 * ((lane & 7) ^ ((d0 >> 1) & 7)));
   }
 
+  // The first two pages are requested before anything else, so that their
+  // latency overlaps the query prologue.
+  if (p_begin < p_end) {
+    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[p_begin].x), g_k0, g_v0);
+    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 1, p_end - 1)].x), g_k1, g_v1);
+  }
+
   // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
   const int q = qtile * kVideoQTile + wave * 32 + l32;
   const bool q_ok = q < a.n_q;
@@ -783,7 +769,18 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
 #pragma unroll
   for (int s = 0; s < 8; ++s)
     qraw[s] = q_ok ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : (u32x4){0u, 0u, 0u, 0u};
-    if (a.mode == 1) {
+  // the range's page-list entries, for the softmax shift below
+  int2 pg_mine = make_int2(0, kPageTokens);
+  float kn2 = 0.f;
+  int n_empty = 0;
+  for (int pi = p_begin + lane; pi < p_end; pi += 64) {
+    pg_mine = a.pages[pi];
+    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pg_mine.x) * a.num_heads + head]);
+    n_empty += kPageTokens - pg_mine.y;
+  }
+  if (a.mode == 1) {
+    int pt = 0, ph = 0, pw = 0;
+    if (q_ok) load_pos(a.rope, a.positions, q, a.flags, pt, ph, pw);
     float ss = 0.f;
 #pragma unroll
     for (int s = 0; s < 8; ++s)
@@ -794,8 +791,6 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
       }
     ss += __shfl_xor(ss, 32);
     const float inv = rsqrtf(ss * (1.0f / kHeadDim) + a.eps);
-    int pt = 0, ph = 0, pw = 0;
-    if (q_ok) load_pos(a.rope, a.positions, q, a.flags, pt, ph, pw);
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int d0 = 16 * s + 8 * half;
@@ -826,19 +821,19 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
   // ---- softmax shift ----
   // Logits arrive in the log2 domain (the scale and log2(e) are folded into
   // Q'').  By Cauchy-Schwarz every logit of row q is at most
-  // B_q = |Q''_q| * max |k| over the split's pages (knorm2 holds the squared
-  // norms of the stored keys).  Softmax is shift invariant, so B_q serves as
-  // the exp2 shift as it stands: p = exp2(s - B_q) <= 1, with no running
-  // maximum and no rescale of O.  The row's largest p is at least 2^(-2 B_q),
-  // so for B_q <= kShiftBoundMax every weight above 2^-46 of the row maximum
-  // stays a normal bf16/fp32 number.  Otherwise the running maximum is raised
-  // lazily: only when a 32-key tile exceeds it by more than kLazyTau
-  // (p then stays below 2^kLazyTau), which makes the O rescale rare.
-  float kn2 = 0.f;
-  for (int pi = p_begin + lane; pi < p_end; pi += 64)
-    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(a.pages[pi].x) * a.num_heads + head]);
+  // B_q = |Q''_q| * max |k| over the segment's pages (knorm2 holds the
+  // squared norms of the stored keys).  Softmax is shift invariant, so B_q
+  // serves as the exp2 shift as it stands: p = exp2(s - B_q) <= 1, with no
+  // running maximum and no rescale of O.  The row's largest p is at least
+  // 2^(-2 B_q), so for B_q <= kShiftBoundMax every weight above 2^-46 of the
+  // row maximum stays a normal bf16/fp32 number.  Otherwise the running
+  // maximum is raised lazily: only when a 32-key tile exceeds it by more than
+  // kLazyTau (p then stays below 2^kLazyTau), which makes the O rescale rare.
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) kn2 = fmaxf(kn2, __shfl_xor(kn2, o));
+  for (int o = 1; o < 64; o <<= 1) {
+    kn2 = fmaxf(kn2, __shfl_xor(kn2, o));
+    n_empty += __shfl_xor(n_empty, o);
+  }
   float qn2 = 0.f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
@@ -849,8 +844,9 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
   qn2 += __shfl_xor(qn2, 32);
   const float bound = sqrtf(qn2 * kn2);
   const bool fixed_shift = a.fixed_shift != 0 && __all(bound <= kShiftBoundMax);
+  n_empty = __builtin_amdgcn_readfirstlane(n_empty);  // uniform after the reduction
 
-  // ---- main loop over this split's pages ----
+  // ---- main loop over this segment's pages ----
   VideoState st;
 #pragma unroll
   for (int t = 0; t < 4; ++t)
@@ -860,22 +856,28 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
   st.l_run = 0.f;
   st.first = true;
 
-  if (p_begin < p_end) {
-    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[p_begin].x), g_k0, g_v0);
-    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 1, p_end - 1)].x), g_k1, g_v1);
-    wait_dma_all_but_last_page();
-  }
+  if (p_begin < p_end) wait_dma_all_but_last_page();
   if (c.active && fixed_shift) {
     if (p_begin < p_end) {
       PipeState ps;
-      video_iter<0, true>(c, st, ps, p_begin, p_end);
+      f32x16 s_init;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s_init[r] = -st.m_run;
+      video_iter<0, true>(c, st, ps, s_init, p_begin, p_end);
       for (int pi = p_begin + 1; pi < p_end; pi += 4) {
-        video_iter<1, false>(c, st, ps, pi, p_end);
-        if (pi + 1 < p_end) video_iter<2, false>(c, st, ps, pi + 1, p_end);
-        if (pi + 2 < p_end) video_iter<3, false>(c, st, ps, pi + 2, p_end);
-        if (pi + 3 < p_end) video_iter<0, false>(c, st, ps, pi + 3, p_end);
+        video_iter<1, false>(c, st, ps, s_init, pi, p_end);
+        if (pi + 1 < p_end) video_iter<2, false>(c, st, ps, s_init, pi + 1, p_end);
+        if (pi + 2 < p_end) video_iter<3, false>(c, st, ps, s_init, pi + 2, p_end);
+        if (pi + 3 < p_end) video_iter<0, false>(c, st, ps, s_init, pi + 3, p_end);
       }
       video_flush(c, st, ps, (p_end - 1 - p_begin) % kStages);
+      // Tail slots past a page's valid tokens are not masked: their stored
+      // keys and values are zero, so each logit is exactly -m_run (exp2
+      // argument) and adds nothing to O, but its weight, rounded to bf16 as
+      // the MFMAs see it, went into the row sum.  Take those weights out
+      // (split between the two lane halves that share a row).
+      const float p_empty = bf16_lo(pack_bf16(fast_exp2(-st.m_run), 0.f));
+      st.l_run -= 0.5f * static_cast<float>(n_empty) * p_empty;
     }
   } else if (c.active) {
     for (int pi = p_begin; pi < p_end; pi += 4) {
@@ -897,9 +899,9 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
 
   // ---- epilogue: lane holds O^T[32t + 8g + 4h + i][q], g = r/4, i = r%4 ----
   const float l_tot = st.l_run + __shfl_xor(st.l_run, 32);
-  if (!q_ok) return;
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-  if (a.n_splits == 1) {
+  if (sg.n_seg == 1) {
+    if (!q_ok) return;
     uint16_t* op = a.out + q * a.out_tok_stride + head * a.out_head_stride;
 #pragma unroll
     for (int t = 0; t < 4; ++t)
@@ -911,20 +913,38 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
         w[1] = pack_bf16(st.o[t][4 * g + 2] * inv, st.o[t][4 * g + 3] * inv);
         *reinterpret_cast<u32x2*>(op + d0) = w;
       }
-  } else {
-    const int64_t row = (static_cast<int64_t>(split) * a.num_heads + head) * a.n_q + q;
-    float* po = a.part_o + row * kHeadDim;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int d0 = 32 * t + 8 * g + 4 * half;
-        *reinterpret_cast<f32x4*>(po + d0) =
-            (f32x4){st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv, st.o[t][4 * g + 2] * inv,
-                    st.o[t][4 * g + 3] * inv};
-      }
-    if (half == 0) a.part_lse[row] = l_tot > 0.f ? st.m_run + __log2f(l_tot) : kNegInf;
+    return;
   }
+  if (!q_ok) return;
+  const int64_t row = (static_cast<int64_t>(sg.seg) * a.num_heads + head) * a.n_q + q;
+  float* po = a.part_o + row * kHeadDim;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int d0 = 32 * t + 8 * g + 4 * half;
+      *reinterpret_cast<f32x4*>(po + d0) =
+          (f32x4){st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv, st.o[t][4 * g + 2] * inv,
+                  st.o[t][4 * g + 3] * inv};
+    }
+  if (half == 0) a.part_lse[row] = l_tot > 0.f ? st.m_run + __log2f(l_tot) : kNegInf;
+}
+
+__global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
+  // Work decode.  Workgroups are dispatched round-robin over the 8 XCDs;
+  // renumber so that each XCD owns a contiguous run of (head, query tile,
+  // key range) items, i.e. whole heads: the query tiles of a head then read
+  // the same pages at about the same time, through that XCD's L2.
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int split = item % a.n_splits;
+  const int rest = item / a.n_splits;
+  const int qtile = rest % a.n_qtiles;
+  const int head = rest / a.n_qtiles;
+  const int p_begin = split * a.pages_per_split;
+  const int p_end = min(a.n_pages, p_begin + a.pages_per_split);
+  video_segment(a, VideoSeg{head, p_begin, p_end, split, a.n_splits}, qtile);
 }
 
 // ------------------------------------------------------------------------- //

@@ -43,7 +43,7 @@ ws_status hip_fail(hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail(e_, #call); \
   } while (0)
 
-constexpr int kMaxVideoSplits = 8;
+using ws::kMaxVideoSplits;
 constexpr int kMaxAudioSplits = 512;
 constexpr int kMaxAudioQ = 64;
 
@@ -391,13 +391,13 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   const int qtile = audio ? ws::kAudioQTile : ws::kVideoQTile;
   a.n_qtiles = (n_q + qtile - 1) / qtile;
   const int n_items = a.n_qtiles * H;
+  const int64_t cap = c->part_rows / (static_cast<int64_t>(H) * n_q);
   int splits = audio ? choose_audio_splits(c, n_items, n_pages) : choose_video_splits(c, n_items, n_pages);
   splits = std::max(1, std::min(splits, std::max(1, n_pages)));
-  const int64_t cap = c->part_rows / (static_cast<int64_t>(H) * n_q);
   splits = static_cast<int>(std::min<int64_t>(splits, std::max<int64_t>(cap, 1)));
   const int pps = n_pages > 0 ? (n_pages + splits - 1) / splits : 0;
   splits = pps > 0 ? (n_pages + pps - 1) / pps : 1;  // no empty splits
-  if (audio && cap < splits) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
+  if (cap < splits) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
   a.n_splits = splits;
   a.pages_per_split = pps;
 

@@ -80,7 +80,7 @@ struct AttnArgs {
   const int2* pages;     // visible pages: (page id, valid tokens)
   const uint16_t* zeros; // 1 KB of zeros (direct-load source for empty blocks)
   int32_t n_pages;
-  int32_t n_splits;      // key-range splits (1: write bf16 output directly)
+  int32_t n_splits;      // key-range splits (1: video writes bf16 output directly)
   int32_t pages_per_split;
   int32_t n_qtiles;
   uint16_t* out;
@@ -111,6 +111,7 @@ hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 
 constexpr int kVideoQTile = 256;
+constexpr int kMaxVideoSplits = 8;  // key-range splits of the video kernel
 constexpr int kVideoWaves = kVideoQTile / 32;
 constexpr int kAudioQTile = 16;
 
