@@ -176,7 +176,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
       }
       if (!valid) y = (u32x4){0u, 0u, 0u, 0u};
     }
-    *reinterpret_cast<u32x4*>(kdst + slot * kHeadDim + 8 * c) = y;
+    *reinterpret_cast<u32x4*>(kdst + k_tile_index(slot, 8 * c)) = y;
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) ss += bf16_lo(y[i]) * bf16_lo(y[i]) + bf16_hi(y[i]) * bf16_hi(y[i]);
@@ -206,7 +206,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
     for (int j = 0; j < 4; ++j)
       y[j] = static_cast<uint32_t>(vt[8 * tc + 2 * j][d]) |
              (static_cast<uint32_t>(vt[8 * tc + 2 * j + 1][d]) << 16);
-    *reinterpret_cast<u32x4*>(vdst + d * kPageTokens + 8 * tc) = y;
+    *reinterpret_cast<u32x4*>(vdst + v_tile_index(8 * tc, d)) = y;
   }
   if (t == 0)
     a.knorm2[static_cast<int64_t>(page) * a.num_heads + head] =
@@ -303,16 +303,17 @@ __device__ __forceinline__ void dma16(const uint16_t* sbase, uint32_t voff, uint
 // the stage (k_dst, v_dst): per wave two 1 KB blocks of each, block
 // b = 8 i + wave.  Block b of K is rows 4b..4b+3, lane l at row
 // R = 32 i + 4 wave + l/16, position l%16; block b of V^T is rows
-// d = 64 i + 8 wave + l/8, position l%8.  In both, the lane's source offset
-// changes with i only by 4096 elements (8 KB).
+// d = 64 i + 8 wave + l/8, position l%8.  The lane's source offset changes
+// with i only by a constant: 32 keys (1024 elements) in the K tile, 64 d
+// rows (2048 elements) in the V tile.
 __device__ __forceinline__ void stage_dma(const VideoCtx& c, int page, uint16_t* k_dst, uint16_t* v_dst) {
   const uint16_t* kp = c.kpool + page * c.page_stride;
   const uint16_t* vp = c.vpool + page * c.page_stride;
   const uint32_t kl = lds_offset(k_dst) + 1024 * c.wave, vl = lds_offset(v_dst) + 1024 * c.wave;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    dma16(kp + 4096 * i, c.dma_k, kl + 8192 * i);
-    dma16(vp + 4096 * i, c.dma_v, vl + 8192 * i);
+    dma16(kp + 1024 * i, c.dma_k, kl + 8192 * i);
+    dma16(vp + 2048 * i, c.dma_v, vl + 8192 * i);
   }
 }
 constexpr int kDmaPerPage = 4;  // direct loads per wave and page
@@ -749,9 +750,9 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   c.l32 = l32;
   {
     const int r0 = 4 * wave + (lane >> 4);  // K row of block i = 0
-    c.dma_k = 2 * (swap23(r0) * kHeadDim + 8 * ((lane & 15) ^ (r0 & 15)));
+    c.dma_k = 2 * k_tile_index(swap23(r0), 8 * ((lane & 15) ^ (r0 & 15)));
     const int d0 = 8 * wave + (lane >> 3);  // V^T row of block i = 0
-    c.dma_v = 2 * (d0 * kPageTokens + 8 * ((lane & 7) ^ ((d0 >> 1) & 7)));
+    c.dma_v = 2 * v_tile_index(8 * ((lane & 7) ^ ((d0 >> 1) & 7)), d0);
   }
 
   // The first two pages are requested before anything else, so that their
@@ -949,70 +950,57 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
 
 // ------------------------------------------------------------------------- //
 // audio_attn: the few audio queries, memory-bound.  A workgroup of 4 waves
-// takes one (head, 16-query tile, key range) and streams its pages through a
-// 4-stage LDS ring with direct global->LDS loads issued three pages ahead; each
-// wave computes 16 keys of every page.  With lane l = 16 g + i (i = query
-// column):
-//   S^T (16 keys x 16 queries) = K Q'^T   4 x v_mfma_f32_16x16x32_bf16
-//   O^T (128 d x 16 queries) += V^T P^T   8 x v_mfma_f32_16x16x16_bf16
-// The S accumulator register r of lane group g holds key 4g + r of the
-// wave's 16, which is exactly the B operand (keys 4g..4g+3) of the P*V MFMA.
-// The four waves' softmax states merge through LDS at the end.
-//   LDS stage: K [64 keys][16 chunks], chunk c of key R at position
-//   c ^ (R & 15); V^T chunk-major [8 key chunks][128 d][16 B].
-// Each wave issues exactly 8 direct loads per page (a page is 32 blocks of
-// 1 KB); blocks past a page's valid tokens read a zero block instead of the
-// pool, so partly filled pages cost only their valid rows in HBM traffic.
+// takes one (head, 16-query tile, key range); wave w streams pages w, w + 4,
+// ... of the range on its own (no LDS staging, no barriers), loading each
+// page's valid K rows and V^T columns straight into registers in MFMA
+// operand layout, and the four waves merge through LDS at the end.  Two
+// workgroups fit a CU, so 8 independent waves per CU keep enough bytes in
+// flight to stream the cache from HBM.  Each workgroup writes the partial of
+// its key range; the combine kernel merges them.
+//
+// With lane l = 16 g + i (i = query column, g = lane group), per page:
+//   S^T (16 keys x 16 queries) = K Q''^T  4 key tiles x 4 v_mfma_f32_16x16x32_bf16
+//   O^T (16 d x 16 queries) += V^T P^T    8 d tiles x 2 key chunks, same MFMA
+// Row m = 4 g' + r of key tile t holds key 32 (t/2) + 8 g' + 4 (t%2) + r, so
+// that accumulator registers r of tiles 2c and 2c + 1 in lane group g are
+// keys 32 c + 8 g + 0..7: exactly the B operand of the P*V MFMA of key chunk c.
 // ------------------------------------------------------------------------- //
-constexpr int kAStages = 4;
-__shared__ __attribute__((aligned(1024))) uint16_t g_ak[kAStages][kPageTokens * kHeadDim];
-__shared__ __attribute__((aligned(1024))) uint16_t g_av[kAStages][kHeadDim * kPageTokens];
+// Row m (lane index i) of key tile t: the key it holds.
+__device__ __forceinline__ int audio_key(int t, int m) {
+  return 32 * (t >> 1) + 8 * (m >> 2) + 4 * (t & 1) + (m & 3);
+}
 
-struct AudioCtx {
-  const_page_list pages;
-  const uint16_t* kpool;   // pool base + this head's tile offset
-  const uint16_t* vpool;
-  const uint16_t* zeros;   // 1 KB of zeros
-  int64_t page_stride;
-  int wave, lane;
-  uint32_t k_off, v_off;   // lane source byte offsets of K block 0 / V block 0
-};
-
-// Direct loads of page `page` (n_valid tokens) into stage `st`: wave w takes
-// blocks j = w + 4 i (i = 0..7); j < 16 are K blocks (keys 4j..4j+3), j >= 16
-// are V^T blocks (key chunk (j-16)/2, d half (j-16)%2).
-__device__ __forceinline__ void audio_dma(const AudioCtx& c, int page, int n_valid, int st) {
-  const uint16_t* kt = c.kpool + page * c.page_stride;
-  const uint16_t* vt = c.vpool + page * c.page_stride;
-  const uint32_t kl = lds_offset(g_ak[st]), vl = lds_offset(g_av[st]);
+// Loads of one page's K operands, k[t][s] = K[key(t, i)][32 s + 8 g .. + 8],
+// and V^T operands, v[dt][c] = V^T[16 dt + i][32 c + 8 g .. + 8].  Rows and
+// columns past n_valid are read from the 1 KB zero block instead (a cache
+// hit), so partly filled pages cost only their valid tokens in HBM traffic
+// and no load is predicated.
+__device__ __forceinline__ void audio_load_k(u32x4 (&k)[4][4], const uint16_t* kt, const uint16_t* zeros,
+                                             int n_valid, int g, int i, int lane) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int j = c.wave + 4 * i;  // wave-uniform; j < 16 exactly when i < 4
-    if (i < 4) {
-      const bool ok = 4 * j < n_valid;
-      // K block j: rows 4j..4j+3; the lane offset k_off is that of block 0
-      dma16(ok ? kt + j * 4 * kHeadDim : c.zeros, ok ? c.k_off : 16u * c.lane, kl + 1024 * j);
-    } else {
-      const int jj = j - 16, chunk = jj >> 1, half = jj & 1;
-      const bool ok = 8 * chunk < n_valid;
-      dma16(ok ? vt + half * 64 * kPageTokens + 8 * chunk : c.zeros, ok ? c.v_off : 16u * c.lane,
-            vl + 2048 * chunk + 1024 * half);
-    }
+  for (int t = 0; t < 4; ++t) {
+    const int key = audio_key(t, i);
+    const uint16_t* src = key < n_valid ? kt + k_tile_index(key, 8 * g) : zeros + 8 * lane;
+    const int step = key < n_valid ? k_tile_index(0, 32) : 0;  // next 32 d
+#pragma unroll
+    for (int s = 0; s < 4; ++s) k[t][s] = *reinterpret_cast<const u32x4*>(src + step * s);
   }
 }
-constexpr int kAudioDmaPerPage = 8;
-// vmcnt(16): this wave's loads of the next two pages may stay in flight
-__device__ __forceinline__ void wait_audio_dma_page() {
-  static_assert(kAudioDmaPerPage * (kAStages - 2) == 16, "vmcnt encoding below");
-  __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt = 16: bits [15:14] = 1, [3:0] = 0
+__device__ __forceinline__ void audio_load_v(u32x4 (&v)[8][2], const uint16_t* vt, const uint16_t* zeros,
+                                             int n_valid, int g, int i, int lane) {
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const bool ok = 32 * c + 8 * g < n_valid;
+    const uint16_t* src = ok ? vt + v_tile_index(32 * c + 8 * g, i) : zeros + 8 * lane;
+    const int step = ok ? v_tile_index(0, 16) : 0;  // next 16 d
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) v[dt][c] = *reinterpret_cast<const u32x4*>(src + step * dt);
+  }
 }
 
-// Page list index of the page staged kAStages - 1 pages ahead of pi.
-__device__ __forceinline__ int audio_ahead(int pi, int p_end) {
-  return pi + kAStages - 1 < p_end ? pi + kAStages - 1 : p_end - 1;
-}
-
-__global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
+  __shared__ float sm_o[4][kHeadDim][16];  // per wave O^T, merged at the end
+  __shared__ float sm_ml[4][2][16];        // per wave (m, l) per query
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, i16 = lane & 15;
@@ -1021,35 +1009,24 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
   const int rest = bid / a.n_splits;
   const int qtile = rest % a.n_qtiles;
   const int head = rest / a.n_qtiles;
-  const int p_begin = split * a.pages_per_split;
-  const int p_end = min(a.n_pages, p_begin + a.pages_per_split);
+  const int p_begin = split * a.pages_per_split + wave;
+  const int p_end = min(a.n_pages, (split + 1) * a.pages_per_split);
+  const_page_list pages = (const_page_list)a.pages;
+  const int64_t page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
+  const uint16_t* kpool = a.kpool + head * kPageHeadElems;
+  const uint16_t* vpool = a.vpool + head * kPageHeadElems;
 
-  AudioCtx c;
-  c.pages = (const_page_list)a.pages;
-  c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
-  c.kpool = a.kpool + head * kPageHeadElems;
-  c.vpool = a.vpool + head * kPageHeadElems;
-  c.zeros = a.zeros;
-  c.wave = wave;
-  c.lane = lane;
+  // the wave's first page is requested before the query prologue
+  u32x4 kreg[4][4], vreg[8][2];
   {
-    // K blocks of this wave are j = wave + 4 i: row R = 4 j + lane/16 has
-    // R & 15 = 4 wave + lane/16 for every i
-    const int r = lane >> 4;
-    c.k_off = 2u * (r * kHeadDim + 8 * ((lane & 15) ^ (4 * wave + r)));
-    c.v_off = 2u * (lane * kPageTokens);  // d = 64 half + lane, key chunk 0
+    int2 pg = make_int2(0, 0);  // no page: zeros
+    if (p_begin < p_end) pg = make_int2(pages[p_begin].x, pages[p_begin].y);
+    audio_load_k(kreg, kpool + pg.x * page_stride, a.zeros, pg.y, g, i16, lane);
+    audio_load_v(vreg, vpool + pg.x * page_stride, a.zeros, pg.y, g, i16, lane);
   }
 
-  // start streaming the first pages before anything else
-  if (p_begin < p_end) {
-#pragma unroll
-    for (int k = 0; k < kAStages - 1; ++k) {
-      const int pk = min(p_begin + k, p_end - 1);
-      audio_dma(c, c.pages[pk].x, c.pages[pk].y, k);
-    }
-  }
-
-  // Q prologue: lane holds Q'[q][32s + 8g + j], s = 0..3
+  // Q prologue: lane holds Q''[q][32 s + 8 g + j], s = 0..3, with the
+  // softmax scale and log2(e) folded in
   const int q = qtile * kAudioQTile + i16;
   const bool q_ok = q < a.n_q;
   u32x4 qraw[4];
@@ -1059,19 +1036,19 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
     qraw[s] = q_ok ? *reinterpret_cast<const u32x4*>(qp + 32 * s) : (u32x4){0u, 0u, 0u, 0u};
   bf16x8 qreg[4];
   if (a.mode == 1) {
+    int pt = 0, ph = 0, pw = 0;
+    if (q_ok) load_pos(a.rope, a.positions, q, a.flags, pt, ph, pw);
     float ss = 0.f;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float x0 = bf16_lo(qraw[s][i]), x1 = bf16_hi(qraw[s][i]);
+      for (int k = 0; k < 4; ++k) {
+        const float x0 = bf16_lo(qraw[s][k]), x1 = bf16_hi(qraw[s][k]);
         ss += x0 * x0 + x1 * x1;
       }
     ss += __shfl_xor(ss, 16);
     ss += __shfl_xor(ss, 32);
     const float inv = rsqrtf(ss * (1.0f / kHeadDim) + a.eps);
-    int pt = 0, ph = 0, pw = 0;
-    if (q_ok) load_pos(a.rope, a.positions, q, a.flags, pt, ph, pw);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const int d0 = 32 * s + 8 * g;
@@ -1080,32 +1057,31 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
       const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
       u32x4 w;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float y0 = bf16_lo(qraw[s][i]) * inv * gg[2 * i];
-        const float y1 = bf16_hi(qraw[s][i]) * inv * gg[2 * i + 1];
-        const float2 cs = rope_cs(a.rope, (d0 >> 1) + i, pt, ph, pw);
-        w[i] = pack_bf16(y0 * cs.x - y1 * cs.y, y0 * cs.y + y1 * cs.x);
+      for (int k = 0; k < 4; ++k) {
+        const float y0 = bf16_lo(qraw[s][k]) * inv * gg[2 * k];
+        const float y1 = bf16_hi(qraw[s][k]) * inv * gg[2 * k + 1];
+        const float2 cs = rope_cs(a.rope, (d0 >> 1) + k, pt, ph, pw);
+        w[k] = pack_bf16((y0 * cs.x - y1 * cs.y) * a.scale_log2, (y0 * cs.y + y1 * cs.x) * a.scale_log2);
       }
       qreg[s] = as_bf16x8(q_ok ? w : (u32x4){0u, 0u, 0u, 0u});
     }
   } else {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) qreg[s] = as_bf16x8(qraw[s]);
+    for (int s = 0; s < 4; ++s) {
+      u32x4 w;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        w[k] = pack_bf16(bf16_lo(qraw[s][k]) * a.scale_log2, bf16_hi(qraw[s][k]) * a.scale_log2);
+      qreg[s] = as_bf16x8(w);
+    }
   }
 
-  f32x4 o[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) o[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  const float sc = a.scale_log2;
-  const int key0 = 16 * wave;  // this wave's keys within a page
-
-  // Softmax shift: as in the video kernel, the logit bound |Q'_q| max|k| *
-  // scale (log2 units) over the range's pages when it is at most
-  // kShiftBoundMax for all 16 queries (then no maximum is tracked and the
-  // page loop has no cross-lane work), else the running maximum.
+  // Softmax shift, as in the video kernel: the logit bound |Q''_q| max |k|
+  // (log2 units) over the wave's pages when it is at most kShiftBoundMax for
+  // all 16 queries, else a running maximum.
   float kn2 = 0.f;
-  for (int pi = p_begin + lane; pi < p_end; pi += 64)
-    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(a.pages[pi].x) * a.num_heads + head]);
+  for (int pi = p_begin + 4 * lane; pi < p_end; pi += 256)
+    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pages[pi].x) * a.num_heads + head]);
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) kn2 = fmaxf(kn2, __shfl_xor(kn2, off));
   float qn2 = 0.f;
@@ -1113,112 +1089,93 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
   for (int s = 0; s < 4; ++s) {
     const u32x4 w = __builtin_bit_cast(u32x4, qreg[s]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) qn2 += bf16_lo(w[i]) * bf16_lo(w[i]) + bf16_hi(w[i]) * bf16_hi(w[i]);
+    for (int k = 0; k < 4; ++k) qn2 += bf16_lo(w[k]) * bf16_lo(w[k]) + bf16_hi(w[k]) * bf16_hi(w[k]);
   }
   qn2 += __shfl_xor(qn2, 16);
   qn2 += __shfl_xor(qn2, 32);
-  const float bound = sqrtf(qn2 * kn2) * sc;
+  const float bound = sqrtf(qn2 * kn2);
   const bool fixed_shift = a.fixed_shift != 0 && __all(bound <= kShiftBoundMax);
-  // m_run is kept in logit units (times sc gives the exp2 shift)
-  float m_run = fixed_shift ? bound / sc : kNegInf, l_run = 0.f;
-  if (fixed_shift && sc == 0.f) m_run = 0.f;
+  float m_run = fixed_shift ? bound : kNegInf, l_run = 0.f;
 
-  if (p_begin < p_end) wait_audio_dma_page();
-  auto page_loop = [&](auto fixed_tag) {
-    constexpr bool kFixed = decltype(fixed_tag)::value;
-  // page-list entries are read one page ahead of their use
-  int n_valid_next = p_begin < p_end ? c.pages[p_begin].y : 0;
-  int pa_next = audio_ahead(p_begin, p_end);
-  int ahead_page_next = p_begin < p_end ? c.pages[pa_next].x : 0;
-  int ahead_valid_next = p_begin < p_end ? c.pages[pa_next].y : 0;
-  for (int pi = p_begin, st = 0; pi < p_end; ++pi, st = st == kAStages - 1 ? 0 : st + 1) {
-    const int n_valid = n_valid_next, ahead_page = ahead_page_next, ahead_valid = ahead_valid_next;
-    if (pi + 1 < p_end) {
-      const int pa2 = audio_ahead(pi + 1, p_end);
-      n_valid_next = c.pages[pi + 1].y;
-      ahead_page_next = c.pages[pa2].x;
-      ahead_valid_next = c.pages[pa2].y;
-    }
-    __syncthreads();
-    audio_dma(c, ahead_page, ahead_valid, st == 0 ? kAStages - 1 : st - 1);
-    const uint16_t* sk = g_ak[st];
-    const uint16_t* sv = g_av[st];
-
-    // S^T for keys key0 + 0..15
-    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-    const int krow = key0 + i16;
+  f32x4 o[8];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const bf16x8 k = as_bf16x8(*reinterpret_cast<const u32x4*>(sk + krow * kHeadDim + 8 * ((4 * s + g) ^ i16)));
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k, qreg[s], sacc, 0, 0, 0);
-    }
-    // V^T operands: d = 16 dt + i16, keys key0 + 4g..4g+3
-    u32x2 vr[8];
-    const int vchunk = (key0 >> 3) + (g >> 1);
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
-      vr[dt] = *reinterpret_cast<const u32x2*>(sv + vchunk * 1024 + (16 * dt + i16) * 8 + 4 * (g & 1));
+  for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
-    // softmax over this wave's keys (register r: key key0 + 4g + r)
+  // Each page's K operands are reloaded (for the wave's next page) as soon
+  // as its S products are issued, and its V^T operands as soon as the P*V
+  // products are, so both loads of a page are in flight while the wave waits
+  // on the one before it.
+  for (int pi = p_begin; pi < p_end; pi += 4) {
+    const int n_valid = pages[pi].y;
+    int2 nxt = make_int2(0, 0);  // past the last page: zeros
+    if (pi + 4 < p_end) nxt = make_int2(pages[pi + 4].x, pages[pi + 4].y);
+    // S^T of the page's four key tiles
+    f32x4 sacc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      sacc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[t][s]), qreg[s], sacc[t], 0, 0, 0);
+    }
+    audio_load_k(kreg, kpool + nxt.x * page_stride, a.zeros, nxt.y, g, i16, lane);
     if (n_valid < kPageTokens) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (key0 + 4 * g + r >= n_valid) sacc[r] = kNegInf;
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (audio_key(t, 4 * g + r) >= n_valid) sacc[t][r] = kNegInf;
     }
-    float alpha = 1.f, mc = m_run * sc;
-    if constexpr (!kFixed) {
-      float mx = fmaxf(fmaxf(sacc[0], sacc[1]), fmaxf(sacc[2], sacc[3]));
+    float alpha = 1.f;
+    if (!fixed_shift) {
+      float mx = kNegInf;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) mx = fmaxf(mx, fmaxf(fmaxf(sacc[t][0], sacc[t][1]), fmaxf(sacc[t][2], sacc[t][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float m_new = fmaxf(m_run, mx);
-      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-      alpha = fast_exp2((m_run - m_use) * sc);
-      mc = m_use * sc;
+      alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
       m_run = m_new;
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sacc[r] = fast_exp2(__builtin_fmaf(sacc[r], sc, -mc));
-    // P in bf16 for the MFMA; the row sum is taken over the same bf16 values
-    u32x2 pw;
-    pw[0] = pack_bf16(sacc[0], sacc[1]);
-    pw[1] = pack_bf16(sacc[2], sacc[3]);
-    {
-      const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-      const uint32_t w0 = pw[0], w1 = pw[1];  // scalar temporaries for the bit-casts
-      const float psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones,
-          __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, 0.f, false), false);
-      l_run = l_run * alpha + psum;
-    }
-    const bf16x4 pb = __builtin_bit_cast(bf16x4, pw);
-    if constexpr (!kFixed) {
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
     }
+    const float m_use = m_run == kNegInf ? 0.f : m_run;
+    // P in bf16 (word c of chunk c: keys 32 c + 8 g + 0..7); the row sum is
+    // taken over the same bf16 values the MFMAs consume
+    u32x4 pw[2];
+    float psum = 0.f;
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
-      o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vr[dt]), pb, o[dt], 0, 0, 0);
-    wait_audio_dma_page();
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4& sc = sacc[2 * c + h];
+        const uint32_t w0 = pack_bf16(fast_exp2(sc[0] - m_use), fast_exp2(sc[1] - m_use));
+        const uint32_t w1 = pack_bf16(fast_exp2(sc[2] - m_use), fast_exp2(sc[3] - m_use));
+        pw[c][2 * h] = w0;
+        pw[c][2 * h + 1] = w1;
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones, psum, false);
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vreg[dt][c]), as_bf16x8(pw[c]), o[dt], 0, 0, 0);
+    audio_load_v(vreg, vpool + nxt.x * page_stride, a.zeros, nxt.y, g, i16, lane);
   }
-  };
-  if (fixed_shift)
-    page_loop(std::true_type{});
-  else
-    page_loop(std::false_type{});
-  wait_dma_all();
 
-  // merge the four waves: lane holds O^T[16 dt + 4g + r][q] of its keys
+  // merge the four waves: lane holds O^T[16 dt + 4 g + r][q] of its keys
   float l_w = l_run + __shfl_xor(l_run, 16);
   l_w += __shfl_xor(l_w, 32);
-  __syncthreads();  // the stages are free: reuse them for the merge
-  float* sm_o = reinterpret_cast<float*>(g_ak[0]);          // [wave][128 d][16 q]
-  float* sm_ml = reinterpret_cast<float*>(g_av[0]);         // [wave][2][16 q]
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sm_o[(wave * kHeadDim + 16 * dt + 4 * g + r) * 16 + i16] = o[dt][r];
+    for (int r = 0; r < 4; ++r) sm_o[wave][16 * dt + 4 * g + r][i16] = o[dt][r];
   if (g == 0) {
-    sm_ml[(wave * 2 + 0) * 16 + i16] = m_run;
-    sm_ml[(wave * 2 + 1) * 16 + i16] = l_w;
+    sm_ml[wave][0][i16] = m_run;
+    sm_ml[wave][1][i16] = l_w;
   }
   __syncthreads();
   // thread t: query t % 16, d = 8 (t / 16) .. + 8
@@ -1226,14 +1183,14 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
   float mw[4], big = kNegInf;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    mw[w] = sm_ml[(w * 2) * 16 + qi];
+    mw[w] = sm_ml[w][0][qi];
     big = fmaxf(big, mw[w]);
   }
   float ew[4], l_tot = 0.f;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    ew[w] = big == kNegInf ? 0.f : fast_exp2((mw[w] - big) * sc);
-    l_tot += ew[w] * sm_ml[(w * 2 + 1) * 16 + qi];
+    ew[w] = big == kNegInf ? 0.f : fast_exp2(mw[w] - big);
+    l_tot += ew[w] * sm_ml[w][1][qi];
   }
   const int qq = qtile * kAudioQTile + qi;
   if (qq >= a.n_q) return;
@@ -1245,12 +1202,12 @@ __global__ __launch_bounds__(256) void audio_attn_kernel(const AttnArgs a) {
   for (int k = 0; k < 8; ++k) {
     float v = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) v += ew[w] * sm_o[(w * kHeadDim + d0 + k) * 16 + qi];
+    for (int w = 0; w < 4; ++w) v += ew[w] * sm_o[w][d0 + k][qi];
     if (k < 4) out0[k] = v * inv; else out1[k - 4] = v * inv;
   }
   *reinterpret_cast<f32x4*>(po) = out0;
   *reinterpret_cast<f32x4*>(po + 4) = out1;
-  if (tid < 16) a.part_lse[row] = l_tot > 0.f ? big * sc + __log2f(l_tot) : kNegInf;
+  if (tid < 16) a.part_lse[row] = l_tot > 0.f ? big + __log2f(l_tot) : kNegInf;
 }
 
 // ------------------------------------------------------------------------- //

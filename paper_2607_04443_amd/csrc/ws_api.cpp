@@ -45,7 +45,7 @@ ws_status hip_fail(hipError_t e, const char* what) {
 
 using ws::kMaxVideoSplits;
 constexpr int kMaxAudioSplits = 512;
-constexpr int kMaxAudioQ = 64;
+using ws::kMaxAudioQ;
 
 struct TimingRing {
   int32_t cap = 0;
@@ -328,10 +328,10 @@ int choose_video_splits(const ws_cache* c, int n_items, int n_pages) {
 
 int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
   if (c->opt_audio_splits > 0) return c->opt_audio_splits;
-  // one workgroup (96 KB of LDS) per CU: as many key ranges as fill the CUs
-  // once, each streaming its pages two ahead
-  const int target = std::max(1, c->num_cus / std::max(n_items, 1));
-  return std::max(1, std::min({target, n_pages, kMaxAudioSplits}));
+  // Two 4-wave workgroups per CU (8 streaming waves): as many key ranges as
+  // fill the CUs once, each wave keeping at least one page.
+  const int target = std::max(1, 2 * c->num_cus / std::max(n_items, 1));
+  return std::max(1, std::min({target, std::max(1, n_pages / 4), kMaxAudioSplits}));
 }
 
 ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
@@ -647,8 +647,8 @@ ws_status ws_cache_export(ws_cache* c, int32_t unit, ws_kind kind, void* k_host,
         for (int d = 0; d < ws::kHeadDim; ++d) {
           const size_t dst = (tok * H + static_cast<size_t>(h)) * ws::kHeadDim + static_cast<size_t>(d);
           const size_t hb = static_cast<size_t>(h) * ws::kPageHeadElems;
-          if (ko) ko[dst] = kp[hb + static_cast<size_t>(slot) * ws::kHeadDim + static_cast<size_t>(d)];
-          if (vo) vo[dst] = vp[hb + static_cast<size_t>(d) * ws::kPageTokens + static_cast<size_t>(slot)];
+          if (ko) ko[dst] = kp[hb + static_cast<size_t>(ws::k_tile_index(slot, d))];
+          if (vo) vo[dst] = vp[hb + static_cast<size_t>(ws::v_tile_index(slot, d))];
         }
     }
   }

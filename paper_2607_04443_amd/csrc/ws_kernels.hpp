@@ -1,14 +1,16 @@
 // Launch interface of the gfx950 kernels (host side sees only these structs
 // and the launch functions; the kernels live in kernels.hip).
 //
-// Device memory layout of the paged cache (all bf16):
-//   K pool: [page][head][64 slots][128 d]   -- a (page, head) tile is 16 KB contiguous
-//   V pool: [page][head][128 d][64 slots]   -- stored transposed, so the P*V
-//           MFMA operand (eight consecutive keys of one d) is one 16-byte load
+// Device memory layout of the paged cache (all bf16).  Pages hold 64 tokens;
+// a (page, head) tile is 16 KB contiguous in each pool:
+//   K pool: [page][head] tile = [4 d groups][64 slots][32 d]
+//   V pool: [page][head] tile = [2 slot halves][128 d][32 slots]  (V stored
+//           transposed: eight consecutive keys of one d, the P*V MFMA operand,
+//           are one 16-byte load)
+// Both tiles are arranged so that the 16-key x 32-d (K) and 16-d x 32-key
+// (V^T) operand blocks of one MFMA step cover whole 128-byte lines, and the
+// video kernel's direct-to-LDS loads keep a constant per-lane source offset.
 // Slots past a segment's last token hold zeros, so masked keys never carry
-// non-finite values into the P*V product.
-// Key norms: knorm2[page][head] holds the largest squared L2 norm of the
-// stored (bf16) keys of that tile; kv_append writes it with the tile.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -20,6 +22,14 @@ namespace ws {
 constexpr int kHeadDim = 128;
 constexpr int kPageTokens = 64;
 constexpr int64_t kPageHeadElems = int64_t(kHeadDim) * kPageTokens;  // 8192
+
+// Element offsets of (slot, d) within a K tile and a V tile.
+__host__ __device__ constexpr int k_tile_index(int slot, int d) {
+  return ((d >> 5) * kPageTokens + slot) * 32 + (d & 31);
+}
+__host__ __device__ constexpr int v_tile_index(int slot, int d) {
+  return ((slot >> 5) * kHeadDim + d) * 32 + (slot & 31);
+}
 
 // Device error flags (ws_cache_check).
 constexpr uint32_t kFlagPositionClamped = 1u;
@@ -105,8 +115,8 @@ struct CombineArgs {
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 // Video path: 256-query tiles on 8 waves, 32x32x16 bf16 MFMA, LDS-staged pages.
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
-// Audio path: 4 waves per (head, 16-query tile, key range), pages streamed
-// through LDS, 16x16x32 / 16x16x16 bf16 MFMA.
+// Audio path: 4 independent waves per (head, 16-query tile, key range),
+// pages loaded straight into registers, 16x16x32 bf16 MFMA.
 hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 
@@ -114,5 +124,6 @@ constexpr int kVideoQTile = 256;
 constexpr int kMaxVideoSplits = 8;  // key-range splits of the video kernel
 constexpr int kVideoWaves = kVideoQTile / 32;
 constexpr int kAudioQTile = 16;
+constexpr int kMaxAudioQ = 64;  // audio queries per call
 
 }  // namespace ws
