@@ -226,25 +226,29 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
 // directly the B operands (eight consecutive keys) of the P*V MFMAs.
 // ------------------------------------------------------------------------- //
 __device__ __forceinline__ int swap23(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
-// LDS stages of the video kernel (a ring of four pages: the previous page,
-// whose V^T the pipelined schedule still reads, the current page, and the
-// next two in flight), filled by direct global->LDS loads
-// (global_load_lds_dwordx4: lane l of a wave writes 16 bytes at base + 16 l).
+// LDS stages of the video kernel (a ring of five pages, 160 KB: the previous
+// page, whose V^T the pipelined schedule still reads, the current page, the
+// next page, already complete so that its first operands can be read before
+// the page barrier, and the two after it in flight), filled by direct
+// global->LDS loads (global_load_lds_dwordx4: lane l of a wave writes 16
+// bytes at base + 16 l).
 //   K    [64 rows][16 chunks]: row R holds key swap23(R); its logical chunk c
 //        (dims 8c..8c+7) sits at position c ^ (R & 15).  Lane i of either
 //        half then reads row i (+32 for the second tile), and the 16 lanes
 //        of a ds_read_b128 pass hit 16 distinct 16-byte bank groups.
 //   V^T  [128 d][8 chunks]: logical chunk c (keys 8c..8c+7) of row d sits at
 //        position c ^ ((d >> 1) & 7).
-constexpr int kStages = 4;
+constexpr int kStages = 5;
 __shared__ __attribute__((aligned(1024))) uint16_t g_k0[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_k1[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_k2[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_k3[kPageTokens * kHeadDim];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k4[kPageTokens * kHeadDim];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v0[kHeadDim * kPageTokens];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v1[kHeadDim * kPageTokens];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v2[kHeadDim * kPageTokens];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v3[kHeadDim * kPageTokens];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v4[kHeadDim * kPageTokens];
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -377,28 +381,29 @@ __device__ __forceinline__ void pin_vgpr(float& x) { asm volatile("" : "+v"(x));
 
 template <int kStage>
 __device__ __forceinline__ uint16_t* stage_k() {
-  return kStage == 0 ? g_k0 : kStage == 1 ? g_k1 : kStage == 2 ? g_k2 : g_k3;
+  return kStage == 0 ? g_k0 : kStage == 1 ? g_k1 : kStage == 2 ? g_k2 : kStage == 3 ? g_k3 : g_k4;
 }
 template <int kStage>
 __device__ __forceinline__ uint16_t* stage_v() {
-  return kStage == 0 ? g_v0 : kStage == 1 ? g_v1 : kStage == 2 ? g_v2 : g_v3;
+  return kStage == 0 ? g_v0 : kStage == 1 ? g_v1 : kStage == 2 ? g_v2 : kStage == 3 ? g_v3 : g_v4;
 }
 __device__ __forceinline__ const uint16_t* stage_v_at(int stage) {
-  return stage == 0 ? g_v0 : stage == 1 ? g_v1 : stage == 2 ? g_v2 : g_v3;
+  return stage == 0 ? g_v0 : stage == 1 ? g_v1 : stage == 2 ? g_v2 : stage == 3 ? g_v3 : g_v4;
 }
 
-// Page list index of the page staged two pages ahead of pi (the range's
-// last page re-stages itself into the idle stage: nothing reads that copy).
-__device__ __forceinline__ int ahead2(int pi, int p_end) { return pi + 2 < p_end ? pi + 2 : p_end - 1; }
+// Page list index of the page staged three pages ahead of pi (near the
+// range's end the last page re-stages itself into an idle stage: nothing
+// reads that copy).
+__device__ __forceinline__ int ahead3(int pi, int p_end) { return pi + 3 < p_end ? pi + 3 : p_end - 1; }
 
 // A page for a wave whose 32 query rows are all padding (ragged last query
-// tile): it only issues its share of the loads of page pi + 2.
+// tile): it only issues its share of the loads of page pi + 3.
 template <int kCur>
 __device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi, int p_end) {
   pi = __builtin_amdgcn_readfirstlane(pi);
-  const int ahead = c.pages[ahead2(pi, p_end)].x;
+  const int ahead = c.pages[ahead3(pi, p_end)].x;
   __syncthreads();
-  stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
+  stage_dma(c, ahead, stage_k<(kCur + 3) % kStages>(), stage_v<(kCur + 3) % kStages>());
   wait_dma_all_but_last_page();
 }
 
@@ -417,22 +422,23 @@ __device__ __forceinline__ void video_page_stage_only(const VideoCtx& c, int pi,
 //     exponentials are taken speculatively against the current m_run; when a
 //     tile raises it by more than kLazyTau (rare after the first tile), a
 //     branch between the phases rescales O and l and recomputes that tile's P.
-// Right after the page's barrier, the direct loads of page pi + 2 into the
-// stage freed by page pi - 1 are issued; at the end of the page each wave
-// waits for its loads of page pi + 1 (issued one page earlier), so every
-// load has two pages to land.  One barrier per page.
+// Right after the page's barrier, the direct loads of page pi + 3 into the
+// stage freed by page pi - 2 are issued; at the end of the page each wave
+// waits for its loads of page pi + 2 (issued one page earlier), so every
+// load has two pages to land and the next page is complete a page before it
+// is used.  One barrier per page.
 template <bool kLazy, int kCur>
 __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, int pi, int p_end) {
   const uint16_t* sk = stage_k<kCur>();
   const uint16_t* sv = stage_v<kCur>();
   pi = __builtin_amdgcn_readfirstlane(pi);
   const int n_valid = c.pages[pi].y;
-  const int ahead = c.pages[ahead2(pi, p_end)].x;
+  const int ahead = c.pages[ahead3(pi, p_end)].x;
   // both scalars are loaded before the barrier: a scalar load left for later
   // would share lgkmcnt with the LDS operand reads
   pin_sgpr(n_valid);
   __syncthreads();
-  stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
+  stage_dma(c, ahead, stage_k<(kCur + 3) % kStages>(), stage_v<(kCur + 3) % kStages>());
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, l32 = c.l32;
 
@@ -581,7 +587,10 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
 // eight MFMAs carries eight exponentials (the softmax VALU then runs in the
 // shadow of the matrix pipe throughout, instead of piling up in two phases).
 // Iteration p (page p from LDS stage kCur, V^T of page p-1 from the stage
-// before it), 32 MFMA steps with operand reads four steps ahead:
+// before it), 32 MFMA steps with operand reads three steps ahead through a
+// ring of four registers; the last three steps read the first operands of
+// page p + 1 (complete since the previous barrier), so the ring runs on
+// across the page barrier:
 //   steps  0- 7  S tile 0 of p                 exp: tile 1 of p-1, keys 0-15
 //   steps  8-11  P*V of p-1, key chunk 2       exp: tile 1 of p-1, keys 16-31
 //   steps 12-15  S tile 1 of p, k-steps 0-3      (same)
@@ -594,8 +603,10 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
 // (kFirst) has no page p-1: steps 0-7 S tile 0, 8-15 S tile 1 with the
 // exponentials of tile 0 keys 0-15, 16-23 P*V chunks 0-1 with those of keys
 // 16-31.  Tile 1 of the last page is finished by video_flush.
+constexpr int kRingAhead = 3;  // operand reads issued this many MFMA steps ahead
 struct PipeState {
   f32x16 s1;      // S tile 1 of the previous page (exp2 argument)
+  bf16x8 ring[kRingAhead + 1];  // operands in flight (slot = step % 4)
 };
 
 template <int kCur, bool kFirst>
@@ -605,23 +616,28 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
   const uint16_t* sk = stage_k<kCur>();
   const uint16_t* sv = stage_v<kCur>();
   const uint16_t* svp = stage_v<kPrev>();
+  constexpr int kNext = (kCur + 1) % kStages;
+  const uint16_t* skn = stage_k<kNext>();
   pi = __builtin_amdgcn_readfirstlane(pi);
-  const int ahead = c.pages[ahead2(pi, p_end)].x;
+  const int ahead = c.pages[ahead3(pi, p_end)].x;
   pin_sgpr(ahead);
   __syncthreads();
-  stage_dma(c, ahead, stage_k<(kCur + 2) % kStages>(), stage_v<(kCur + 2) % kStages>());
+  stage_dma(c, ahead, stage_k<(kCur + 3) % kStages>(), stage_v<(kCur + 3) % kStages>());
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, l32 = c.l32;
-  auto kread = [&](int n) {  // S k-step n % 8 of tile n / 8
+  auto kread_at = [&](const uint16_t* k, int n) {  // S k-step n % 8 of tile n / 8
     const int row = n < 8 ? l32 : 32 + l32;
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(sk + row * kHeadDim + 8 * ((2 * (n & 7) + half) ^ (l32 & 15))));
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(k + row * kHeadDim + 8 * ((2 * (n & 7) + half) ^ (l32 & 15))));
   };
+  auto kread = [&](int n) { return kread_at(sk, n); };
   auto vread = [&](const uint16_t* v, int t4, int jc) {  // d tile t4, key chunk jc
     const int d = 32 * t4 + l32;
     return as_bf16x8(*reinterpret_cast<const u32x4*>(v + d * kPageTokens + 8 * ((2 * jc + half) ^ ((l32 >> 1) & 7))));
   };
   constexpr int kSteps = kFirst ? 24 : 32;
+  static_assert(kSteps % (kRingAhead + 1) == 0, "ring slots must line up across iterations");
   auto oread = [&](int o) {
+    if (o >= kSteps) return kread_at(skn, o - kSteps);  // page p + 1, first S steps
     if (kFirst) return o < 16 ? kread(o) : vread(sv, (o - 16) & 3, (o - 16) >> 2);
     if (o < 8) return kread(o);
     if (o < 12) return vread(svp, o - 8, 2);
@@ -630,10 +646,12 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
     if (o < 24) return kread(12 + o - 20);
     return vread(sv, (o - 24) & 3, (o - 24) >> 2);
   };
-  constexpr int kAhead = 4;
-  bf16x8 ring[kAhead + 1];
+  constexpr int kAhead = kRingAhead;
+  bf16x8* ring = ps.ring;
+  if (kFirst) {  // the range's first page: nothing was read ahead
 #pragma unroll
-  for (int o = 0; o < kAhead; ++o) ring[o] = oread(o);
+    for (int o = 0; o < kAhead; ++o) ring[o] = oread(o);
+  }
   __builtin_amdgcn_sched_barrier(0);
 
   // The first MFMA of each S tile takes its accumulator input from s_init
@@ -660,8 +678,8 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
 
 #pragma unroll
   for (int o = 0; o < kSteps; ++o) {
-    if (o + kAhead < kSteps) ring[(o + kAhead) % (kAhead + 1)] = oread(o + kAhead);
     const bf16x8 a = ring[o % (kAhead + 1)];
+    ring[(o + kAhead) % (kAhead + 1)] = oread(o + kAhead);
     if (kFirst) {
       if (o < 8) {
         s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
@@ -755,11 +773,12 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
     c.dma_v = 2 * v_tile_index(8 * ((lane & 7) ^ ((d0 >> 1) & 7)), d0);
   }
 
-  // The first two pages are requested before anything else, so that their
+  // The first three pages are requested before anything else, so that their
   // latency overlaps the query prologue.
   if (p_begin < p_end) {
     stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[p_begin].x), g_k0, g_v0);
     stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 1, p_end - 1)].x), g_k1, g_v1);
+    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 2, p_end - 1)].x), g_k2, g_v2);
   }
 
   // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
@@ -865,11 +884,12 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 #pragma unroll
       for (int r = 0; r < 16; ++r) s_init[r] = -st.m_run;
       video_iter<0, true>(c, st, ps, s_init, p_begin, p_end);
-      for (int pi = p_begin + 1; pi < p_end; pi += 4) {
+      for (int pi = p_begin + 1; pi < p_end; pi += 5) {
         video_iter<1, false>(c, st, ps, s_init, pi, p_end);
         if (pi + 1 < p_end) video_iter<2, false>(c, st, ps, s_init, pi + 1, p_end);
         if (pi + 2 < p_end) video_iter<3, false>(c, st, ps, s_init, pi + 2, p_end);
-        if (pi + 3 < p_end) video_iter<0, false>(c, st, ps, s_init, pi + 3, p_end);
+        if (pi + 3 < p_end) video_iter<4, false>(c, st, ps, s_init, pi + 3, p_end);
+        if (pi + 4 < p_end) video_iter<0, false>(c, st, ps, s_init, pi + 4, p_end);
       }
       video_flush(c, st, ps, (p_end - 1 - p_begin) % kStages);
       // Tail slots past a page's valid tokens are not masked: their stored
@@ -881,18 +901,20 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
       st.l_run -= 0.5f * static_cast<float>(n_empty) * p_empty;
     }
   } else if (c.active) {
-    for (int pi = p_begin; pi < p_end; pi += 4) {
+    for (int pi = p_begin; pi < p_end; pi += 5) {
       video_page<true, 0>(c, st, pi, p_end);
       if (pi + 1 < p_end) video_page<true, 1>(c, st, pi + 1, p_end);
       if (pi + 2 < p_end) video_page<true, 2>(c, st, pi + 2, p_end);
       if (pi + 3 < p_end) video_page<true, 3>(c, st, pi + 3, p_end);
+      if (pi + 4 < p_end) video_page<true, 4>(c, st, pi + 4, p_end);
     }
   } else {
-    for (int pi = p_begin; pi < p_end; pi += 4) {
+    for (int pi = p_begin; pi < p_end; pi += 5) {
       video_page_stage_only<0>(c, pi, p_end);
       if (pi + 1 < p_end) video_page_stage_only<1>(c, pi + 1, p_end);
       if (pi + 2 < p_end) video_page_stage_only<2>(c, pi + 2, p_end);
       if (pi + 3 < p_end) video_page_stage_only<3>(c, pi + 3, p_end);
+      if (pi + 4 < p_end) video_page_stage_only<4>(c, pi + 4, p_end);
     }
   }
   // no direct load may still be writing this workgroup's LDS when it exits
