@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--video-splits", type=int, default=0)
     ap.add_argument("--audio-splits", type=int, default=0)
     ap.add_argument("--cold-audio-reps", type=int, default=20)
+    ap.add_argument("--long-reps", type=int, default=5)
     return ap.parse_args()
 
 
@@ -84,6 +85,52 @@ def cpu_baseline(budget_s=12.0):
             "kind": "oracle",
             "sample": f"{heads} of {H} heads of the video attention ({LU} queries x {lk} keys, "
                       f"fp64, with those heads' Q/K RMS-norm and rotary): {dt:.1f} s"}
+
+
+def long_history(args, ws, sets, gamma, eps, stream, dev):
+    """Long-history stress: 32 committed history units (256 + 33 x 920 =
+    30616 keys) and 4 denoising steps issued back-to-back on one stream, each
+    rewriting the current unit's K/V in place (append with RMS-norm + rotary)
+    and running the video attention.  Timed with events around the 4 steps;
+    the median of `long_reps` repetitions.  The history reuses the two
+    resident input sets (values do not change the timing)."""
+    import torch
+    from paper_2607_04443_amd import synth
+    hist_l = 32
+    cache = ws.Cache(H, 4 + (hist_l + 2) * 16 + 8, max_q_tokens=1024)
+    pos = [torch.from_numpy(synth.video_positions(u, GRID)).to(dev) for u in range(hist_l + 1)]
+    s0 = sets[0]
+    cache.append(0, ws.WS_KIND_COND, s0["ck"], s0["cv"], ws.WS_APPEND_RAW)
+    for u in range(hist_l):
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, pos[u], gamma, eps)
+        cache.commit(u)
+    out = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
+    mask = ws.mask_spec(hist_l, 0, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
+
+    def four_steps():
+        for step in range(4):
+            s = sets[step % 2]
+            cache.append(hist_l, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, pos[hist_l],
+                         gamma, eps)
+            cache.unit_attention(s["q"], out, mask, ws.WS_APPEND_NORM_ROPE, pos[hist_l], gamma, eps)
+
+    four_steps()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(args.long_reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        four_steps()
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b) * 1e3)
+    cache.close()
+    times.sort()
+    med = times[len(times) // 2]
+    lk = COND + (hist_l + 1) * LU
+    return {"keys": lk, "us_4_steps": med, "us_per_step": med / 4,
+            "tflops": 4 * video_flop(LU, lk) / (med * 1e-6) / 1e12}
 
 
 def main():
@@ -234,6 +281,8 @@ def main():
                 "frac_hbm": audio_bytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBS, "keys": lk_a}
         del scrub
 
+    long_hist = long_history(args, ws, sets, gamma, eps, stream, dev) if args.long_reps > 0 else None
+
     t_vkern, t_vmerge = kernel_us("video", "attn_us"), kernel_us("video", "merge_us")
     v_splits = sorted({c["n_splits"] for c in calls if c["path"] == "video"})
     achieved = fv / (t_vkern * 1e-6) / 1e12
@@ -260,6 +309,7 @@ def main():
         "audio_attention": {"us_warm": t_audio, "gbps_warm": audio_bytes / (t_audio * 1e-6) / 1e9,
                             "bytes": audio_bytes, "cold": cold},
         "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
+        "long_history": long_hist,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},

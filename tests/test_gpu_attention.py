@@ -41,6 +41,43 @@ def test_video_parity(ws, name, heads):
         L.close()
 
 
+def test_long_history_back_to_back_steps(ws):
+    """32 history units (30616 keys) and 4 denoising steps issued one after
+    another on one stream, each rewriting the current unit's K/V in place
+    (the appends and attentions of all steps are enqueued before the first
+    read-back).  Heads 0, 13, 26, 39 of steps 0 and 3 against the oracle,
+    which applies the same rewrites to its logical cache."""
+    import torch
+    wl = synth.make_workload("long32")
+    heads = [0, 13, 26, 39]
+    L = Loaded(ws, wl)
+    try:
+        outs = []
+        for s, st in enumerate(wl.steps):
+            if s > 0:
+                for seg in st.segments:
+                    L.append(seg)  # same (unit, kind): rewritten in place
+            q, pos = to_dev(st.q_video), dev_i32(st.q_video_pos)
+            out = torch.full_like(q, float("nan"))
+            L._keep += [q, pos]
+            L.cache.unit_attention(q, out, ws.mask_spec(wl.current_unit, -(2 ** 31), VIDEO_KINDS),
+                                   ws.WS_APPEND_NORM_ROPE, pos, L.gq, wl.eps)
+            outs.append(out)
+        torch.cuda.synchronize()
+        # the oracle cache holds the last step's K/V: check step 3 first
+        st = wl.steps[3]
+        ref = L.oracle(st.q_video, st.q_video_pos, wl.current_unit, VIDEO_KINDS, heads=heads)
+        print("step 3", assert_gates(bf16_f64(from_dev(outs[3]))[:, heads], ref, label="long32 step 3"))
+        st0 = wl.steps[0]
+        for seg in st0.segments:
+            L.ocache.append(seg.unit, seg.kind, seg.k, seg.v, oracle.MODE_NORM_ROPE, seg.positions,
+                            wl.gamma_k.astype(np.float64), wl.eps)
+        ref = L.oracle(st0.q_video, st0.q_video_pos, wl.current_unit, VIDEO_KINDS, heads=heads)
+        print("step 0", assert_gates(bf16_f64(from_dev(outs[0]))[:, heads], ref, label="long32 step 0"))
+    finally:
+        L.close()
+
+
 @pytest.mark.parametrize("variant", ["seeded", "sharp"])
 def test_video_parity_gamma_variants(ws, variant):
     wl = synth.make_workload("v01", variant=variant)
