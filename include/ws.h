@@ -140,7 +140,8 @@ typedef struct ws_cache_stats {
 /* Tuning knobs (0 = automatic choice).  They change scheduling only, never
  * results beyond floating-point summation order. */
 typedef enum ws_option {
-  WS_OPT_VIDEO_KV_SPLITS = 0,  /* key-range splits of the video kernel (1..8) */
+  WS_OPT_VIDEO_KV_SPLITS = 0,  /* video kernel: split every head's keys into this many
+                                  equal ranges (1..8) instead of the balanced share */
   WS_OPT_AUDIO_KV_SPLITS = 1,  /* key-range splits of the audio kernel (1..512) */
   /* Softmax shift of the video kernel: 0 = automatic (a query row's logit
    * bound |q''| * max |k| when it is at most 40 in log2 units, else a lazily
@@ -210,8 +211,9 @@ WS_API ws_status ws_kv_release(ws_cache* cache, int32_t unit, ws_kind kind);
  *   q:   device bf16 [n_q][H][128] with strides (q_tok_stride, q_head_stride).
  *   out: device bf16 [n_q][H][128] with strides (out_tok_stride, out_head_stride).
  * 1 <= n_q <= max_q_tokens.  MFMA flash kernel: 256-query tiles, 64-key pages.
- * A head's keys may be split into ranges (split-KV), merged by log-sum-exp
- * in a second kernel.
+ * Groups of workgroups (one per query tile) take even shares of the
+ * (head, page) work, so a head's keys may be split into ranges (split-KV);
+ * those are merged by log-sum-exp in a second kernel.
  * The softmax shift of a query row is its logit bound |Q''_i| * max |K'_j|
  * (Cauchy-Schwarz over the pages of one key range) when that bound is at most
  * 40 in log2 units, else a lazily raised running maximum
@@ -257,7 +259,7 @@ WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t val
  * (older calls are overwritten); recording adds no synchronization. */
 typedef struct ws_call_timing {
   int32_t path;      /* 0 = ws_unit_attention (video), 1 = ws_audio_attention */
-  int32_t n_splits;  /* key-range splits of the call (1 = video without merge) */
+  int32_t n_splits;  /* audio: key-range splits; video: workgroup groups */
   float attn_us;     /* attention kernel, microseconds */
   float merge_us;    /* merge kernel, microseconds (0 when there is none) */
 } ws_call_timing;

@@ -741,17 +741,29 @@ __device__ __forceinline__ void video_flush(const VideoCtx& c, VideoState& st, c
   }
 }
 
-// The work of one video workgroup: query tile `qtile` of head `head` against
-// pages [p_begin, p_end) of the visible list, which is key range `seg` of the
-// n_seg ranges that split this head's pages.  With one range the output is
-// written in bf16; otherwise the softmax-normalised fp32 partial and its
-// log-sum-exp go to the split-KV workspace for the combine kernel.
+// One segment of a video workgroup's work: query tile `qtile` of head `head`
+// against pages [p_begin, p_end) of the visible list, which is key range `seg`
+// of the n_seg ranges that split this head's pages.  With one range the
+// output is written in bf16; otherwise the softmax-normalised fp32 partial and
+// its log-sum-exp go to the split-KV workspace for the combine kernel.
 struct VideoSeg {
   int head, p_begin, p_end, seg, n_seg;
 };
 
-__device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg& sg, int qtile) {
-  const int tid = threadIdx.x;
+// The first of `groups` even shares of `units` (share g = [g U / G,
+// (g+1) U / G)) that holds unit x.  Used by the video kernel and by the
+// combine kernel, which must agree on how many key ranges a head has.
+__device__ __forceinline__ int64_t video_group_of(int64_t x, int64_t groups, int64_t units) {
+  return ((x + 1) * groups + units - 1) / units - 1;
+}
+
+__device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg& sg, int qtile,
+                                              bool first_segment) {
+  // Lane-derived values (LDS and load offsets) are recomputed per segment:
+  // kept live across the segment loop they would push the page loop into
+  // register spills.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, l32 = lane & 31;
@@ -774,7 +786,9 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   }
 
   // The first three pages are requested before anything else, so that their
-  // latency overlaps the query prologue.
+  // latency overlaps the query prologue.  A later segment first waits for
+  // every wave to be done with the previous segment's stages.
+  if (!first_segment) __syncthreads();
   if (p_begin < p_end) {
     stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[p_begin].x), g_k0, g_v0);
     stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 1, p_end - 1)].x), g_k1, g_v1);
@@ -954,20 +968,39 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 }
 
 __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
-  // Work decode.  Workgroups are dispatched round-robin over the 8 XCDs;
-  // renumber so that each XCD owns a contiguous run of (head, query tile,
-  // key range) items, i.e. whole heads: the query tiles of a head then read
-  // the same pages at about the same time, through that XCD's L2.
+  // Work decode.  The grid is n_groups groups of n_qtiles workgroups; group g
+  // takes the (head, page) units [g U / G, (g+1) U / G) of the head-major
+  // order (U = heads x visible pages, G = n_groups), one workgroup per query
+  // tile, so every workgroup gets an even share of the pages in a single
+  // round, and a share that crosses a head boundary is processed as two
+  // segments.  Workgroups are dispatched round-robin over the 8 XCDs;
+  // renumber so that consecutive work items (the query tiles of a group,
+  // which read the same pages at the same time, and neighbouring groups) run
+  // on one XCD and share its L2.
   const int nblk = gridDim.x, bid = blockIdx.x;
   const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
   const int item = xcd * per + min(xcd, rem) + (bid >> 3);
-  const int split = item % a.n_splits;
-  const int rest = item / a.n_splits;
-  const int qtile = rest % a.n_qtiles;
-  const int head = rest / a.n_qtiles;
-  const int p_begin = split * a.pages_per_split;
-  const int p_end = min(a.n_pages, p_begin + a.pages_per_split);
-  video_segment(a, VideoSeg{head, p_begin, p_end, split, a.n_splits}, qtile);
+  const int qtile = item % a.n_qtiles;
+  const int64_t group = item / a.n_qtiles;
+  const int64_t n_pages = a.n_pages;
+  if (n_pages == 0) {  // nothing visible: one empty segment per head, output 0
+    if (group < a.num_heads)
+      video_segment(a, VideoSeg{static_cast<int>(group), 0, 0, 0, 1}, qtile, true);
+    return;
+  }
+  const int64_t units = static_cast<int64_t>(a.num_heads) * n_pages, groups = a.n_groups;
+  const int64_t lo = group * units / groups, hi = (group + 1) * units / groups;
+  bool first = true;
+  for (int64_t x = lo; x < hi; first = false) {
+    const int64_t head = x / n_pages, h0 = head * n_pages;
+    const int64_t x_end = min(hi, h0 + n_pages);
+    const int64_t g_first = video_group_of(h0, groups, units);
+    const int64_t g_last = video_group_of(h0 + n_pages - 1, groups, units);
+    const VideoSeg sg{static_cast<int>(head), static_cast<int>(x - h0), static_cast<int>(x_end - h0),
+                      static_cast<int>(group - g_first), static_cast<int>(g_last - g_first + 1)};
+    video_segment(a, sg, qtile, first);
+    x = x_end;
+  }
 }
 
 // ------------------------------------------------------------------------- //
@@ -1250,10 +1283,20 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
   const bool row_ok = row < a.num_heads * a.n_q;
   const int d0 = 4 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
+  // Key ranges of this row's head: n_splits, or under the video schedule the
+  // number of groups whose share holds some of the head's pages (a head in
+  // one range was written in bf16 by the attention kernel: nothing to merge).
+  int n_splits = a.n_splits;
+  if (a.n_groups > 0 && row_ok) {
+    const int64_t units = static_cast<int64_t>(a.num_heads) * a.n_pages, h0 = static_cast<int64_t>(row / a.n_q) * a.n_pages;
+    n_splits = static_cast<int>(video_group_of(h0 + a.n_pages - 1, a.n_groups, units) -
+                                video_group_of(h0, a.n_groups, units) + 1);
+  }
+  const bool active = row_ok && (a.n_groups == 0 || n_splits > 1);
   float mx = kNegInf, wsum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (row_ok) {
-    for (int sp = g; sp < a.n_splits; sp += kGroups) {
+  if (active) {
+    for (int sp = g; sp < n_splits; sp += kGroups) {
       const float l = a.part_lse[sp * split_stride + row];
       if (l == kNegInf) continue;
       const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + (sp * split_stride + row) * kHeadDim + d0);
@@ -1291,7 +1334,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
     }
     mx = big;
   }
-  if (!row_ok) return;
+  if (!active) return;
   const int head = row / a.n_q, q = row % a.n_q;
   if (mx != kNegInf) acc *= 1.0f / wsum;
   u32x2 w;
@@ -1309,7 +1352,7 @@ hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_qtiles * a.num_heads * a.n_splits);
+  dim3 grid(a.n_qtiles * a.n_groups);
   hipLaunchKernelGGL(unit_attn_kernel, grid, dim3(kVideoWaves * 64), 0, stream, a);
   return hipGetLastError();
 }

@@ -304,26 +304,36 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
   return WS_OK;
 }
 
-int choose_video_splits(const ws_cache* c, int n_items, int n_pages) {
-  if (c->opt_video_splits > 0) return c->opt_video_splits;
-  // One workgroup per CU: a split count s runs in ceil(items * s / CUs)
-  // rounds of ceil(pages / s) pages each, plus a fixed per-item cost (query
-  // prologue, pipeline fill, partial write-back and merge) worth about ten
-  // pages (measured on MI355X for 1..33 history units of 920 tokens x 40
-  // heads).  Pick the s with the smallest estimate.
-  constexpr int64_t kItemCostPages = 10;
-  int best = 1;
-  int64_t best_cost = -1;
-  for (int s = 1; s <= kMaxVideoSplits; ++s) {
-    const int64_t rounds = (static_cast<int64_t>(n_items) * s + c->num_cus - 1) / c->num_cus;
-    const int64_t cost = rounds * ((n_pages + s - 1) / s + kItemCostPages);
-    if (best_cost < 0 || cost < best_cost) {
-      best = s;
+// Number of workgroup groups of the video kernel (a group is one workgroup
+// per query tile; together the groups share the (head, page) units evenly).
+// One round of groups fits the CUs when groups * n_qtiles <= CUs.  A group
+// whose share crosses a head boundary pays one more query prologue, pipeline
+// fill and partial write-back, worth about kSegCostPages pages (measured on
+// MI355X: ~15 us against ~1.6 us per page), and every head split into more
+// than one range is merged by the combine kernel.  A forced split count s
+// gives H * s groups: every head in s equal key ranges.
+int choose_video_groups(const ws_cache* c, int n_heads, int n_qtiles, int n_pages) {
+  if (n_pages == 0) return n_heads;
+  if (c->opt_video_splits > 0) return n_heads * c->opt_video_splits;
+  constexpr double kSegCostPages = 9.5;
+  constexpr int64_t kMinGroupPages = 4;
+  const int64_t units = static_cast<int64_t>(n_heads) * n_pages;
+  const int64_t one_round = std::max<int64_t>(1, c->num_cus / n_qtiles);
+  // at most kMaxVideoSplits ranges per head: ceil(G / H) + 1 <= kMaxVideoSplits
+  const int64_t g_max = std::min<int64_t>({static_cast<int64_t>(n_heads) * (kMaxVideoSplits - 1),
+                                           std::max<int64_t>(1, units / kMinGroupPages), 4 * one_round});
+  int64_t best = std::min<int64_t>(n_heads, g_max);
+  double best_cost = -1.0;
+  for (int64_t g = 1; g <= g_max; ++g) {
+    const double rounds = static_cast<double>((g + one_round - 1) / one_round);
+    const double segs = static_cast<double>(g + std::min<int64_t>(g, n_heads) - 1) / g;
+    const double cost = rounds * (static_cast<double>(units) / g + kSegCostPages * segs);
+    if (best_cost < 0 || cost < best_cost - 1e-9) {
+      best = g;
       best_cost = cost;
     }
-    if (s >= n_pages) break;
   }
-  return best;
+  return static_cast<int>(best);
 }
 
 int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
@@ -392,14 +402,30 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   a.n_qtiles = (n_q + qtile - 1) / qtile;
   const int n_items = a.n_qtiles * H;
   const int64_t cap = c->part_rows / (static_cast<int64_t>(H) * n_q);
-  int splits = audio ? choose_audio_splits(c, n_items, n_pages) : choose_video_splits(c, n_items, n_pages);
-  splits = std::max(1, std::min(splits, std::max(1, n_pages)));
-  splits = static_cast<int>(std::min<int64_t>(splits, std::max<int64_t>(cap, 1)));
-  const int pps = n_pages > 0 ? (n_pages + splits - 1) / splits : 0;
-  splits = pps > 0 ? (n_pages + pps - 1) / pps : 1;  // no empty splits
-  if (cap < splits) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
-  a.n_splits = splits;
-  a.pages_per_split = pps;
+  int splits = 1;         // audio: key ranges; video: workgroup groups
+  bool merge = audio;
+  if (audio) {
+    splits = choose_audio_splits(c, n_items, n_pages);
+    splits = std::max(1, std::min(splits, std::max(1, n_pages)));
+    splits = static_cast<int>(std::min<int64_t>(splits, std::max<int64_t>(cap, 1)));
+    const int pps = n_pages > 0 ? (n_pages + splits - 1) / splits : 0;
+    splits = pps > 0 ? (n_pages + pps - 1) / pps : 1;  // no empty splits
+    if (cap < splits) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
+    a.n_splits = splits;
+    a.pages_per_split = pps;
+  } else {
+    const int groups = choose_video_groups(c, H, a.n_qtiles, n_pages);
+    // ranges per head: exactly the forced split count, else at most
+    // ceil(groups / H) + 1 (a share of at most one head's pages meets at
+    // most two heads); a single range writes bf16 directly
+    const int64_t max_ranges = c->opt_video_splits > 0 ? c->opt_video_splits
+                               : std::max<int64_t>(2, (groups + H - 1) / H + 1);
+    if (cap < max_ranges) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
+    a.n_groups = groups;
+    a.n_splits = 1;
+    splits = groups;
+    merge = n_pages > 0 && groups != H;
+  }
 
   TimingRing& tr = c->timing;
   const int slot = tr.cap > 0 ? tr.next : -1;
@@ -410,11 +436,14 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   hipError_t e = audio ? ws::launch_audio_attention(a, stream) : ws::launch_unit_attention(a, stream);
   if (e != hipSuccess) return hip_fail(e, audio ? "audio_attn launch" : "unit_attn launch");
   if (slot >= 0) WS_HIP(hipEventRecord(tr.ev[3 * slot + 1], stream));
-  if (audio || splits > 1) {
+  if (merge) {
     ws::CombineArgs cb{};
     cb.part_o = c->part_o;
     cb.part_lse = c->part_lse;
-    cb.n_splits = splits;
+    cb.n_splits = audio ? splits : static_cast<int>(std::min<int64_t>(
+                                       kMaxVideoSplits, (splits + H - 1) / H + 1));
+    cb.n_groups = audio ? 0 : splits;
+    cb.n_pages = n_pages;
     cb.n_q = n_q;
     cb.num_heads = H;
     cb.out = a.out;

@@ -90,8 +90,9 @@ struct AttnArgs {
   const int2* pages;     // visible pages: (page id, valid tokens)
   const uint16_t* zeros; // 1 KB of zeros (direct-load source for empty blocks)
   int32_t n_pages;
-  int32_t n_splits;      // key-range splits (1: video writes bf16 output directly)
+  int32_t n_splits;      // audio: key-range splits (the combine kernel merges them)
   int32_t pages_per_split;
+  int32_t n_groups;      // video: workgroup groups sharing the (head, page) units
   int32_t n_qtiles;
   uint16_t* out;
   int64_t out_tok_stride;
@@ -104,7 +105,9 @@ struct AttnArgs {
 struct CombineArgs {
   const float* part_o;
   const float* part_lse;
-  int32_t n_splits;
+  int32_t n_splits;      // key ranges per head (when n_groups == 0)
+  int32_t n_groups;      // > 0: video schedule, ranges per head follow from
+  int32_t n_pages;       //      the groups' even shares of heads x n_pages
   int32_t n_q;
   int32_t num_heads;
   uint16_t* out;
@@ -113,7 +116,9 @@ struct CombineArgs {
 };
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
-// Video path: 256-query tiles on 8 waves, 32x32x16 bf16 MFMA, LDS-staged pages.
+// Video path: 256-query tiles on 8 waves, 32x32x16 bf16 MFMA, LDS-staged
+// pages; n_groups x n_qtiles workgroups, each with an even share of the
+// (head, page) units.
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
 // Audio path: 4 independent waves per (head, 16-query tile, key range),
 // pages loaded straight into registers, 16x16x32 bf16 MFMA.
