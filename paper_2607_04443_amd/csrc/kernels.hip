@@ -952,17 +952,23 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
       }
     return;
   }
+  // Partial of a key range: the softmax-normalised O rounded to bf16 (a
+  // convex combination of V rows, so bf16 keeps its range; the merge adds at
+  // most one more bf16 rounding of the output's size) and its fp32
+  // log-sum-exp.  Half the bytes of fp32 partials, written here and read by
+  // the combine kernel.
   if (!q_ok) return;
   const int64_t row = (static_cast<int64_t>(sg.seg) * a.num_heads + head) * a.n_q + q;
-  float* po = a.part_o + row * kHeadDim;
+  uint16_t* po = reinterpret_cast<uint16_t*>(a.part_o) + row * kHeadDim;
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int d0 = 32 * t + 8 * g + 4 * half;
-      *reinterpret_cast<f32x4*>(po + d0) =
-          (f32x4){st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv, st.o[t][4 * g + 2] * inv,
-                  st.o[t][4 * g + 3] * inv};
+      u32x2 w;
+      w[0] = pack_bf16(st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv);
+      w[1] = pack_bf16(st.o[t][4 * g + 2] * inv, st.o[t][4 * g + 3] * inv);
+      *reinterpret_cast<u32x2*>(po + d0) = w;
     }
   if (half == 0) a.part_lse[row] = l_tot > 0.f ? st.m_run + __log2f(l_tot) : kNegInf;
 }
@@ -1283,20 +1289,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
   const bool row_ok = row < a.num_heads * a.n_q;
   const int d0 = 4 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
-  // Key ranges of this row's head: n_splits, or under the video schedule the
-  // number of groups whose share holds some of the head's pages (a head in
-  // one range was written in bf16 by the attention kernel: nothing to merge).
-  int n_splits = a.n_splits;
-  if (a.n_groups > 0 && row_ok) {
-    const int64_t units = static_cast<int64_t>(a.num_heads) * a.n_pages, h0 = static_cast<int64_t>(row / a.n_q) * a.n_pages;
-    n_splits = static_cast<int>(video_group_of(h0 + a.n_pages - 1, a.n_groups, units) -
-                                video_group_of(h0, a.n_groups, units) + 1);
-  }
-  const bool active = row_ok && (a.n_groups == 0 || n_splits > 1);
   float mx = kNegInf, wsum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (active) {
-    for (int sp = g; sp < n_splits; sp += kGroups) {
+  if (row_ok) {
+    for (int sp = g; sp < a.n_splits; sp += kGroups) {
       const float l = a.part_lse[sp * split_stride + row];
       if (l == kNegInf) continue;
       const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + (sp * split_stride + row) * kHeadDim + d0);
@@ -1334,13 +1330,66 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
     }
     mx = big;
   }
-  if (!active) return;
+  if (!row_ok) return;
   const int head = row / a.n_q, q = row % a.n_q;
   if (mx != kNegInf) acc *= 1.0f / wsum;
   u32x2 w;
   w[0] = pack_bf16(acc[0], acc[1]);
   w[1] = pack_bf16(acc[2], acc[3]);
   *reinterpret_cast<u32x2*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = w;
+}
+
+// ------------------------------------------------------------------------- //
+// video_combine: merges the key ranges of the video schedule.  A head's
+// range count follows from the groups' even shares of heads x pages (a head
+// in one range was written in bf16 by the attention kernel: nothing to
+// merge).  32 threads per (head, query) row, 4 d each, 8 rows per block; all
+// of a row's (at most kMaxVideoSplits) partials are requested before any is
+// used.
+// ------------------------------------------------------------------------- //
+__global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a) {
+  const int lane = threadIdx.x & 31;
+  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
+  if (row >= a.num_heads * a.n_q) return;
+  const int head = row / a.n_q, q = row % a.n_q;
+  const int64_t units = static_cast<int64_t>(a.num_heads) * a.n_pages, h0 = static_cast<int64_t>(head) * a.n_pages;
+  const int n_ranges = static_cast<int>(video_group_of(h0 + a.n_pages - 1, a.n_groups, units) -
+                                        video_group_of(h0, a.n_groups, units) + 1);
+  if (n_ranges < 2) return;
+  const int d0 = 4 * lane;
+  const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
+  const uint16_t* po = reinterpret_cast<const uint16_t*>(a.part_o);
+  float l[kMaxVideoSplits];
+  u32x2 w[kMaxVideoSplits];
+#pragma unroll
+  for (int sp = 0; sp < kMaxVideoSplits; ++sp) {
+    if (sp < n_ranges) {
+      l[sp] = a.part_lse[sp * split_stride + row];
+      w[sp] = *reinterpret_cast<const u32x2*>(po + (sp * split_stride + row) * kHeadDim + d0);
+    } else {
+      l[sp] = kNegInf;
+      w[sp] = (u32x2){0u, 0u};
+    }
+  }
+  float mx = kNegInf;
+#pragma unroll
+  for (int sp = 0; sp < kMaxVideoSplits; ++sp) mx = fmaxf(mx, l[sp]);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (mx != kNegInf) {
+    float wsum = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < kMaxVideoSplits; ++sp) {
+      if (l[sp] == kNegInf) continue;
+      const float e = fast_exp2(l[sp] - mx);
+      acc += e * (f32x4){bf16_lo(w[sp][0]), bf16_hi(w[sp][0]), bf16_lo(w[sp][1]), bf16_hi(w[sp][1])};
+      wsum += e;
+    }
+    acc *= 1.0f / wsum;
+  }
+  u32x2 o;
+  o[0] = pack_bf16(acc[0], acc[1]);
+  o[1] = pack_bf16(acc[2], acc[3]);
+  *reinterpret_cast<u32x2*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = o;
 }
 
 }  // namespace
@@ -1365,6 +1414,10 @@ hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   const int rows = a.num_heads * a.n_q;
+  if (a.n_groups > 0) {
+    hipLaunchKernelGGL(video_combine_kernel, dim3((rows + 7) / 8), dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
   int groups = 1;
   if (rows < 4096) groups = a.n_splits >= 8 ? 8 : a.n_splits >= 4 ? 4 : a.n_splits >= 2 ? 2 : 1;
   const int rows_per_block = 8 / groups;

@@ -97,7 +97,7 @@ struct AttnArgs {
   uint16_t* out;
   int64_t out_tok_stride;
   int64_t out_head_stride;
-  float* part_o;         // [split][head][n_q][128] fp32, normalised
+  float* part_o;         // [split][head][n_q][128], normalised: fp32 (audio), bf16 (video)
   float* part_lse;       // [split][head][n_q], log2 domain (scaled logits)
   uint32_t* flags;
 };
