@@ -785,36 +785,72 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
     c.dma_v = 2 * v_tile_index(8 * ((lane & 7) ^ ((d0 >> 1) & 7)), d0);
   }
 
-  // The first three pages are requested before anything else, so that their
-  // latency overlaps the query prologue.  A later segment first waits for
-  // every wave to be done with the previous segment's stages.
-  if (!first_segment) __syncthreads();
+  // Prologue loads, issued so that no dependent load waits behind an
+  // unrelated one (vector memory counters complete in order): the page-list
+  // entries of the first three pages are scalar loads; then every
+  // independent vector load (positions, the page-list entries of the
+  // key-norm scan, Q, gamma); then the direct loads of the first three pages
+  // (a later segment first waits for every wave to be done with the
+  // previous segment's stages); then the loads that depend on the first
+  // batch (key norms, rotary table entries).
+  int pg_first[3] = {0, 0, 0};
   if (p_begin < p_end) {
-    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[p_begin].x), g_k0, g_v0);
-    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 1, p_end - 1)].x), g_k1, g_v1);
-    stage_dma(c, __builtin_amdgcn_readfirstlane(a.pages[min(p_begin + 2, p_end - 1)].x), g_k2, g_v2);
+#pragma unroll
+    for (int k = 0; k < 3; ++k) pg_first[k] = c.pages[min(p_begin + k, p_end - 1)].x;
   }
-
-  // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
   const int q = qtile * kVideoQTile + wave * 32 + l32;
   const bool q_ok = q < a.n_q;
+  const bool norm_rope = a.mode == 1;
+  int3 qpos = make_int3(0, 0, 0);
+  if (norm_rope && q_ok) qpos = make_int3(a.positions[3 * q], a.positions[3 * q + 1], a.positions[3 * q + 2]);
+  // the segment's page-list entries (two per lane in the first pass)
+  int2 pgl[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int pi = p_begin + lane + 64 * k;
+    pgl[k] = pi < p_end ? a.pages[pi] : make_int2(-1, kPageTokens);
+  }
   u32x4 qraw[8];
   const uint16_t* qp = a.q + q * a.q_tok_stride + head * a.q_head_stride + 8 * half;
 #pragma unroll
   for (int s = 0; s < 8; ++s)
     qraw[s] = q_ok ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : (u32x4){0u, 0u, 0u, 0u};
-  // the range's page-list entries, for the softmax shift below
-  int2 pg_mine = make_int2(0, kPageTokens);
+  float gam[8][8];
+  if (norm_rope) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const float4 g0 = *reinterpret_cast<const float4*>(a.gamma + 16 * s + 8 * half);
+      const float4 g1 = *reinterpret_cast<const float4*>(a.gamma + 16 * s + 8 * half + 4);
+      gam[s][0] = g0.x; gam[s][1] = g0.y; gam[s][2] = g0.z; gam[s][3] = g0.w;
+      gam[s][4] = g1.x; gam[s][5] = g1.y; gam[s][6] = g1.z; gam[s][7] = g1.w;
+    }
+  }
+  if (!first_segment) __syncthreads();
+  if (p_begin < p_end) {
+    stage_dma(c, pg_first[0], g_k0, g_v0);
+    stage_dma(c, pg_first[1], g_k1, g_v1);
+    stage_dma(c, pg_first[2], g_k2, g_v2);
+  }
+  // key norms of the segment's pages, and the count of their empty tail slots
   float kn2 = 0.f;
   int n_empty = 0;
-  for (int pi = p_begin + lane; pi < p_end; pi += 64) {
-    pg_mine = a.pages[pi];
-    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pg_mine.x) * a.num_heads + head]);
-    n_empty += kPageTokens - pg_mine.y;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    if (pgl[k].x >= 0) {
+      kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pgl[k].x) * a.num_heads + head]);
+      n_empty += kPageTokens - pgl[k].y;
+    }
   }
-  if (a.mode == 1) {
+  for (int pi = p_begin + lane + 128; pi < p_end; pi += 64) {  // segments longer than 128 pages
+    const int2 pg = a.pages[pi];
+    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pg.x) * a.num_heads + head]);
+    n_empty += kPageTokens - pg.y;
+  }
+
+  // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
+  if (norm_rope) {
     int pt = 0, ph = 0, pw = 0;
-    if (q_ok) load_pos(a.rope, a.positions, q, a.flags, pt, ph, pw);
+    if (q_ok) clamp_pos(a.rope, qpos.x, qpos.y, qpos.z, a.flags, pt, ph, pw);
     float ss = 0.f;
 #pragma unroll
     for (int s = 0; s < 8; ++s)
@@ -828,14 +864,11 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int d0 = 16 * s + 8 * half;
-      const float4 g0 = *reinterpret_cast<const float4*>(a.gamma + d0);
-      const float4 g1 = *reinterpret_cast<const float4*>(a.gamma + d0 + 4);
-      const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
       u32x4 w;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float y0 = bf16_lo(qraw[s][i]) * inv * g[2 * i];
-        const float y1 = bf16_hi(qraw[s][i]) * inv * g[2 * i + 1];
+        const float y0 = bf16_lo(qraw[s][i]) * inv * gam[s][2 * i];
+        const float y1 = bf16_hi(qraw[s][i]) * inv * gam[s][2 * i + 1];
         const float2 cs = rope_cs(a.rope, (d0 >> 1) + i, pt, ph, pw);
         w[i] = pack_bf16((y0 * cs.x - y1 * cs.y) * a.scale_log2, (y0 * cs.y + y1 * cs.x) * a.scale_log2);
       }
