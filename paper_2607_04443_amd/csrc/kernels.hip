@@ -14,6 +14,7 @@
 // The attention is the performer's per-step attention over its K/V cache
 // (Wan-Streamer v0.2, Sec. 3); block-causal visibility (Fig. 1 caption) is
 // resolved on the host into the list of visible pages.
+#include <cstddef>
 #include <type_traits>
 
 #include "ws_kernels.hpp"
@@ -262,6 +263,17 @@ struct VideoState {
 // Read-only for a whole launch: accessed through the constant address space
 // so that uniform reads become scalar loads.
 typedef const __attribute__((address_space(4))) int2* const_page_list;
+
+// The call's visible page list: in device memory, or in the kernel
+// arguments themselves (the kernel's only argument is the AttnArgs, at the
+// start of the kernel argument segment; addressing it through the segment
+// pointer keeps the compiler from copying the argument to private memory).
+__device__ __forceinline__ const_page_list page_list(const AttnArgs& a) {
+  if (a.pages) return (const_page_list)a.pages;
+  const __attribute__((address_space(4))) char* seg =
+      (const __attribute__((address_space(4))) char*)__builtin_amdgcn_kernarg_segment_ptr();
+  return (const_page_list)(seg + offsetof(AttnArgs, inline_pages));
+}
 
 struct VideoCtx {
   bool active;             // the wave has at least one real query row
@@ -770,7 +782,7 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   const int head = sg.head, p_begin = sg.p_begin, p_end = sg.p_end;
 
   VideoCtx c;
-  c.pages = (const_page_list)a.pages;
+  c.pages = page_list(a);
   c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
   c.kpool = a.kpool + head * kPageHeadElems;
   c.vpool = a.vpool + head * kPageHeadElems;
@@ -808,7 +820,7 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int pi = p_begin + lane + 64 * k;
-    pgl[k] = pi < p_end ? a.pages[pi] : make_int2(-1, kPageTokens);
+    pgl[k] = pi < p_end ? make_int2(c.pages[pi].x, c.pages[pi].y) : make_int2(-1, kPageTokens);
   }
   u32x4 qraw[8];
   const uint16_t* qp = a.q + q * a.q_tok_stride + head * a.q_head_stride + 8 * half;
@@ -842,7 +854,7 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
     }
   }
   for (int pi = p_begin + lane + 128; pi < p_end; pi += 64) {  // segments longer than 128 pages
-    const int2 pg = a.pages[pi];
+    const int2 pg = make_int2(c.pages[pi].x, c.pages[pi].y);
     kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pg.x) * a.num_heads + head]);
     n_empty += kPageTokens - pg.y;
   }
@@ -1105,7 +1117,7 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
   const int head = rest / a.n_qtiles;
   const int p_begin = split * a.pages_per_split + wave;
   const int p_end = min(a.n_pages, (split + 1) * a.pages_per_split);
-  const_page_list pages = (const_page_list)a.pages;
+  const_page_list pages = page_list(a);
   const int64_t page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
   const uint16_t* kpool = a.kpool + head * kPageHeadElems;
   const uint16_t* vpool = a.vpool + head * kPageHeadElems;

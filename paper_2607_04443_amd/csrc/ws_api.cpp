@@ -367,11 +367,20 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
     return fail(WS_ERR_INVALID_ARG, "bad softmax_scale");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
 
+  // The visible page list goes into the kernel arguments when it fits, else
+  // into the device arena (one upload per distinct list).
+  ws::AttnArgs a{};
   const int2* plist = nullptr;
   int32_t n_pages = 0;
-  if (ws_status st = visible_list(c, m, stream, &plist, &n_pages); st != WS_OK) return st;
-
-  ws::AttnArgs a{};
+  c->pt.visible_pages(ws::MaskSpec{m->q_unit, m->min_visible_unit, m->kind_mask}, &c->scratch_list);
+  if (c->scratch_list.size() <= static_cast<size_t>(ws::AttnArgs::kInlinePages)) {
+    n_pages = static_cast<int32_t>(c->scratch_list.size());
+    for (int32_t i = 0; i < n_pages; ++i)
+      a.inline_pages[i] = make_int2(c->scratch_list[static_cast<size_t>(i)].page,
+                                    c->scratch_list[static_cast<size_t>(i)].n_valid);
+  } else if (ws_status st = visible_list(c, m, stream, &plist, &n_pages); st != WS_OK) {
+    return st;
+  }
   a.q = static_cast<const uint16_t*>(q);
   a.q_tok_stride = q_tok_stride;
   a.q_head_stride = q_head_stride;

@@ -72,6 +72,10 @@ struct AppendArgs {
 };
 
 struct AttnArgs {
+  // Visible page lists up to this length travel in the kernel arguments
+  // (no upload, no copy dispatch ahead of the kernel); longer ones are
+  // uploaded to device memory.
+  static constexpr int kInlinePages = 384;
   const uint16_t* q;
   int64_t q_tok_stride;
   int64_t q_head_stride;
@@ -87,7 +91,8 @@ struct AttnArgs {
   const uint16_t* vpool;
   const float* knorm2;
   int32_t fixed_shift;   // 1: softmax shift from the key-norm bound when it is small enough
-  const int2* pages;     // visible pages: (page id, valid tokens)
+  const int2* pages;     // visible pages (page id, valid tokens) in device memory, or
+                         // nullptr: the first n_pages entries of inline_pages
   const uint16_t* zeros; // 1 KB of zeros (direct-load source for empty blocks)
   int32_t n_pages;
   int32_t n_splits;      // audio: key-range splits (the combine kernel merges them)
@@ -100,6 +105,7 @@ struct AttnArgs {
   float* part_o;         // [split][head][n_q][128], normalised: fp32 (audio), bf16 (video)
   float* part_lse;       // [split][head][n_q], log2 domain (scaled logits)
   uint32_t* flags;
+  int2 inline_pages[kInlinePages];
 };
 
 struct CombineArgs {
