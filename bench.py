@@ -7,10 +7,12 @@ state with an 8-unit history window (Wan-Streamer v0.2, Sec. 3 unit schedule;
 Sec. 2.1 history commit):
   1. the thinker's 256-token conditioning slice is written into the cache
      (stored as given, in place of the previous unit's slice);
-  2. unit u's 920 video and 4 audio K/V are appended (RMS-norm + rotary on K);
-     steps 1 and 2 are one batched append (a single kernel launch);
-  3. video attention: 920 queries (norm + rotary fused) over 256 + 9 x 920 =
-     8536 keys;
+  2. unit u's 920 video and 4 audio K/V are appended (RMS-norm + rotary on K)
+     and its 920 video and 4 audio queries prepared (RMS-norm + rotary, the
+     softmax scale folded in); steps 1 and 2 are one kernel launch
+     (ws_step_append);
+  3. video attention: the 920 prepared queries over 256 + 9 x 920 = 8536
+     keys;
   4. audio attention: 4 queries over cond + 9 x (920 + 4) = 8572 keys;
   5. unit u is committed to history and the unit that left the window evicted.
 All inputs are synthetic N(0,1) bf16 resident in HBM; H = 40 heads of 128.
@@ -92,8 +94,9 @@ def cpu_baseline(budget_s=12.0):
 def long_history(args, ws, sets, gamma, eps, stream, dev):
     """Long-history stress: 32 committed history units (256 + 33 x 920 =
     30616 keys) and 4 denoising steps issued back-to-back on one stream, each
-    rewriting the current unit's K/V in place (append with RMS-norm + rotary)
-    and running the video attention.  Timed with events around the 4 steps;
+    rewriting the current unit's K/V in place (append with RMS-norm + rotary,
+    and the query preparation, in one launch) and running the video
+    attention.  Timed with events around the 4 steps;
     the median of `long_reps` repetitions.  The history reuses the two
     resident input sets (values do not change the timing)."""
     import torch
@@ -108,14 +111,17 @@ def long_history(args, ws, sets, gamma, eps, stream, dev):
         cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, pos[u], gamma, eps)
         cache.commit(u)
     out = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
+    q_v = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
     mask = ws.mask_spec(hist_l, 0, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
 
     def four_steps():
         for step in range(4):
             s = sets[step % 2]
-            cache.append(hist_l, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, pos[hist_l],
-                         gamma, eps)
-            cache.unit_attention(s["q"], out, mask, ws.WS_APPEND_NORM_ROPE, pos[hist_l], gamma, eps)
+            cache.step_append(
+                [dict(unit=hist_l, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"],
+                      mode=ws.WS_APPEND_NORM_ROPE, positions=pos[hist_l], gamma=gamma, eps=eps)],
+                [dict(q=s["q"], q_out=q_v, positions=pos[hist_l], gamma=gamma, eps=eps)])
+            cache.unit_attention(q_v, out, mask, ws.WS_QUERY_PREPARED)
 
     four_steps()
     torch.cuda.synchronize()
@@ -190,29 +196,34 @@ def main():
 
     ev = {name: [] for name in ("append", "video", "audio")}
 
+    q_v = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)  # prepared queries
+    q_a = torch.empty((AUDIO, H, D), dtype=torch.bfloat16, device=dev)
+
     def step(u, timed):
         s = sets[u % 2]
         e = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if timed else None
         if timed:
             e[0].record(stream)
-        cache.append_many([
+        cache.step_append([
             dict(unit=0, kind=ws.WS_KIND_COND, k=s["ck"], v=s["cv"], mode=ws.WS_APPEND_RAW),
             dict(unit=u, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"], mode=ws.WS_APPEND_NORM_ROPE,
                  positions=vpos[u], gamma=gamma, eps=eps),
             dict(unit=u, kind=ws.WS_KIND_AUDIO, k=s["ka"], v=s["va"], mode=ws.WS_APPEND_NORM_ROPE,
-                 positions=apos[u], gamma=gamma, eps=eps)])
+                 positions=apos[u], gamma=gamma, eps=eps)],
+            [dict(q=s["q"], q_out=q_v, positions=vpos[u], gamma=gamma, eps=eps),
+             dict(q=s["qa"], q_out=q_a, positions=apos[u], gamma=gamma, eps=eps)])
         if timed:
             e[1].record(stream)
             e[2].record(stream)
-        cache.unit_attention(s["q"], out_v, ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
-                             ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.unit_attention(q_v, out_v, ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
+                             ws.WS_QUERY_PREPARED)
         if timed:
             e[3].record(stream)
             e[4].record(stream)
-        cache.audio_attention(s["qa"], out_a,
+        cache.audio_attention(q_a, out_a,
                               ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO,
                                                          ws.WS_KIND_AUDIO)),
-                              ws.WS_APPEND_NORM_ROPE, apos[u], gamma, eps)
+                              ws.WS_QUERY_PREPARED)
         if timed:
             e[5].record(stream)
             ev["append"].append((e[0], e[1]))
@@ -260,7 +271,7 @@ def main():
     fa = 4.0 * H * AUDIO * lk_a * D
     t_video, t_audio, t_append = avg_us("video"), avg_us("audio"), avg_us("append")
     audio_bytes = 2.0 * lk_a * H * D * 2 + 2.0 * AUDIO * H * D * 2
-    append_bytes = 4.0 * (COND + LU + AUDIO) * H * D * 2
+    append_bytes = 4.0 * (COND + LU + AUDIO) * H * D * 2 + 2.0 * (LU + AUDIO) * H * D * 2
 
     # audio path with cold caches: between repetitions a 1 GiB buffer is read
     # (a reduction), which evicts the cache with clean lines, so the timed
@@ -271,17 +282,19 @@ def main():
         scrub = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         scrub_sum = torch.empty((), dtype=torch.float32, device=dev)
         s = sets[u % 2]
-        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
-        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma,
-                     eps)
+        cache.step_append([
+            dict(unit=u, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"], mode=ws.WS_APPEND_NORM_ROPE,
+                 positions=vpos[u], gamma=gamma, eps=eps),
+            dict(unit=u, kind=ws.WS_KIND_AUDIO, k=s["ka"], v=s["va"], mode=ws.WS_APPEND_NORM_ROPE,
+                 positions=apos[u], gamma=gamma, eps=eps)],
+            [dict(q=s["qa"], q_out=q_a, positions=apos[u], gamma=gamma, eps=eps)])
         amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
         times = []
         for _ in range(args.cold_audio_reps):
             torch.sum(scrub, dim=0, out=scrub_sum)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            cache.audio_attention(s["qa"], out_a, amask, ws.WS_APPEND_NORM_ROPE, apos[u], gamma,
-                                  eps)
+            cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
             b.record(stream)
             b.synchronize()
             times.append(a.elapsed_time(b) * 1e3)

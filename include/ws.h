@@ -75,8 +75,16 @@ typedef enum ws_kind { WS_KIND_COND = 0, WS_KIND_VIDEO = 1, WS_KIND_AUDIO = 2 } 
 #define WS_KIND_BIT(kind) (1u << (unsigned)(kind))
 
 /* RAW: keys stored as given (the thinker's slice arrives in final form).
- * NORM_ROPE: keys RMS-normed per head, weighted by gamma, then rotated. */
-typedef enum ws_append_mode { WS_APPEND_RAW = 0, WS_APPEND_NORM_ROPE = 1 } ws_append_mode;
+ * NORM_ROPE: keys RMS-normed per head, weighted by gamma, then rotated.
+ * PREPARED (queries of the attention calls only): the queries are already
+ * Q'' = RoPE(RMSNorm(Q) * gamma, positions) * softmax_scale * log2(e) in
+ * bf16 (or Q * softmax_scale * log2(e) for RAW), as ws_step_append writes
+ * them; the attention uses them as given. */
+typedef enum ws_append_mode {
+  WS_APPEND_RAW = 0,
+  WS_APPEND_NORM_ROPE = 1,
+  WS_QUERY_PREPARED = 2
+} ws_append_mode;
 
 typedef struct ws_cache_config {
   int32_t num_heads;       /* H >= 1 */
@@ -112,12 +120,31 @@ typedef struct ws_append_item {
 #define WS_MAX_APPEND_ITEMS 16
 
 typedef struct ws_query_desc {
-  ws_append_mode mode;       /* NORM_ROPE: RMS-norm + rotary on Q; RAW: Q used as given */
+  ws_append_mode mode;       /* NORM_ROPE: RMS-norm + rotary on Q; RAW: Q used as given;
+                                PREPARED: Q'' from ws_step_append (the fields below unused) */
   const int32_t* positions;  /* device int32 [n_q][3]; NORM_ROPE only */
   const float* gamma;        /* device fp32 [head_dim]; NORM_ROPE only */
   float eps;
   float softmax_scale;       /* logit scale; 0 selects 1/sqrt(head_dim) */
 } ws_query_desc;
+
+/* One query set prepared by ws_step_append: q (mode RAW or NORM_ROPE in
+ * desc) is turned into Q'' (see WS_QUERY_PREPARED) and written to q_out.
+ *   q:     device bf16 [n_q][H][128], strides (tok_stride, head_stride);
+ *   q_out: device bf16 [n_q][H][128], strides (out_tok_stride, out_head_stride),
+ *          not overlapping q. */
+typedef struct ws_query_item {
+  const void* q;
+  int64_t tok_stride;
+  int64_t head_stride;
+  int32_t n_q;               /* >= 1 */
+  ws_query_desc desc;
+  void* q_out;
+  int64_t out_tok_stride;
+  int64_t out_head_stride;
+} ws_query_item;
+
+#define WS_MAX_QUERY_ITEMS 4
 
 /* Block-causal visibility for a query set that belongs to unit q_unit.  A
  * segment (unit u, kind k) is visible iff bit k of kind_mask is set, u <= q_unit,
@@ -181,7 +208,7 @@ WS_API ws_status ws_kv_append(ws_cache* cache, const void* k, const void* v, int
 
 /* ws_kv_append for n (1..WS_MAX_APPEND_ITEMS) segments at once, e.g. a
  * denoising step's video and audio K/V together with a thinker slice (Sec. 3):
- * the writes of all items share kernel launches (one launch per 4 items and 192
+ * the writes of all items share kernel launches (one launch per 8 items and 192
  * pages).  Each item obeys the rules of ws_kv_append and is stored exactly as a
  * separate ws_kv_append of it would store it.  All items are checked before any
  * page is taken, and if one item fails (bad argument, two items naming the same
@@ -190,6 +217,20 @@ WS_API ws_status ws_kv_append(ws_cache* cache, const void* k, const void* v, int
  * items: host array of n entries, read before the call returns. */
 WS_API ws_status ws_kv_append_many(ws_cache* cache, int32_t n, const ws_append_item* items,
                                    void* hip_stream);
+
+/* A denoising step's input stage in one launch (Sec. 3: the performer writes
+ * the step's K/V into its cache and attends with the step's queries): the K/V
+ * appends of ws_kv_append_many (n_kv items, 0..WS_MAX_APPEND_ITEMS) and the
+ * query preparation of n_q query sets (0..WS_MAX_QUERY_ITEMS; RMS-norm, gamma
+ * and rotary as for NORM_ROPE keys, then the softmax scale and log2(e),
+ * rounded once to bf16).  n_kv + n_q >= 1.  The K/V items follow every rule
+ * of ws_kv_append_many (and are all checked, with the query items, before any
+ * page is taken); ws_unit_attention / ws_audio_attention then take q_out
+ * with mode WS_QUERY_PREPARED and give the same result as NORM_ROPE (or RAW)
+ * on q, up to the summation order of the RMS norm.  kv and qs: host arrays,
+ * read before the call returns (either may be NULL when its count is 0). */
+WS_API ws_status ws_step_append(ws_cache* cache, int32_t n_kv, const ws_append_item* kv,
+                                int32_t n_q, const ws_query_item* qs, void* hip_stream);
 
 /* Marks the VIDEO and AUDIO segments of `unit` as committed history
  * (Sec. 2.1); they can no longer be rewritten.  Host-only. */

@@ -81,25 +81,135 @@ __device__ __forceinline__ void load_pos(const RopeTables& r, const int32_t* pos
   pw = cw;
 }
 
+typedef const __attribute__((address_space(4))) AppendSeg* const_append_seg;
+typedef const __attribute__((address_space(4))) AppendArgs* const_append_args;
+
+// The append launch's arguments, read in place from the kernel argument
+// segment (the kernel's only argument is the AppendArgs): with run-time
+// indexes into the by-value argument the compiler copies all of it to
+// private memory.
+__device__ __forceinline__ const_append_args append_args() {
+  return (const_append_args)__builtin_amdgcn_kernarg_segment_ptr();
+}
+
+// Query preparation, one block of an append launch: tokens 64 chunk ..
+// 64 chunk + 63 of query set si, one head, 16 threads per token row as in
+// the key path below.  Q'' = RoPE(RMSNorm(Q) * gamma, positions) * scale *
+// log2(e) (mode 3) or Q * scale * log2(e) (mode 2), in fp32, rounded once to
+// bf16: the attention kernels' own query prologue, done once per step
+// instead of once per workgroup that reads the queries.
+__device__ __forceinline__ void prepare_queries(const RopeTables& rope, uint32_t* flags, const_append_seg sg,
+                                                int chunk, int head) {
+  const uint16_t* src = sg->k;
+  const int64_t tok_stride = sg->tok_stride, head_stride = sg->head_stride;
+  const int n_tokens = sg->n_tokens;
+  const bool norm_rope = (sg->mode & 1) != 0;
+  const float scale = sg->scale_log2;
+  uint16_t* dst = sg->q_out;
+  const int64_t out_tok_stride = sg->out_tok_stride, out_head_stride = sg->out_head_stride;
+  const int t = threadIdx.x, c = t & 15, rr = t >> 4;
+  const int tok0 = chunk * kPageTokens;
+  float g[8];
+  float eps = 0.f;
+  const int32_t* positions = nullptr;
+  if (norm_rope) {
+    const float* gamma = sg->gamma;
+    eps = sg->eps;
+    positions = sg->positions;
+    const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * c);
+    const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * c + 4);
+    g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
+    g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+  }
+  u32x4 qx[4];
+  int tpos[4][3];
+#pragma unroll
+  for (int pass = 0; pass < 4; ++pass) {
+    const int tok = tok0 + pass * 16 + rr;
+    const bool valid = tok < n_tokens;
+    qx[pass] = valid ? *reinterpret_cast<const u32x4*>(src + tok * tok_stride + head * head_stride + 8 * c)
+                     : (u32x4){0u, 0u, 0u, 0u};
+    if (norm_rope && valid) {
+      tpos[pass][0] = positions[3 * tok + 0];
+      tpos[pass][1] = positions[3 * tok + 1];
+      tpos[pass][2] = positions[3 * tok + 2];
+    } else {
+      tpos[pass][0] = tpos[pass][1] = tpos[pass][2] = 0;
+    }
+  }
+#pragma unroll
+  for (int pass = 0; pass < 4; ++pass) {
+    const int tok = tok0 + pass * 16 + rr;
+    const bool valid = tok < n_tokens;
+    const u32x4 x = qx[pass];
+    u32x4 y;
+    if (norm_rope) {
+      float f[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = bf16_lo(x[i]);
+        f[2 * i + 1] = bf16_hi(x[i]);
+      }
+      float ss = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss += f[i] * f[i];
+      ss += __shfl_xor(ss, 1);
+      ss += __shfl_xor(ss, 2);
+      ss += __shfl_xor(ss, 4);
+      ss += __shfl_xor(ss, 8);
+      const float inv = rsqrtf(ss * (1.0f / kHeadDim) + eps);
+      int pt = 0, ph = 0, pw = 0;
+      if (valid) clamp_pos(rope, tpos[pass][0], tpos[pass][1], tpos[pass][2], flags, pt, ph, pw);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float y0 = f[2 * i] * inv * g[2 * i];
+        const float y1 = f[2 * i + 1] * inv * g[2 * i + 1];
+        const float2 cs = rope_cs(rope, 4 * c + i, pt, ph, pw);
+        y[i] = pack_bf16((y0 * cs.x - y1 * cs.y) * scale, (y0 * cs.y + y1 * cs.x) * scale);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) y[i] = pack_bf16(bf16_lo(x[i]) * scale, bf16_hi(x[i]) * scale);
+    }
+    if (valid) *reinterpret_cast<u32x4*>(dst + tok * out_tok_stride + head * out_head_stride + 8 * c) = y;
+  }
+}
+
 // ------------------------------------------------------------------------- //
-// kv_append: grid (pages of this launch, heads), 256 threads; the pages may
-// belong to up to AppendArgs::kMaxSegs segments.
+// kv_append: grid (blocks of this launch, heads), 256 threads; the blocks
+// may belong to up to AppendArgs::kMaxSegs segments (K/V pages or query
+// chunks).
 // ------------------------------------------------------------------------- //
-__global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
+__global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
+  (void)args;  // read in place, through append_args()
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPageTokens][kHeadDim + 8];
   __shared__ float wave_norm2[4];
+  const const_append_args A = append_args();
   const int head = blockIdx.y;
-  const int page = a.pages[blockIdx.x];
-  const int si = a.blk_seg[blockIdx.x];
-  const uint16_t* src_k = a.seg[si].k;
-  const uint16_t* src_v = a.seg[si].v;
-  const int64_t tok_stride = a.seg[si].tok_stride, head_stride = a.seg[si].head_stride;
-  const int n_tokens = a.seg[si].n_tokens;
-  const int mode = a.seg[si].mode;
-  const int tok0 = a.blk_page[blockIdx.x] * kPageTokens;
-  const int64_t tile = (static_cast<int64_t>(page) * a.num_heads + head) * kPageHeadElems;
-  uint16_t* kdst = a.kpool + tile;
-  uint16_t* vdst = a.vpool + tile;
+  const const_append_seg sg = A->seg + A->blk_seg[blockIdx.x];
+  RopeTables rope;
+#pragma unroll
+  for (int b = 0; b < 3; ++b) {
+    rope.tab[b] = A->rope.tab[b];
+    rope.max_pos[b] = A->rope.max_pos[b];
+    rope.pairs[b] = A->rope.pairs[b];
+  }
+  uint32_t* const flags = A->flags;
+  if (sg->mode & kAppendQuery) {
+    prepare_queries(rope, flags, sg, A->blk_page[blockIdx.x], head);
+    return;
+  }
+  const int num_heads = A->num_heads;
+  const int page = A->pages[blockIdx.x];
+  const uint16_t* src_k = sg->k;
+  const uint16_t* src_v = sg->v;
+  const int64_t tok_stride = sg->tok_stride, head_stride = sg->head_stride;
+  const int n_tokens = sg->n_tokens;
+  const int mode = sg->mode;
+  const int tok0 = A->blk_page[blockIdx.x] * kPageTokens;
+  const int64_t tile = (static_cast<int64_t>(page) * num_heads + head) * kPageHeadElems;
+  uint16_t* kdst = A->kpool + tile;
+  uint16_t* vdst = A->vpool + tile;
   const int t = threadIdx.x;
 
   // K: 16 threads per token row, 8 consecutive d each; 16 rows per pass.
@@ -111,9 +221,9 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
   float eps = 0.f;
   const int32_t* positions = nullptr;
   if (mode == 1) {
-    const float* gamma = a.seg[si].gamma;
-    eps = a.seg[si].eps;
-    positions = a.seg[si].positions;
+    const float* gamma = sg->gamma;
+    eps = sg->eps;
+    positions = sg->positions;
     const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * c);
     const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * c + 4);
     g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
@@ -167,12 +277,12 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
       ss += __shfl_xor(ss, 8);
       const float inv = rsqrtf(ss * (1.0f / kHeadDim) + eps);
       int pt = 0, ph = 0, pw = 0;
-      if (valid) clamp_pos(a.rope, tpos[pass][0], tpos[pass][1], tpos[pass][2], a.flags, pt, ph, pw);
+      if (valid) clamp_pos(rope, tpos[pass][0], tpos[pass][1], tpos[pass][2], flags, pt, ph, pw);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float y0 = f[2 * i] * inv * g[2 * i];
         const float y1 = f[2 * i + 1] * inv * g[2 * i + 1];
-        const float2 cs = rope_cs(a.rope, 4 * c + i, pt, ph, pw);
+        const float2 cs = rope_cs(rope, 4 * c + i, pt, ph, pw);
         y[i] = pack_bf16(y0 * cs.x - y1 * cs.y, y0 * cs.y + y1 * cs.x);
       }
       if (!valid) y = (u32x4){0u, 0u, 0u, 0u};
@@ -210,7 +320,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
     *reinterpret_cast<u32x4*>(vdst + v_tile_index(8 * tc, d)) = y;
   }
   if (t == 0)
-    a.knorm2[static_cast<int64_t>(page) * a.num_heads + head] =
+    A->knorm2[static_cast<int64_t>(page) * num_heads + head] =
         fmaxf(fmaxf(wave_norm2[0], wave_norm2[1]), fmaxf(wave_norm2[2], wave_norm2[3]));
 }
 
@@ -886,6 +996,9 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
       }
       c.qreg[s] = as_bf16x8(q_ok ? w : (u32x4){0u, 0u, 0u, 0u});
     }
+  } else if (a.mode == 2) {  // prepared: Q'' as given
+#pragma unroll
+    for (int s = 0; s < 8; ++s) c.qreg[s] = as_bf16x8(qraw[s]);
   } else {
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -1171,6 +1284,9 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
       }
       qreg[s] = as_bf16x8(q_ok ? w : (u32x4){0u, 0u, 0u, 0u});
     }
+  } else if (a.mode == 2) {  // prepared: Q'' as given
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qreg[s] = as_bf16x8(qraw[s]);
   } else {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {

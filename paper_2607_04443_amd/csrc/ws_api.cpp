@@ -344,6 +344,13 @@ int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
   return std::max(1, std::min({target, std::max(1, n_pages / 4), kMaxAudioSplits}));
 }
 
+// The logit scale times log2(e), folded into Q'' (0 selects 1/sqrt(128)).
+float scale_log2_of(float softmax_scale) {
+  const double scale = softmax_scale > 0.f ? static_cast<double>(softmax_scale)
+                                           : 1.0 / std::sqrt(static_cast<double>(ws::kHeadDim));
+  return static_cast<float>(scale * 1.4426950408889634);
+}
+
 ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
                          int32_t n_q, const ws_query_desc* qd, ws_cache* c, const ws_mask_spec* m,
                          void* out, int64_t out_tok_stride, int64_t out_head_stride,
@@ -356,7 +363,7 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   if (ws_status st = check_strides("q", q, q_tok_stride, q_head_stride, n_q, H); st != WS_OK) return st;
   if (ws_status st = check_strides("out", out, out_tok_stride, out_head_stride, n_q, H); st != WS_OK)
     return st;
-  if (qd->mode != WS_APPEND_RAW && qd->mode != WS_APPEND_NORM_ROPE)
+  if (qd->mode != WS_APPEND_RAW && qd->mode != WS_APPEND_NORM_ROPE && qd->mode != WS_QUERY_PREPARED)
     return fail(WS_ERR_INVALID_ARG, "bad query mode %d", static_cast<int>(qd->mode));
   if (qd->mode == WS_APPEND_NORM_ROPE) {
     if (!qd->positions || !qd->gamma) return fail(WS_ERR_INVALID_ARG, "NORM_ROPE needs positions and gamma");
@@ -390,9 +397,7 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   a.positions = qd->positions;
   a.gamma = qd->gamma;
   a.eps = qd->eps;
-  const float scale = qd->softmax_scale > 0.f ? qd->softmax_scale
-                                              : static_cast<float>(1.0 / std::sqrt(double(ws::kHeadDim)));
-  a.scale_log2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  a.scale_log2 = scale_log2_of(qd->softmax_scale);
   a.rope = c->rope;
   a.kpool = c->kpool;
   a.vpool = c->vpool;
@@ -507,6 +512,18 @@ ws_status ws_kv_append_many(ws_cache* c, int32_t n, const ws_append_item* items,
   if (!c || !items) return fail(WS_ERR_INVALID_ARG, "NULL argument");
   if (n < 1 || n > WS_MAX_APPEND_ITEMS)
     return fail(WS_ERR_INVALID_ARG, "append item count %d outside [1, %d]", n, WS_MAX_APPEND_ITEMS);
+  return ws_step_append(c, n, items, 0, nullptr, hip_stream);
+}
+
+ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, int32_t n_q,
+                         const ws_query_item* qs, void* hip_stream) {
+  if (!c) return fail(WS_ERR_INVALID_ARG, "NULL cache");
+  if (n < 0 || n > WS_MAX_APPEND_ITEMS)
+    return fail(WS_ERR_INVALID_ARG, "append item count %d outside [0, %d]", n, WS_MAX_APPEND_ITEMS);
+  if (n_q < 0 || n_q > WS_MAX_QUERY_ITEMS)
+    return fail(WS_ERR_INVALID_ARG, "query item count %d outside [0, %d]", n_q, WS_MAX_QUERY_ITEMS);
+  if (n + n_q < 1) return fail(WS_ERR_INVALID_ARG, "nothing to do: no append and no query item");
+  if ((n > 0 && !items) || (n_q > 0 && !qs)) return fail(WS_ERR_INVALID_ARG, "NULL item array");
   if (ws_status st = check_device(c); st != WS_OK) return st;
   const int H = c->cfg.num_heads;
   // Every item is checked before any page is taken.
@@ -531,6 +548,26 @@ ws_status ws_kv_append_many(ws_cache* c, int32_t n, const ws_append_item* items,
       if (items[j].desc.unit == d->unit && items[j].desc.kind == d->kind)
         return fail(WS_ERR_INVALID_ARG, "items %d and %d name the same unit %d kind %d", j, i, d->unit,
                     static_cast<int>(d->kind));
+  }
+  for (int i = 0; i < n_q; ++i) {
+    const ws_query_item& it = qs[i];
+    const ws_query_desc* d = &it.desc;
+    if (d->mode != WS_APPEND_RAW && d->mode != WS_APPEND_NORM_ROPE)
+      return fail(WS_ERR_INVALID_ARG, "query item %d: bad mode %d", i, static_cast<int>(d->mode));
+    if (it.n_q < 1) return fail(WS_ERR_SHAPE, "query item %d: n_q must be >= 1", i);
+    if (ws_status st = check_strides("q", it.q, it.tok_stride, it.head_stride, it.n_q, H); st != WS_OK)
+      return st;
+    if (ws_status st = check_strides("q_out", it.q_out, it.out_tok_stride, it.out_head_stride, it.n_q, H);
+        st != WS_OK)
+      return st;
+    if (d->mode == WS_APPEND_NORM_ROPE) {
+      if (!d->positions || !d->gamma)
+        return fail(WS_ERR_INVALID_ARG, "query item %d: NORM_ROPE needs positions and gamma", i);
+      if (!aligned16(d->gamma)) return fail(WS_ERR_INVALID_ARG, "query item %d: gamma is not 16-byte aligned", i);
+      if (!(d->eps >= 0.f) || !std::isfinite(d->eps)) return fail(WS_ERR_INVALID_ARG, "query item %d: bad eps", i);
+    }
+    if (!std::isfinite(d->softmax_scale) || d->softmax_scale < 0.f)
+      return fail(WS_ERR_INVALID_ARG, "query item %d: bad softmax_scale", i);
   }
   // Pages: all items or none.  Page lists are copied out at once (the table's
   // segment storage may move on the next creation).
@@ -603,6 +640,7 @@ ws_status ws_kv_append_many(ws_cache* c, int32_t n, const ws_append_item* items,
         }
         slot = n_segs++;
         ws::AppendSeg& sg = a.seg[slot];
+        sg = ws::AppendSeg{};
         sg.k = static_cast<const uint16_t*>(it.k);
         sg.v = static_cast<const uint16_t*>(it.v);
         sg.tok_stride = it.tok_stride;
@@ -615,6 +653,48 @@ ws_status ws_kv_append_many(ws_cache* c, int32_t n, const ws_append_item* items,
       }
       a.pages[a.n_blocks] = pl[p];
       a.blk_page[a.n_blocks] = static_cast<int32_t>(p);
+      a.blk_seg[a.n_blocks] = static_cast<uint8_t>(slot);
+      ++a.n_blocks;
+    }
+  }
+  // query sets: 64-token chunks, no pages
+  for (int i = 0; i < n_q; ++i) {
+    const ws_query_item& it = qs[i];
+    const int chunks = (it.n_q + ws::kPageTokens - 1) / ws::kPageTokens;
+    int slot = -1;
+    for (int ch = 0; ch < chunks; ++ch) {
+      if (a.n_blocks == ws::AppendArgs::kMaxAppendPages) {
+        if (hipError_t e = flush(); e != hipSuccess) {
+          roll_back();
+          return hip_fail(e, "kv_append launch");
+        }
+        slot = -1;
+      }
+      if (slot < 0) {
+        if (n_segs == ws::AppendArgs::kMaxSegs) {
+          if (hipError_t e = flush(); e != hipSuccess) {
+            roll_back();
+            return hip_fail(e, "kv_append launch");
+          }
+        }
+        slot = n_segs++;
+        ws::AppendSeg& sg = a.seg[slot];
+        sg = ws::AppendSeg{};
+        sg.k = static_cast<const uint16_t*>(it.q);
+        sg.tok_stride = it.tok_stride;
+        sg.head_stride = it.head_stride;
+        sg.n_tokens = it.n_q;
+        sg.mode = ws::kAppendQuery | (it.desc.mode == WS_APPEND_NORM_ROPE ? 1 : 0);
+        sg.positions = it.desc.positions;
+        sg.gamma = it.desc.gamma;
+        sg.eps = it.desc.eps;
+        sg.scale_log2 = scale_log2_of(it.desc.softmax_scale);
+        sg.q_out = static_cast<uint16_t*>(it.q_out);
+        sg.out_tok_stride = it.out_tok_stride;
+        sg.out_head_stride = it.out_head_stride;
+      }
+      a.pages[a.n_blocks] = -1;
+      a.blk_page[a.n_blocks] = ch;
       a.blk_seg[a.n_blocks] = static_cast<uint8_t>(slot);
       ++a.n_blocks;
     }

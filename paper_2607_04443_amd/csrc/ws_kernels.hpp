@@ -40,23 +40,32 @@ struct RopeTables {
   int32_t pairs[3];
 };
 
-// One segment of an append launch.
+// One segment of an append launch: a K/V segment (mode 0 raw, 1 norm +
+// rope; block x writes one page) or a query set (mode 2 raw, 3 norm + rope:
+// the key path's arithmetic, then the scale, written to q_out; block x
+// prepares 64 tokens, no page).
 struct AppendSeg {
-  const uint16_t* k;
+  const uint16_t* k;     // keys, or the queries
   const uint16_t* v;
   int64_t tok_stride;
   int64_t head_stride;
   int32_t n_tokens;      // tokens of the whole segment
-  int32_t mode;          // 0 raw, 1 norm + rope
+  int32_t mode;
   const int32_t* positions;
   const float* gamma;
   float eps;
+  float scale_log2;      // queries: softmax scale * log2(e)
+  uint16_t* q_out;       // queries: prepared Q''
+  int64_t out_tok_stride;
+  int64_t out_head_stride;
 };
+constexpr int kAppendQuery = 2;  // mode bit: a query set
 
 // Several segments in one launch: block x of the grid writes page pages[x],
-// which is page blk_page[x] of segment blk_seg[x].
+// which is page blk_page[x] of segment blk_seg[x] (for a query set: token
+// chunk blk_page[x]).
 struct AppendArgs {
-  static constexpr int kMaxSegs = 4;
+  static constexpr int kMaxSegs = 8;
   static constexpr int kMaxAppendPages = 192;
   AppendSeg seg[kMaxSegs];
   int32_t n_blocks;
@@ -81,7 +90,7 @@ struct AttnArgs {
   int64_t q_head_stride;
   int32_t n_q;
   int32_t num_heads;
-  int32_t mode;          // query prologue: 0 raw, 1 norm + rope
+  int32_t mode;          // query prologue: 0 raw, 1 norm + rope, 2 prepared (Q'' as given)
   const int32_t* positions;
   const float* gamma;
   float eps;

@@ -31,7 +31,7 @@ STATUS_NAMES = {0: "WS_OK", 1: "WS_ERR_INVALID_ARG", 2: "WS_ERR_SHAPE", 3: "WS_E
                 4: "WS_ERR_UNKNOWN_UNIT", 5: "WS_ERR_COMMITTED", 6: "WS_ERR_UNSUPPORTED",
                 7: "WS_ERR_HIP"}
 WS_KIND_COND, WS_KIND_VIDEO, WS_KIND_AUDIO = 0, 1, 2
-WS_APPEND_RAW, WS_APPEND_NORM_ROPE = 0, 1
+WS_APPEND_RAW, WS_APPEND_NORM_ROPE, WS_QUERY_PREPARED = 0, 1, 2
 WS_OPT_VIDEO_KV_SPLITS, WS_OPT_AUDIO_KV_SPLITS, WS_OPT_VIDEO_RUNNING_MAX = 0, 1, 2
 INT32_MIN = -(2 ** 31)
 
@@ -67,6 +67,16 @@ class ws_query_desc(ctypes.Structure):
                 ("softmax_scale", ctypes.c_float)]
 
 
+class ws_query_item(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("tok_stride", ctypes.c_int64),
+                ("head_stride", ctypes.c_int64), ("n_q", ctypes.c_int32),
+                ("desc", ws_query_desc), ("q_out", ctypes.c_void_p),
+                ("out_tok_stride", ctypes.c_int64), ("out_head_stride", ctypes.c_int64)]
+
+
+WS_MAX_QUERY_ITEMS = 4
+
+
 class ws_mask_spec(ctypes.Structure):
     _fields_ = [("q_unit", ctypes.c_int32), ("min_visible_unit", ctypes.c_int32),
                 ("kind_mask", ctypes.c_uint32)]
@@ -90,6 +100,7 @@ _SIGS = {
     "ws_cache_reset": [_vp],
     "ws_kv_append": [_vp, _vp, _vp, _i64, _i64, _P(ws_append_desc), _vp],
     "ws_kv_append_many": [_vp, _i32, _P(ws_append_item), _vp],
+    "ws_step_append": [_vp, _i32, _P(ws_append_item), _i32, _P(ws_query_item), _vp],
     "ws_unit_commit": [_vp, _i32],
     "ws_kv_evict_before": [_vp, _i32],
     "ws_kv_release": [_vp, _i32, _i32],
@@ -151,6 +162,14 @@ def ws_kv_append_many(cache, items, stream):
     """items: a sequence of ws_append_item."""
     arr = (ws_append_item * len(items))(*items)
     _check(_lib.ws_kv_append_many(cache, len(items), arr, stream), "ws_kv_append_many")
+
+
+def ws_step_append(cache, items, queries, stream):
+    """items: a sequence of ws_append_item; queries: a sequence of ws_query_item."""
+    arr = (ws_append_item * len(items))(*items) if items else None
+    qarr = (ws_query_item * len(queries))(*queries) if queries else None
+    _check(_lib.ws_step_append(cache, len(items), arr, len(queries), qarr, stream),
+           "ws_step_append")
 
 
 def ws_unit_commit(cache, unit):
@@ -290,6 +309,32 @@ class Cache:
     def append_many(self, items, stream=None):
         """items: dicts with the keyword arguments of append (stream aside)."""
         ws_kv_append_many(self.handle, [self._item(**x) for x in items], _stream_handle(stream))
+
+    @staticmethod
+    def _query_item(q, q_out, mode=WS_APPEND_NORM_ROPE, positions=None, gamma=None, eps=1e-6,
+                    scale=0.0):
+        import torch
+        _check_tensor("q", q, torch.bfloat16)
+        _check_tensor("q_out", q_out, torch.bfloat16)
+        if q.shape != q_out.shape:
+            raise ValueError("q and q_out must have the same shape")
+        it = ws_query_item()
+        it.q, it.tok_stride, it.head_stride, it.n_q = q.data_ptr(), q.stride(0), q.stride(1), q.shape[0]
+        d = it.desc
+        d.mode = mode
+        d.positions = positions.data_ptr() if positions is not None else None
+        d.gamma = gamma.data_ptr() if gamma is not None else None
+        d.eps, d.softmax_scale = eps, scale
+        it.q_out, it.out_tok_stride, it.out_head_stride = q_out.data_ptr(), q_out.stride(0), q_out.stride(1)
+        return it
+
+    def step_append(self, items=(), queries=(), stream=None):
+        """One launch for a step's K/V appends (dicts with the keyword arguments
+        of append) and query preparations (dicts with q, q_out, mode, positions,
+        gamma, eps, scale); q_out then feeds the attention calls with mode
+        WS_QUERY_PREPARED."""
+        ws_step_append(self.handle, [self._item(**x) for x in items],
+                       [self._query_item(**x) for x in queries], _stream_handle(stream))
 
     def _attn(self, fn, q, out, mask, mode, positions, gamma, eps, scale, stream):
         import torch

@@ -44,7 +44,8 @@ def dev_f32(a):
 class Loaded:
     """A workload written into a GPU cache and mirrored in an oracle cache."""
 
-    def __init__(self, ws, wl, max_pages=None, step=0, max_q_tokens=1024, keep=None):
+    def __init__(self, ws, wl, max_pages=None, step=0, max_q_tokens=1024, keep=None,
+                 step_segments=True):
         cfg = wl.config
         if max_pages is None:
             max_pages = 8 + (cfg.hist + 2) * (cfg.unit_tokens // 64 + 3) + cfg.cond // 64
@@ -56,7 +57,7 @@ class Loaded:
         self._keep = [] if keep is None else keep
         for seg in wl.cached:
             self.append(seg)
-        if wl.steps:
+        if wl.steps and step_segments:
             for seg in wl.steps[step].segments:
                 self.append(seg)
 

@@ -75,7 +75,12 @@ int main(void) {
   S(ws_call_timing) P(ws_call_timing, n_splits) P(ws_call_timing, attn_us) P(ws_call_timing, merge_us)
   S(ws_append_item) P(ws_append_item, v) P(ws_append_item, tok_stride) P(ws_append_item, head_stride)
   P(ws_append_item, desc)
+  S(ws_query_item) P(ws_query_item, tok_stride) P(ws_query_item, head_stride) P(ws_query_item, n_q)
+  P(ws_query_item, desc) P(ws_query_item, q_out) P(ws_query_item, out_tok_stride)
+  P(ws_query_item, out_head_stride)
   printf("max_items %d\n", WS_MAX_APPEND_ITEMS);
+  printf("max_query_items %d\n", WS_MAX_QUERY_ITEMS);
+  printf("prepared %d\n", (int)WS_QUERY_PREPARED);
   printf("enum %zu\n", sizeof(ws_kind));
   return 0;
 }
@@ -96,11 +101,14 @@ def test_struct_layouts_match_c(tmp_path):
     c = {k: int(v) for k, v in c.items()}
     assert c["enum"] == 4
     assert c["max_items"] == ws.WS_MAX_APPEND_ITEMS
+    assert c["max_query_items"] == ws.WS_MAX_QUERY_ITEMS
+    assert c["prepared"] == ws.WS_QUERY_PREPARED
     for name, typ in (("ws_cache_config", ws.ws_cache_config),
                       ("ws_append_desc", ws.ws_append_desc), ("ws_query_desc", ws.ws_query_desc),
                       ("ws_mask_spec", ws.ws_mask_spec), ("ws_cache_stats", ws.ws_cache_stats),
                       ("ws_call_timing", ws.ws_call_timing),
-                      ("ws_append_item", ws.ws_append_item)):
+                      ("ws_append_item", ws.ws_append_item),
+                      ("ws_query_item", ws.ws_query_item)):
         assert ctypes.sizeof(typ) == c[name], name
         for key, off in c.items():
             if key.startswith(name + "."):

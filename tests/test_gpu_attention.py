@@ -403,3 +403,99 @@ def test_launch_timing_ring(ws):
             L.cache.timing_read()
     finally:
         L.close()
+
+
+def _prepare(L, q_bits, pos, mode=None, scale=0.0, kv_segments=()):
+    """One ws_step_append: the given K/V segments plus the preparation of
+    q_bits; returns the prepared Q'' tensor on the device."""
+    import torch
+    ws = L.ws
+    q = to_dev(q_bits)
+    q_out = torch.full_like(q, float("nan"))
+    L._keep += [q, q_out]
+    mode = ws.WS_APPEND_NORM_ROPE if mode is None else mode
+    items = []
+    for seg in kv_segments:
+        k, v = to_dev(seg.k), to_dev(seg.v)
+        p = dev_i32(seg.positions) if seg.positions is not None else None
+        L._keep += [k, v, p]
+        if seg.mode == synth.MODE_RAW:
+            items.append(dict(unit=seg.unit, kind=seg.kind, k=k, v=v, mode=ws.WS_APPEND_RAW))
+        else:
+            items.append(dict(unit=seg.unit, kind=seg.kind, k=k, v=v, mode=ws.WS_APPEND_NORM_ROPE,
+                              positions=p, gamma=L.gk, eps=L.wl.eps))
+        L.ocache.append(seg.unit, seg.kind, seg.k, seg.v,
+                        oracle.MODE_RAW if seg.mode == synth.MODE_RAW else oracle.MODE_NORM_ROPE,
+                        seg.positions, L.wl.gamma_k.astype(np.float64), L.wl.eps)
+    qpos = dev_i32(pos)
+    L._keep.append(qpos)
+    L.cache.step_append(items, [dict(q=q, q_out=q_out, mode=mode, positions=qpos, gamma=L.gq,
+                                     eps=L.wl.eps, scale=scale)])
+    return q_out
+
+
+def _run_prepared(L, path, q_out, q_unit, kinds):
+    import torch
+    ws = L.ws
+    out = torch.full_like(q_out, float("nan"))
+    fn = L.cache.unit_attention if path == "video" else L.cache.audio_attention
+    fn(q_out, out, ws.mask_spec(q_unit, -(2 ** 31), kinds), ws.WS_QUERY_PREPARED)
+    torch.cuda.synchronize()
+    return bf16_f64(from_dev(out))
+
+
+@pytest.mark.parametrize("mode", ["norm_rope", "raw"])
+def test_prepared_queries_match_the_oracle_prologue(ws, mode):
+    """Q'' written by ws_step_append: the oracle's Q' (RMS-norm, gamma,
+    rotary, or Q as given) times softmax scale * log2(e), within one bf16 ulp
+    (plus the fp32 error of a rotated pair that cancels to near zero); ragged
+    query count (3 chunks of 64, the last holding 9 tokens)."""
+    wl = synth.make_workload("v01", variant="seeded")
+    L = Loaded(ws, wl)
+    try:
+        rng = np.random.default_rng(synth.SEED_BASE + 91)
+        n_q = 137
+        q = synth.normal_bf16(rng, (n_q, wl.config.heads, 128))
+        pos = np.stack([np.full(n_q, 5), rng.integers(0, 12, n_q), rng.integers(0, 21, n_q)],
+                       axis=1).astype(np.int32)
+        scale = 0.07 if mode == "raw" else 0.0
+        wmode = ws.WS_APPEND_RAW if mode == "raw" else ws.WS_APPEND_NORM_ROPE
+        omode = oracle.MODE_RAW if mode == "raw" else oracle.MODE_NORM_ROPE
+        q_out = _prepare(L, q, pos, mode=wmode, scale=scale)
+        import torch
+        torch.cuda.synchronize()
+        got = bf16_f64(from_dev(q_out))
+        s = (scale if scale > 0 else 1.0 / np.sqrt(128.0)) * np.log2(np.e)
+        for h in range(wl.config.heads):
+            ref = s * oracle.query_prologue(q[:, h, :], omode, pos, wl.gamma_q.astype(np.float64),
+                                            wl.eps)
+            err = np.abs(got[:, h] - ref)
+            ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126))) - 7)
+            assert (err <= ulp + 2.0 ** -15).all(), (h, float(err.max()))
+    finally:
+        L.close()
+
+
+@pytest.mark.parametrize("name", ["v02_single", "audio_c256"])
+def test_prepared_step_parity(ws, name):
+    """A step through ws_step_append (the current unit's K/V and the query
+    preparation in one launch) and the attention on the prepared queries:
+    within the gates of the oracle, and close to the NORM_ROPE path on the raw
+    queries (the two differ only in the summation order of the RMS norm)."""
+    wl = synth.make_workload(name)
+    L = Loaded(ws, wl, step_segments=False)
+    try:
+        st = wl.steps[0]
+        if name.startswith("audio"):
+            path, qb, qp, kinds = "audio", st.q_audio, st.q_audio_pos, ALL_KINDS
+        else:
+            path, qb, qp, kinds = "video", st.q_video, st.q_video_pos, VIDEO_KINDS
+        q_out = _prepare(L, qb, qp, kv_segments=st.segments)
+        got = _run_prepared(L, path, q_out, wl.current_unit, kinds)
+        ref = L.oracle(qb, qp, wl.current_unit, kinds)
+        print(name, assert_gates(got, ref, label=f"{name} prepared"))
+        direct = L.run(path, qb, qp, wl.current_unit, kinds)
+        e = errors(got, direct)
+        assert e["frob"] <= 2e-3, e
+    finally:
+        L.close()

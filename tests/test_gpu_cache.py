@@ -190,7 +190,7 @@ def test_append_many_matches_separate_appends(ws):
 @pytest.mark.parametrize("layout", ["long_segment", "many_segments"])
 def test_append_many_launch_packing(ws, layout):
     """Segments split across launches: one longer than a launch's 192 pages,
-    and six one-page segments (more than a launch's four)."""
+    and ten one-page segments (more than a launch's eight)."""
     import torch
     rng = np.random.default_rng(synth.SEED_BASE + 77)
     R, N = synth.MODE_RAW, synth.MODE_NORM_ROPE
@@ -199,7 +199,7 @@ def test_append_many_launch_packing(ws, layout):
         specs = [(1, V, N, 150), (2, C, R, 200 * 64 - 5), (3, V, N, 1), (4, A, R, 100),
                  (5, A, N, 64)]
     else:
-        specs = [(u, V if u % 2 else A, N if u % 3 else R, 1 + 9 * u) for u in range(6)]
+        specs = [(u, V if u % 2 else A, N if u % 3 else R, 1 + 6 * u) for u in range(10)]
     heads = 2
     segs = _random_segments(rng, heads, specs)
     gamma = rng.uniform(0.5, 1.5, size=128).astype(np.float32)
