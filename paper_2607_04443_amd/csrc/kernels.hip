@@ -252,6 +252,13 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
     vx[i] = tok < n_tokens ? *reinterpret_cast<const u32x4*>(src_v + tok * tok_stride + head * head_stride + 8 * (ch & 15))
                            : (u32x4){0u, 0u, 0u, 0u};
   }
+  // V rows go to LDS ([slot][d]) as soon as they arrive, which frees their
+  // registers before the key arithmetic
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = t + 256 * i;
+    *reinterpret_cast<u32x4*>(&vt[ch >> 4][8 * (ch & 15)]) = vx[i];
+  }
 
 #pragma unroll
   for (int pass = 0; pass < 4; ++pass) {
@@ -301,12 +308,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
   norm2 = fmaxf(norm2, __shfl_xor(norm2, 32));
   if ((t & 63) == 0) wave_norm2[t >> 6] = norm2;
 
-  // V: stage [slot][d] in LDS, write [d][slot].
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ch = t + 256 * i;
-    *reinterpret_cast<u32x4*>(&vt[ch >> 4][8 * (ch & 15)]) = vx[i];
-  }
+  // V: staged [slot][d] in LDS above, written [d][slot].
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
