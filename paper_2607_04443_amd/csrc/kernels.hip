@@ -1506,53 +1506,59 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
 // video_combine: merges the key ranges of the video schedule.  A head's
 // range count follows from the groups' even shares of heads x pages (a head
 // in one range was written in bf16 by the attention kernel: nothing to
-// merge).  32 threads per (head, query) row, 4 d each, 8 rows per block; all
-// of a row's (at most kMaxVideoSplits) partials are requested before any is
-// used.
+// merge).  16 threads per (head, query) row, 8 d each (16-byte loads), 16
+// rows per block; all of a row's (at most kMaxVideoSplits) partials are
+// requested before any is used.
 // ------------------------------------------------------------------------- //
 __global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a) {
-  const int lane = threadIdx.x & 31;
-  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
+  const int lane = threadIdx.x & 15;
+  const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (row >= a.num_heads * a.n_q) return;
   const int head = row / a.n_q, q = row % a.n_q;
   const int64_t units = static_cast<int64_t>(a.num_heads) * a.n_pages, h0 = static_cast<int64_t>(head) * a.n_pages;
   const int n_ranges = static_cast<int>(video_group_of(h0 + a.n_pages - 1, a.n_groups, units) -
                                         video_group_of(h0, a.n_groups, units) + 1);
   if (n_ranges < 2) return;
-  const int d0 = 4 * lane;
+  const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
   const uint16_t* po = reinterpret_cast<const uint16_t*>(a.part_o);
   float l[kMaxVideoSplits];
-  u32x2 w[kMaxVideoSplits];
+  u32x4 w[kMaxVideoSplits];
 #pragma unroll
   for (int sp = 0; sp < kMaxVideoSplits; ++sp) {
     if (sp < n_ranges) {
       l[sp] = a.part_lse[sp * split_stride + row];
-      w[sp] = *reinterpret_cast<const u32x2*>(po + (sp * split_stride + row) * kHeadDim + d0);
+      w[sp] = *reinterpret_cast<const u32x4*>(po + (sp * split_stride + row) * kHeadDim + d0);
     } else {
       l[sp] = kNegInf;
-      w[sp] = (u32x2){0u, 0u};
+      w[sp] = (u32x4){0u, 0u, 0u, 0u};
     }
   }
   float mx = kNegInf;
 #pragma unroll
   for (int sp = 0; sp < kMaxVideoSplits; ++sp) mx = fmaxf(mx, l[sp]);
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (mx != kNegInf) {
     float wsum = 0.f;
 #pragma unroll
     for (int sp = 0; sp < kMaxVideoSplits; ++sp) {
       if (l[sp] == kNegInf) continue;
       const float e = fast_exp2(l[sp] - mx);
-      acc += e * (f32x4){bf16_lo(w[sp][0]), bf16_hi(w[sp][0]), bf16_lo(w[sp][1]), bf16_hi(w[sp][1])};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] += e * bf16_lo(w[sp][i]);
+        acc[2 * i + 1] += e * bf16_hi(w[sp][i]);
+      }
       wsum += e;
     }
-    acc *= 1.0f / wsum;
+    const float inv = 1.0f / wsum;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] *= inv;
   }
-  u32x2 o;
-  o[0] = pack_bf16(acc[0], acc[1]);
-  o[1] = pack_bf16(acc[2], acc[3]);
-  *reinterpret_cast<u32x2*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = o;
+  u32x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = pack_bf16(acc[2 * i], acc[2 * i + 1]);
+  *reinterpret_cast<u32x4*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = o;
 }
 
 }  // namespace
@@ -1578,7 +1584,7 @@ hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   const int rows = a.num_heads * a.n_q;
   if (a.n_groups > 0) {
-    hipLaunchKernelGGL(video_combine_kernel, dim3((rows + 7) / 8), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(video_combine_kernel, dim3((rows + 15) / 16), dim3(256), 0, stream, a);
     return hipGetLastError();
   }
   int groups = 1;
