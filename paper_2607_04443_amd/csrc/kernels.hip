@@ -874,13 +874,6 @@ struct VideoSeg {
   int head, p_begin, p_end, seg, n_seg;
 };
 
-// The first of `groups` even shares of `units` (share g = [g U / G,
-// (g+1) U / G)) that holds unit x.  Used by the video kernel and by the
-// combine kernel, which must agree on how many key ranges a head has.
-__device__ __forceinline__ int64_t video_group_of(int64_t x, int64_t groups, int64_t units) {
-  return ((x + 1) * groups + units - 1) / units - 1;
-}
-
 __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg& sg, int qtile,
                                               bool first_segment) {
   // Lane-derived values (LDS and load offsets) are recomputed per segment:
@@ -1135,11 +1128,10 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 
 __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
   // Work decode.  The grid is n_groups groups of n_qtiles workgroups; group g
-  // takes the (head, page) units [g U / G, (g+1) U / G) of the head-major
-  // order (U = heads x visible pages, G = n_groups), one workgroup per query
-  // tile, so every workgroup gets an even share of the pages in a single
-  // round, and a share that crosses a head boundary is processed as two
-  // segments.  Workgroups are dispatched round-robin over the 8 XCDs;
+  // takes a contiguous share of the (head, page) units in head-major order
+  // (VideoPartition: even shares of pages plus a cost per head started), one
+  // workgroup per query tile, so the work fits a single round, and a share
+  // that crosses a head boundary is processed as two segments.  Workgroups are dispatched round-robin over the 8 XCDs;
   // renumber so that consecutive work items (the query tiles of a group,
   // which read the same pages at the same time, and neighbouring groups) run
   // on one XCD and share its L2.
@@ -1154,14 +1146,14 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
       video_segment(a, VideoSeg{static_cast<int>(group), 0, 0, 0, 1}, qtile, true);
     return;
   }
-  const int64_t units = static_cast<int64_t>(a.num_heads) * n_pages, groups = a.n_groups;
-  const int64_t lo = group * units / groups, hi = (group + 1) * units / groups;
+  const VideoPartition part{a.num_heads, n_pages, a.seg_cost, a.n_groups};
+  const int64_t lo = video_group_lo(part, group), hi = video_group_lo(part, group + 1);
   bool first = true;
   for (int64_t x = lo; x < hi; first = false) {
     const int64_t head = x / n_pages, h0 = head * n_pages;
     const int64_t x_end = min(hi, h0 + n_pages);
-    const int64_t g_first = video_group_of(h0, groups, units);
-    const int64_t g_last = video_group_of(h0 + n_pages - 1, groups, units);
+    const int64_t g_first = video_group_of(part, h0);
+    const int64_t g_last = video_group_of(part, h0 + n_pages - 1);
     const VideoSeg sg{static_cast<int>(head), static_cast<int>(x - h0), static_cast<int>(x_end - h0),
                       static_cast<int>(group - g_first), static_cast<int>(g_last - g_first + 1)};
     video_segment(a, sg, qtile, first);
@@ -1504,7 +1496,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
 
 // ------------------------------------------------------------------------- //
 // video_combine: merges the key ranges of the video schedule.  A head's
-// range count follows from the groups' even shares of heads x pages (a head
+// range count follows from the groups' shares (VideoPartition; a head
 // in one range was written in bf16 by the attention kernel: nothing to
 // merge).  16 threads per (head, query) row, 8 d each (16-byte loads), 16
 // rows per block; all of a row's (at most kMaxVideoSplits) partials are
@@ -1515,9 +1507,9 @@ __global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a)
   const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (row >= a.num_heads * a.n_q) return;
   const int head = row / a.n_q, q = row % a.n_q;
-  const int64_t units = static_cast<int64_t>(a.num_heads) * a.n_pages, h0 = static_cast<int64_t>(head) * a.n_pages;
-  const int n_ranges = static_cast<int>(video_group_of(h0 + a.n_pages - 1, a.n_groups, units) -
-                                        video_group_of(h0, a.n_groups, units) + 1);
+  const VideoPartition part{a.num_heads, a.n_pages, a.seg_cost, a.n_groups};
+  const int64_t h0 = static_cast<int64_t>(head) * a.n_pages;
+  const int n_ranges = static_cast<int>(video_group_of(part, h0 + a.n_pages - 1) - video_group_of(part, h0) + 1);
   if (n_ranges < 2) return;
   const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;

@@ -312,6 +312,11 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
 // MI355X: ~15 us against ~1.6 us per page), and every head split into more
 // than one range is merged by the combine kernel.  A forced split count s
 // gives H * s groups: every head in s equal key ranges.
+// Partition cost of starting a head's segment inside a workgroup's share, in
+// pages: the segment switch (epilogue stores, query load, key-norm bound,
+// pipeline refill) takes about as long as six pages of the main loop.
+constexpr int kVideoSegCostPages = 6;
+
 int choose_video_groups(const ws_cache* c, int n_heads, int n_qtiles, int n_pages) {
   if (n_pages == 0) return n_heads;
   if (c->opt_video_splits > 0) return n_heads * c->opt_video_splits;
@@ -436,6 +441,8 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
                                : std::max<int64_t>(2, (groups + H - 1) / H + 1);
     if (cap < max_ranges) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
     a.n_groups = groups;
+    // forced splits keep equal ranges per head
+    a.seg_cost = c->opt_video_splits > 0 ? 0 : kVideoSegCostPages;
     a.n_splits = 1;
     splits = groups;
     merge = n_pages > 0 && groups != H;
@@ -458,6 +465,7 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
                                        kMaxVideoSplits, (splits + H - 1) / H + 1));
     cb.n_groups = audio ? 0 : splits;
     cb.n_pages = n_pages;
+    cb.seg_cost = a.seg_cost;
     cb.n_q = n_q;
     cb.num_heads = H;
     cb.out = a.out;

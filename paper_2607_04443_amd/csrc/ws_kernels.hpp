@@ -34,6 +34,34 @@ __host__ __device__ constexpr int v_tile_index(int slot, int d) {
 // Device error flags (ws_cache_check).
 constexpr uint32_t kFlagPositionClamped = 1u;
 
+// Video work partition.  For one query tile the (head, page) units are laid
+// on a line in head-major order with seg_cost extra places in front of
+// every head (the price of starting a head: query load, key-norm bound,
+// pipeline refill), and group g takes the units whose place falls in
+// [floor(g L / G), floor((g+1) L / G)), L = heads * (pages + seg_cost): a
+// group whose share starts another head gets correspondingly fewer pages.
+// The attention kernel (shares), the merge kernel (ranges per head) and the
+// host (workspace bound) use these same functions.
+struct VideoPartition {
+  int64_t heads, pages, seg_cost, groups;
+};
+__host__ __device__ inline int64_t video_place(const VideoPartition& p, int64_t x) {
+  const int64_t h = x / p.pages;
+  return h * (p.pages + p.seg_cost) + p.seg_cost + (x - h * p.pages);
+}
+// The group that holds unit x.
+__host__ __device__ inline int64_t video_group_of(const VideoPartition& p, int64_t x) {
+  const int64_t len = p.heads * (p.pages + p.seg_cost);
+  return ((video_place(p, x) + 1) * p.groups + len - 1) / len - 1;
+}
+// The first unit of group g's share (g = groups gives the end).
+__host__ __device__ inline int64_t video_group_lo(const VideoPartition& p, int64_t g) {
+  const int64_t len = p.heads * (p.pages + p.seg_cost);
+  const int64_t v0 = g * len / p.groups;
+  const int64_t h = v0 / (p.pages + p.seg_cost), o = v0 - h * (p.pages + p.seg_cost);
+  return h * p.pages + (o > p.seg_cost ? o - p.seg_cost : 0);
+}
+
 struct RopeTables {
   const float2* tab[3];  // (cos, sin) per band: [max_pos[b]][pairs[b]]
   int32_t max_pos[3];
@@ -107,6 +135,7 @@ struct AttnArgs {
   int32_t n_splits;      // audio: key-range splits (the combine kernel merges them)
   int32_t pages_per_split;
   int32_t n_groups;      // video: workgroup groups sharing the (head, page) units
+  int32_t seg_cost;      // video: partition cost of starting a head (VideoPartition)
   int32_t n_qtiles;
   uint16_t* out;
   int64_t out_tok_stride;
@@ -122,7 +151,8 @@ struct CombineArgs {
   const float* part_lse;
   int32_t n_splits;      // key ranges per head (when n_groups == 0)
   int32_t n_groups;      // > 0: video schedule, ranges per head follow from
-  int32_t n_pages;       //      the groups' even shares of heads x n_pages
+  int32_t n_pages;       //      the groups' shares (VideoPartition)
+  int32_t seg_cost;
   int32_t n_q;
   int32_t num_heads;
   uint16_t* out;
