@@ -55,6 +55,12 @@ def parse():
     ap.add_argument("--audio-splits", type=int, default=0)
     ap.add_argument("--cold-audio-reps", type=int, default=20)
     ap.add_argument("--long-reps", type=int, default=5)
+    ap.add_argument("--pmc-driver", action="store_true",
+                    help="run one step, then the video and audio attention and a 256 MiB device "
+                         "copy three times each, untimed (the program rocprofv3 --pmc runs)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc -f csv runs of --pmc-driver (FETCH_SIZE, "
+                         "WRITE_SIZE) as markdown")
     return ap.parse_args()
 
 
@@ -141,8 +147,135 @@ def long_history(args, ws, sets, gamma, eps, stream, dev):
             "tflops": 4 * video_flop(LU, lk) / (med * 1e-6) / 1e12}
 
 
+COPY_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "unit_attn_traffic.md")
+KERNELS_SRC = os.path.join(ROOT, "paper_2607_04443_amd", "csrc", "kernels.hip")
+
+
+def kernels_sha256():
+    import hashlib
+    with open(KERNELS_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per unit_attn_kernel launch from the committed counter
+    summary, or None when it was taken on other kernel sources."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines()
+                  if line.startswith(("kernels_sha256: ", "unit_attn_traffic_bytes: ")))
+    if fields.get("kernels_sha256") != kernels_sha256() or "unit_attn_traffic_bytes" not in fields:
+        return None
+    return float(fields["unit_attn_traffic_bytes"])
+
+
+def pmc_summary(fetch_dir, write_dir):
+    """Markdown summary of a FETCH_SIZE and a WRITE_SIZE counter run of
+    --pmc-driver: per-dispatch KiB (median over each kernel's dispatches),
+    scaled by what the same counter reads for the 256 MiB device copy."""
+    import csv
+    import glob
+    import statistics
+
+    def per_kernel(d, counter):
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        disp = {}
+        for f in files:
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] != counter:
+                    continue
+                key = (f, r["Dispatch_Id"])
+                name, grid = r["Kernel_Name"], int(r.get("Grid_Size") or 0)
+                disp.setdefault(key, [name, grid, 0.0])[2] += float(r["Counter_Value"])
+        out = {}
+        for name, grid, val in disp.values():
+            out.setdefault(name, []).append((grid, val))
+        return out
+
+    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(table, key):
+        rows = [v for n, vals in table.items() if key in n for v in vals]
+        if key == "copyBuffer":  # the 256 MiB copy: the largest grid
+            g = max(r[0] for r in rows)
+            rows = [r for r in rows if r[0] == g]
+        return statistics.median(v for _, v in rows), len(rows)
+
+    f_copy, _ = pick(fetch, "copyBuffer")
+    w_copy, _ = pick(write, "copyBuffer")
+    f_scale, w_scale = f_copy * 1024 / COPY_BYTES, w_copy * 1024 / COPY_BYTES
+    lines = ["# HBM traffic: unit_attn_kernel and audio_attn_kernel, v0.2 unit with an 8-unit history",
+             "",
+             "Counters per dispatch (median over the driver's dispatches of each kernel), from two",
+             "runs of the same committed program, one counter each (from the repo root on the GPU box):",
+             "",
+             "    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc FETCH_SIZE -d <repo>/gpurun_out/pmc_fetch "
+             "-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver",
+             "    cd /tmp && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -d <repo>/gpurun_out/pmc_write "
+             "-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver",
+             "    python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write",
+             "",
+             f"Calibration: the {COPY_BYTES >> 20} MiB device copy (__amd_rocclr_copyBuffer) reads "
+             f"FETCH_SIZE {f_copy:.0f} KiB and WRITE_SIZE {w_copy:.0f} KiB, i.e. "
+             f"{f_scale:.3f} and {w_scale:.3f} counted bytes per byte moved; the figures below are "
+             "divided by these factors.",
+             "",
+             "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes per launch |",
+             "|---|---|---|---|---|"]
+    result = {}
+    for label, key in (("unit_attn_kernel", "unit_attn_kernel"), ("video_combine_kernel", "video_combine"),
+                       ("audio_attn_kernel", "audio_attn_kernel"), ("combine_kernel (audio)", "combine_kernel<"),
+                       ("kv_append_kernel", "kv_append_kernel")):
+        try:
+            fv, n = pick(fetch, key)
+            wv, _ = pick(write, key)
+        except (ValueError, statistics.StatisticsError):
+            continue
+        b = fv * 1024 / f_scale + wv * 1024 / w_scale
+        result[label] = b
+        lines.append(f"| {label} | {n} | {fv:.0f} | {wv:.0f} | {b / 1e6:.1f} MB |")
+    lk_v = COND + (HIST + 1) * LU
+    kv_bytes = 2.0 * lk_v * H * D * 2
+    lines += ["",
+              f"Video K/V visible to one launch: {kv_bytes / 1e6:.1f} MB (each (head, page) tile is "
+              "read by the four query-tile workgroups; pages the 256 MB cache already holds are not "
+              "fetched from HBM again).",
+              "",
+              f"kernels_sha256: {kernels_sha256()}",
+              f"unit_attn_traffic_bytes: {result.get('unit_attn_kernel', float('nan')):.0f}"]
+    print("\n".join(lines))
+
+
+def pmc_driver(ws, cache, step, u, q_v, out_v, q_a, out_a, vpos, apos, gamma, eps):
+    import torch
+    step(u, False)
+    torch.cuda.synchronize()
+    vmask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
+    amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
+    for _ in range(3):
+        cache.unit_attention(q_v, out_v, vmask, ws.WS_QUERY_PREPARED)
+        torch.cuda.synchronize()
+    for _ in range(3):
+        cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
+        torch.cuda.synchronize()
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=q_v.device)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    log("pmc driver: 1 step, 3 video, 3 audio, 3 copies of", COPY_BYTES >> 20, "MiB")
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
               "multi-GPU path", file=sys.stderr)
@@ -233,6 +366,10 @@ def main():
         cache.evict_before(u - HIST + 1)
 
     u = HIST
+    if args.pmc_driver:
+        pmc_driver(ws, cache, step, u, q_v, out_v, q_a, out_a, vpos, apos, gamma, eps)
+        cache.close()
+        return
     for _ in range(args.warmup):
         step(u, False)
         u += 1
@@ -335,7 +472,7 @@ def main():
         "long_history": long_hist,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic()},
         "cpu_baseline": None,
     }
     cache.close()
