@@ -1447,19 +1447,33 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
   float mx = kNegInf, wsum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   if (row_ok) {
-    for (int sp = g; sp < a.n_splits; sp += kGroups) {
-      const float l = a.part_lse[sp * split_stride + row];
-      if (l == kNegInf) continue;
-      const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + (sp * split_stride + row) * kHeadDim + d0);
-      if (l > mx) {
-        const float sc = fast_exp2(mx - l);
-        acc *= sc;
-        wsum *= sc;
-        mx = l;
+    // the group's splits g, g + kGroups, ..., kBatch at a time, every load of
+    // a batch issued before any is used
+    constexpr int kBatch = 4;
+    for (int sp0 = g; sp0 < a.n_splits; sp0 += kBatch * kGroups) {
+      float lb[kBatch];
+      f32x4 ob[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int sp = sp0 + i * kGroups;
+        lb[i] = sp < a.n_splits ? a.part_lse[sp * split_stride + row] : kNegInf;
+        ob[i] = sp < a.n_splits ? *reinterpret_cast<const f32x4*>(a.part_o + (sp * split_stride + row) * kHeadDim + d0)
+                                : (f32x4){0.f, 0.f, 0.f, 0.f};
       }
-      const float w = fast_exp2(l - mx);
-      acc += w * o;
-      wsum += w;
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const float l = lb[i];
+        if (l == kNegInf) continue;
+        if (l > mx) {
+          const float sc = fast_exp2(mx - l);
+          acc *= sc;
+          wsum *= sc;
+          mx = l;
+        }
+        const float w = fast_exp2(l - mx);
+        acc += w * ob[i];
+        wsum += w;
+      }
     }
   }
   if (kGroups > 1) {
