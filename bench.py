@@ -14,16 +14,20 @@ Sec. 2.1 history commit):
   3. video attention: the 920 prepared queries over 256 + 9 x 920 = 8536
      keys;
   4. audio attention: 4 queries over cond + 9 x (920 + 4) = 8572 keys;
+     steps 3 and 4 are one ws_step_attention call (video kernel, audio
+     kernel, one launch merging both calls' key ranges);
   5. unit u is committed to history and the unit that left the window evicted.
 All inputs are synthetic N(0,1) bf16 resident in HBM; H = 40 heads of 128.
 
 Prints one JSON line.  `value` is attention TFLOP/s over the whole step
 (video + audio FLOP / step time), from `steps` steps timed with nothing
-recorded in between.  A second pass of `steps` steps records events around
-each component (the per-component fields) and the library's launch timing
-(ws_cache_timing_*): `roofline` is for the video attention kernel (the
-dominant one), its FLOP per launch over its average launch time from HIP
-events recorded on the calls' stream around the kernel itself.
+recorded in between.  A second pass of `steps` steps issues the two
+attentions as separate calls (ws_unit_attention, ws_audio_attention, each
+with its own merge) and records events around each component (the
+per-component fields) and the library's launch timing (ws_cache_timing_*):
+`roofline` is for the video attention kernel (the dominant one), its FLOP
+per launch over its average launch time from HIP events recorded on the
+calls' stream around the kernel itself.
 `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
 """
 import argparse
@@ -345,18 +349,18 @@ def main():
                  positions=apos[u], gamma=gamma, eps=eps)],
             [dict(q=s["q"], q_out=q_v, positions=vpos[u], gamma=gamma, eps=eps),
              dict(q=s["qa"], q_out=q_a, positions=apos[u], gamma=gamma, eps=eps)])
+        vmask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
+        amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
+        if not timed:
+            cache.step_attention(dict(q=q_v, out=out_v, mask=vmask, mode=ws.WS_QUERY_PREPARED),
+                                 dict(q=q_a, out=out_a, mask=amask, mode=ws.WS_QUERY_PREPARED))
         if timed:
             e[1].record(stream)
             e[2].record(stream)
-        cache.unit_attention(q_v, out_v, ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
-                             ws.WS_QUERY_PREPARED)
-        if timed:
+            cache.unit_attention(q_v, out_v, vmask, ws.WS_QUERY_PREPARED)
             e[3].record(stream)
             e[4].record(stream)
-        cache.audio_attention(q_a, out_a,
-                              ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO,
-                                                         ws.WS_KIND_AUDIO)),
-                              ws.WS_QUERY_PREPARED)
+            cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
         if timed:
             e[5].record(stream)
             ev["append"].append((e[0], e[1]))

@@ -273,6 +273,31 @@ WS_API ws_status ws_audio_attention(const void* q, int64_t q_tok_stride, int64_t
                              const ws_mask_spec* mask, void* out, int64_t out_tok_stride,
                              int64_t out_head_stride, void* hip_stream);
 
+/* One attention call of ws_step_attention: the arguments of
+ * ws_unit_attention / ws_audio_attention. */
+typedef struct ws_attn_call {
+  const void* q;
+  int64_t q_tok_stride;
+  int64_t q_head_stride;
+  int32_t n_q;
+  ws_query_desc desc;
+  ws_mask_spec mask;
+  void* out;
+  int64_t out_tok_stride;
+  int64_t out_head_stride;
+} ws_attn_call;
+
+/* A denoising step's two attentions over the cache (Sec. 3: the long video
+ * latent queries and the short audio latent queries of the same unit): the
+ * video kernel, the audio kernel, and one launch that merges both calls' key
+ * ranges.  Each output equals what ws_unit_attention(video) and
+ * ws_audio_attention(audio) write, bit for bit; both calls are validated
+ * before anything is enqueued.  video, audio: host structs, read before the
+ * call returns.  The audio call's key ranges use a workspace of their own.  With timing enabled the call records two ring entries: the
+ * video kernel (merge time 0) and the audio kernel with the shared merge. */
+WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, const ws_attn_call* audio,
+                                   void* hip_stream);
+
 /* Debug read-back of one segment in logical order: k_host and v_host receive
  * bf16 [n_tokens][H][128] (contiguous host buffers owned by the caller).
  * Waits for the device.  k_host or v_host may be NULL to skip it. */

@@ -1433,14 +1433,14 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
 // parallel; few splits with many rows (video) use one group per row.
 // ------------------------------------------------------------------------- //
 template <int kGroups>
-__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
+__device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   constexpr int kRowsPerBlock = 8 / kGroups;
   __shared__ float sm_m[8], sm_w[8];
   __shared__ f32x4 sm_acc[8][32];
   const int grp = threadIdx.x >> 5;
   const int lane = threadIdx.x & 31;
   const int g = grp % kGroups;
-  const int row = blockIdx.x * kRowsPerBlock + grp / kGroups;
+  const int row = bid * kRowsPerBlock + grp / kGroups;
   const bool row_ok = row < a.num_heads * a.n_q;
   const int d0 = 4 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
@@ -1508,6 +1508,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
   *reinterpret_cast<u32x2*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = w;
 }
 
+template <int kGroups>
+__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
+  combine_block<kGroups>(a, blockIdx.x);
+}
+
 // ------------------------------------------------------------------------- //
 // video_combine: merges the key ranges of the video schedule.  A head's
 // range count follows from the groups' shares (VideoPartition; a head
@@ -1516,9 +1521,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
 // rows per block; all of a row's (at most kMaxVideoSplits) partials are
 // requested before any is used.
 // ------------------------------------------------------------------------- //
-__global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a) {
+__device__ __forceinline__ void video_combine_block(const CombineArgs& a, int bid) {
   const int lane = threadIdx.x & 15;
-  const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int row = bid * 16 + (threadIdx.x >> 4);
   if (row >= a.num_heads * a.n_q) return;
   const int head = row / a.n_q, q = row % a.n_q;
   const VideoPartition part{a.num_heads, a.n_pages, a.seg_cost, a.n_groups};
@@ -1567,6 +1572,21 @@ __global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a)
   *reinterpret_cast<u32x4*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = o;
 }
 
+__global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a) {
+  video_combine_block(a, blockIdx.x);
+}
+
+// The merges of one step's video and audio calls in one launch: blocks below
+// n_video merge video rows, the rest audio rows.
+template <int kGroups>
+__global__ __launch_bounds__(256) void step_combine_kernel(const CombineArgs v, const CombineArgs au,
+                                                           int n_video) {
+  if (static_cast<int>(blockIdx.x) < n_video)
+    video_combine_block(v, blockIdx.x);
+  else
+    combine_block<kGroups>(au, blockIdx.x - n_video);
+}
+
 }  // namespace
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
@@ -1587,14 +1607,36 @@ hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+namespace {
+int audio_combine_groups(const CombineArgs& a) {
+  const int rows = a.num_heads * a.n_q;
+  if (rows >= 4096) return 1;
+  return a.n_splits >= 8 ? 8 : a.n_splits >= 4 ? 4 : a.n_splits >= 2 ? 2 : 1;
+}
+}  // namespace
+
+hipError_t launch_step_combine(const CombineArgs& v, const CombineArgs& au, hipStream_t stream) {
+  const int n_video = v.n_groups > 0 ? (v.num_heads * v.n_q + 15) / 16 : 0;
+  const int groups = au.num_heads > 0 ? audio_combine_groups(au) : 1;
+  const int n_audio = au.num_heads > 0 ? (au.num_heads * au.n_q + 8 / groups - 1) / (8 / groups) : 0;
+  if (n_video + n_audio == 0) return hipSuccess;
+  const dim3 grid(n_video + n_audio);
+  switch (groups) {
+    case 8: hipLaunchKernelGGL(step_combine_kernel<8>, grid, dim3(256), 0, stream, v, au, n_video); break;
+    case 4: hipLaunchKernelGGL(step_combine_kernel<4>, grid, dim3(256), 0, stream, v, au, n_video); break;
+    case 2: hipLaunchKernelGGL(step_combine_kernel<2>, grid, dim3(256), 0, stream, v, au, n_video); break;
+    default: hipLaunchKernelGGL(step_combine_kernel<1>, grid, dim3(256), 0, stream, v, au, n_video); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   const int rows = a.num_heads * a.n_q;
   if (a.n_groups > 0) {
     hipLaunchKernelGGL(video_combine_kernel, dim3((rows + 15) / 16), dim3(256), 0, stream, a);
     return hipGetLastError();
   }
-  int groups = 1;
-  if (rows < 4096) groups = a.n_splits >= 8 ? 8 : a.n_splits >= 4 ? 4 : a.n_splits >= 2 ? 2 : 1;
+  const int groups = audio_combine_groups(a);
   const int rows_per_block = 8 / groups;
   dim3 grid((rows + rows_per_block - 1) / rows_per_block);
   switch (groups) {

@@ -81,9 +81,11 @@ struct ws_cache {
   size_t arena_used = 0;
   ListCacheEntry lists[4];
   int list_next = 0;
-  float* part_o = nullptr;
+  float* part_o = nullptr;    // video key-range partials
   float* part_lse = nullptr;
-  int64_t part_rows = 0;  // capacity in (split, head, query) rows
+  float* apart_o = nullptr;   // audio key-range partials (a separate workspace, so
+  float* apart_lse = nullptr; // that one step's two paths can be merged together)
+  int64_t part_rows = 0;  // capacity of each workspace in (split, head, query) rows
   int32_t opt_video_splits = 0;
   int32_t opt_audio_splits = 0;
   int32_t opt_running_max = 0;
@@ -226,6 +228,8 @@ void free_all(ws_cache* c) {
   if (c->arena_host) (void)hipHostFree(c->arena_host);
   if (c->part_o) (void)hipFree(c->part_o);
   if (c->part_lse) (void)hipFree(c->part_lse);
+  if (c->apart_o) (void)hipFree(c->apart_o);
+  if (c->apart_lse) (void)hipFree(c->apart_lse);
   if (c->knorm2) (void)hipFree(c->knorm2);
   if (c->zeros) (void)hipFree(c->zeros);
   c->knorm2 = nullptr;
@@ -234,7 +238,7 @@ void free_all(ws_cache* c) {
   c->rope_dev = nullptr;
   c->flags_dev = nullptr;
   c->arena_dev = c->arena_host = nullptr;
-  c->part_o = c->part_lse = nullptr;
+  c->part_o = c->part_lse = c->apart_o = c->apart_lse = nullptr;
 }
 
 ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
@@ -300,6 +304,10 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
     return bail(hip_fail(e, "hipMalloc(partials)"));
   if ((e = hipMalloc(&c->part_lse, static_cast<size_t>(c->part_rows) * sizeof(float))) != hipSuccess)
     return bail(hip_fail(e, "hipMalloc(partials)"));
+  if ((e = hipMalloc(&c->apart_o, static_cast<size_t>(c->part_rows) * ws::kHeadDim * sizeof(float))) != hipSuccess)
+    return bail(hip_fail(e, "hipMalloc(partials)"));
+  if ((e = hipMalloc(&c->apart_lse, static_cast<size_t>(c->part_rows) * sizeof(float))) != hipSuccess)
+    return bail(hip_fail(e, "hipMalloc(partials)"));
   *out = c;
   return WS_OK;
 }
@@ -356,10 +364,19 @@ float scale_log2_of(float softmax_scale) {
   return static_cast<float>(scale * 1.4426950408889634);
 }
 
-ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+// One attention call, validated and resolved into launch arguments.
+struct AttnPlan {
+  bool audio = false;
+  ws::AttnArgs a{};
+  bool merge = false;
+  ws::CombineArgs cb{};
+  int splits = 1;  // audio: key ranges; video: workgroup groups
+};
+
+ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
                          int32_t n_q, const ws_query_desc* qd, ws_cache* c, const ws_mask_spec* m,
                          void* out, int64_t out_tok_stride, int64_t out_head_stride,
-                         void* hip_stream) {
+                         hipStream_t stream, AttnPlan* plan) {
   if (!c || !qd || !m) return fail(WS_ERR_INVALID_ARG, "NULL argument");
   if (ws_status st = check_device(c); st != WS_OK) return st;
   const int H = c->cfg.num_heads;
@@ -377,11 +394,12 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   }
   if (!std::isfinite(qd->softmax_scale) || qd->softmax_scale < 0.f)
     return fail(WS_ERR_INVALID_ARG, "bad softmax_scale");
-  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
 
   // The visible page list goes into the kernel arguments when it fits, else
   // into the device arena (one upload per distinct list).
-  ws::AttnArgs a{};
+  plan->audio = audio;
+  ws::AttnArgs& a = plan->a;
+  a = ws::AttnArgs{};
   const int2* plist = nullptr;
   int32_t n_pages = 0;
   c->pt.visible_pages(ws::MaskSpec{m->q_unit, m->min_visible_unit, m->kind_mask}, &c->scratch_list);
@@ -414,8 +432,8 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
   a.out = static_cast<uint16_t*>(out);
   a.out_tok_stride = out_tok_stride;
   a.out_head_stride = out_head_stride;
-  a.part_o = c->part_o;
-  a.part_lse = c->part_lse;
+  a.part_o = audio ? c->apart_o : c->part_o;
+  a.part_lse = audio ? c->apart_lse : c->part_lse;
   a.flags = c->flags_dev;
   const int qtile = audio ? ws::kAudioQTile : ws::kVideoQTile;
   a.n_qtiles = (n_q + qtile - 1) / qtile;
@@ -448,19 +466,13 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
     merge = n_pages > 0 && groups != H;
   }
 
-  TimingRing& tr = c->timing;
-  const int slot = tr.cap > 0 ? tr.next : -1;
-  if (slot >= 0) {
-    tr.meta[slot] = ws_call_timing{audio ? 1 : 0, splits, 0.f, 0.f};
-    WS_HIP(hipEventRecord(tr.ev[3 * slot], stream));
-  }
-  hipError_t e = audio ? ws::launch_audio_attention(a, stream) : ws::launch_unit_attention(a, stream);
-  if (e != hipSuccess) return hip_fail(e, audio ? "audio_attn launch" : "unit_attn launch");
-  if (slot >= 0) WS_HIP(hipEventRecord(tr.ev[3 * slot + 1], stream));
+  plan->splits = splits;
+  plan->merge = merge;
   if (merge) {
-    ws::CombineArgs cb{};
-    cb.part_o = c->part_o;
-    cb.part_lse = c->part_lse;
+    ws::CombineArgs& cb = plan->cb;
+    cb = ws::CombineArgs{};
+    cb.part_o = a.part_o;
+    cb.part_lse = a.part_lse;
     cb.n_splits = audio ? splits : static_cast<int>(std::min<int64_t>(
                                        kMaxVideoSplits, (splits + H - 1) / H + 1));
     cb.n_groups = audio ? 0 : splits;
@@ -471,15 +483,52 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
     cb.out = a.out;
     cb.out_tok_stride = out_tok_stride;
     cb.out_head_stride = out_head_stride;
-    e = ws::launch_combine(cb, stream);
-    if (e != hipSuccess) return hip_fail(e, "combine launch");
   }
-  if (slot >= 0) {
-    WS_HIP(hipEventRecord(tr.ev[3 * slot + 2], stream));
+  return WS_OK;
+}
+
+hipError_t launch_plan_kernel(const AttnPlan& p, hipStream_t stream) {
+  return p.audio ? ws::launch_audio_attention(p.a, stream) : ws::launch_unit_attention(p.a, stream);
+}
+
+// Timing ring slot of the next call (or -1), with its first event recorded.
+ws_status timing_begin(ws_cache* c, const AttnPlan& p, hipStream_t stream, int* slot) {
+  TimingRing& tr = c->timing;
+  *slot = tr.cap > 0 ? tr.next : -1;
+  if (*slot >= 0) {
+    tr.meta[*slot] = ws_call_timing{p.audio ? 1 : 0, p.splits, 0.f, 0.f};
+    WS_HIP(hipEventRecord(tr.ev[3 * *slot], stream));
     tr.next = (tr.next + 1) % tr.cap;
     tr.count = std::min(tr.count + 1, tr.cap);
   }
   return WS_OK;
+}
+
+ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream) {
+  if (slot >= 0) WS_HIP(hipEventRecord(c->timing.ev[3 * slot + k], stream));
+  return WS_OK;
+}
+
+ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+                         int32_t n_q, const ws_query_desc* qd, ws_cache* c, const ws_mask_spec* m,
+                         void* out, int64_t out_tok_stride, int64_t out_head_stride,
+                         void* hip_stream) {
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  AttnPlan p;
+  if (ws_status st = plan_attention(audio, q, q_tok_stride, q_head_stride, n_q, qd, c, m, out, out_tok_stride,
+                                    out_head_stride, stream, &p);
+      st != WS_OK)
+    return st;
+  int slot = -1;
+  if (ws_status st = timing_begin(c, p, stream, &slot); st != WS_OK) return st;
+  hipError_t e = launch_plan_kernel(p, stream);
+  if (e != hipSuccess) return hip_fail(e, audio ? "audio_attn launch" : "unit_attn launch");
+  if (ws_status st = timing_mark(c, slot, 1, stream); st != WS_OK) return st;
+  if (p.merge) {
+    e = ws::launch_combine(p.cb, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine launch");
+  }
+  return timing_mark(c, slot, 2, stream);
 }
 
 }  // namespace
@@ -748,6 +797,39 @@ ws_status ws_audio_attention(const void* q, int64_t q_tok_stride, int64_t q_head
                              void* hip_stream) {
   return attention_impl(true, q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
                         out_tok_stride, out_head_stride, hip_stream);
+}
+
+ws_status ws_step_attention(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio, void* hip_stream) {
+  if (!c || !video || !audio) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  AttnPlan pv, pa;
+  if (ws_status st = plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, video->n_q,
+                                    &video->desc, c, &video->mask, video->out, video->out_tok_stride,
+                                    video->out_head_stride, stream, &pv);
+      st != WS_OK)
+    return st;
+  if (ws_status st = plan_attention(true, audio->q, audio->q_tok_stride, audio->q_head_stride, audio->n_q,
+                                    &audio->desc, c, &audio->mask, audio->out, audio->out_tok_stride,
+                                    audio->out_head_stride, stream, &pa);
+      st != WS_OK)
+    return st;
+  // video kernel, audio kernel, then one launch merging both
+  int sv = -1, sa = -1;
+  if (ws_status st = timing_begin(c, pv, stream, &sv); st != WS_OK) return st;
+  hipError_t e = launch_plan_kernel(pv, stream);
+  if (e != hipSuccess) return hip_fail(e, "unit_attn launch");
+  if (ws_status st = timing_mark(c, sv, 1, stream); st != WS_OK) return st;
+  if (ws_status st = timing_mark(c, sv, 2, stream); st != WS_OK) return st;
+  if (ws_status st = timing_begin(c, pa, stream, &sa); st != WS_OK) return st;
+  e = launch_plan_kernel(pa, stream);
+  if (e != hipSuccess) return hip_fail(e, "audio_attn launch");
+  if (ws_status st = timing_mark(c, sa, 1, stream); st != WS_OK) return st;
+  if (pv.merge || pa.merge) {
+    ws::CombineArgs none{};
+    e = ws::launch_step_combine(pv.merge ? pv.cb : none, pa.merge ? pa.cb : none, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine launch");
+  }
+  return timing_mark(c, sa, 2, stream);
 }
 
 ws_status ws_cache_export(ws_cache* c, int32_t unit, ws_kind kind, void* k_host, void* v_host) {

@@ -169,6 +169,9 @@ hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
 // pages loaded straight into registers, 16x16x32 bf16 MFMA.
 hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+// The merges of a video call (n_groups > 0) and an audio call (num_heads > 0)
+// in one launch; either may be absent (zero-initialised).
+hipError_t launch_step_combine(const CombineArgs& video, const CombineArgs& audio, hipStream_t stream);
 
 constexpr int kVideoQTile = 256;
 constexpr int kMaxVideoSplits = 8;  // key-range splits of the video kernel

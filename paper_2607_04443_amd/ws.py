@@ -82,6 +82,13 @@ class ws_mask_spec(ctypes.Structure):
                 ("kind_mask", ctypes.c_uint32)]
 
 
+class ws_attn_call(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("q_tok_stride", ctypes.c_int64),
+                ("q_head_stride", ctypes.c_int64), ("n_q", ctypes.c_int32),
+                ("desc", ws_query_desc), ("mask", ws_mask_spec), ("out", ctypes.c_void_p),
+                ("out_tok_stride", ctypes.c_int64), ("out_head_stride", ctypes.c_int64)]
+
+
 class ws_cache_stats(ctypes.Structure):
     _fields_ = [("pages_total", ctypes.c_int32), ("pages_free", ctypes.c_int32),
                 ("n_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
@@ -108,6 +115,7 @@ _SIGS = {
                           _i64, _i64, _vp],
     "ws_audio_attention": [_vp, _i64, _i64, _i32, _P(ws_query_desc), _vp, _P(ws_mask_spec), _vp,
                            _i64, _i64, _vp],
+    "ws_step_attention": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_cache_export": [_vp, _i32, _i32, _vp, _vp],
     "ws_segment_tokens": [_vp, _i32, _i32, _P(_i32)],
     "ws_cache_info": [_vp, _P(ws_cache_stats)],
@@ -196,6 +204,11 @@ def ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, 
     _check(_lib.ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, ctypes.byref(qdesc), cache,
                                    ctypes.byref(mask), out, out_tok_stride, out_head_stride,
                                    stream), "ws_audio_attention")
+
+
+def ws_step_attention(cache, video: ws_attn_call, audio: ws_attn_call, stream):
+    _check(_lib.ws_step_attention(cache, ctypes.byref(video), ctypes.byref(audio), stream),
+           "ws_step_attention")
 
 
 def ws_cache_export(cache, unit, kind, k_host, v_host):
@@ -348,6 +361,29 @@ class Cache:
         fn(q.data_ptr(), q.stride(0), q.stride(1), q.shape[0], qd, self.handle, mask,
            out.data_ptr(), out.stride(0), out.stride(1), _stream_handle(stream))
         return out
+
+    @staticmethod
+    def _call(q, out, mask, mode=WS_APPEND_NORM_ROPE, positions=None, gamma=None, eps=1e-6,
+              scale=0.0):
+        import torch
+        _check_tensor("q", q, torch.bfloat16)
+        _check_tensor("out", out, torch.bfloat16)
+        c = ws_attn_call()
+        c.q, c.q_tok_stride, c.q_head_stride, c.n_q = q.data_ptr(), q.stride(0), q.stride(1), q.shape[0]
+        d = c.desc
+        d.mode = mode
+        d.positions = positions.data_ptr() if positions is not None else None
+        d.gamma = gamma.data_ptr() if gamma is not None else None
+        d.eps, d.softmax_scale = eps, scale
+        c.mask = mask
+        c.out, c.out_tok_stride, c.out_head_stride = out.data_ptr(), out.stride(0), out.stride(1)
+        return c
+
+    def step_attention(self, video, audio, stream=None):
+        """video, audio: dicts with the arguments of unit_attention /
+        audio_attention (q, out, mask, mode, positions, gamma, eps, scale)."""
+        ws_step_attention(self.handle, self._call(**video), self._call(**audio),
+                          _stream_handle(stream))
 
     def unit_attention(self, q, out, mask, mode=WS_APPEND_NORM_ROPE, positions=None, gamma=None,
                        eps=1e-6, scale=0.0, stream=None):

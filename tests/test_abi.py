@@ -78,6 +78,9 @@ int main(void) {
   S(ws_query_item) P(ws_query_item, tok_stride) P(ws_query_item, head_stride) P(ws_query_item, n_q)
   P(ws_query_item, desc) P(ws_query_item, q_out) P(ws_query_item, out_tok_stride)
   P(ws_query_item, out_head_stride)
+  S(ws_attn_call) P(ws_attn_call, q_tok_stride) P(ws_attn_call, n_q) P(ws_attn_call, desc)
+  P(ws_attn_call, mask) P(ws_attn_call, out) P(ws_attn_call, out_tok_stride)
+  P(ws_attn_call, out_head_stride)
   printf("max_items %d\n", WS_MAX_APPEND_ITEMS);
   printf("max_query_items %d\n", WS_MAX_QUERY_ITEMS);
   printf("prepared %d\n", (int)WS_QUERY_PREPARED);
@@ -108,7 +111,7 @@ def test_struct_layouts_match_c(tmp_path):
                       ("ws_mask_spec", ws.ws_mask_spec), ("ws_cache_stats", ws.ws_cache_stats),
                       ("ws_call_timing", ws.ws_call_timing),
                       ("ws_append_item", ws.ws_append_item),
-                      ("ws_query_item", ws.ws_query_item)):
+                      ("ws_query_item", ws.ws_query_item), ("ws_attn_call", ws.ws_attn_call)):
         assert ctypes.sizeof(typ) == c[name], name
         for key, off in c.items():
             if key.startswith(name + "."):

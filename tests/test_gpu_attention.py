@@ -499,3 +499,42 @@ def test_prepared_step_parity(ws, name):
         assert e["frob"] <= 2e-3, e
     finally:
         L.close()
+
+
+@pytest.mark.parametrize("name,splits", [("audio_c256", 0), ("audio_c256", 3)])
+def test_step_attention_equals_separate_calls(ws, name, splits):
+    """ws_step_attention (video kernel, audio kernel, one launch merging both)
+    writes exactly what ws_unit_attention and ws_audio_attention write, with
+    and without video key ranges to merge; with timing on it records the two
+    calls."""
+    import torch
+    wl = synth.make_workload(name)
+    L = Loaded(ws, wl)
+    try:
+        if splits:
+            L.cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, splits)
+        st = wl.steps[0]
+        qv, qa = to_dev(st.q_video), to_dev(st.q_audio)
+        pv, pa = dev_i32(st.q_video_pos), dev_i32(st.q_audio_pos)
+        vmask = ws.mask_spec(wl.current_unit, -(2 ** 31), VIDEO_KINDS)
+        amask = ws.mask_spec(wl.current_unit, -(2 ** 31), ALL_KINDS)
+        sep_v, sep_a = torch.full_like(qv, float("nan")), torch.full_like(qa, float("nan"))
+        L.cache.unit_attention(qv, sep_v, vmask, ws.WS_APPEND_NORM_ROPE, pv, L.gq, wl.eps)
+        L.cache.audio_attention(qa, sep_a, amask, ws.WS_APPEND_NORM_ROPE, pa, L.gq, wl.eps)
+        L.cache.timing_enable(4)
+        step_v, step_a = torch.full_like(qv, float("nan")), torch.full_like(qa, float("nan"))
+        L.cache.step_attention(
+            dict(q=qv, out=step_v, mask=vmask, mode=ws.WS_APPEND_NORM_ROPE, positions=pv,
+                 gamma=L.gq, eps=wl.eps),
+            dict(q=qa, out=step_a, mask=amask, mode=ws.WS_APPEND_NORM_ROPE, positions=pa,
+                 gamma=L.gq, eps=wl.eps))
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(from_dev(step_v), from_dev(sep_v))
+        np.testing.assert_array_equal(from_dev(step_a), from_dev(sep_a))
+        rec = L.cache.timing_read()
+        assert [r["path"] for r in rec] == ["video", "audio"]
+        assert all(r["attn_us"] > 0 for r in rec) and rec[1]["merge_us"] > 0
+        ref = L.oracle(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+        assert_gates(bf16_f64(from_dev(step_a)), ref, label=f"{name} step audio")
+    finally:
+        L.close()
