@@ -52,8 +52,10 @@ def video_flop(lq, lk):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The GPU takes about 20 ms of this load (some 100 steps) to settle: with
+    # 5 warm-up steps the first 50 timed steps average about 10% slower.
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--video-splits", type=int, default=0)
     ap.add_argument("--audio-splits", type=int, default=0)
