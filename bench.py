@@ -387,13 +387,14 @@ def main():
     for _ in range(args.steps):
         step(u, False)
         u += 1
+    enqueued = time.perf_counter() - t0  # host time to issue the steps
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
     # A second pass of `steps` steps for the breakdown: events around each
     # component, and the library's launch timing of the attention calls (HIP
     # events on the calls' stream around each kernel).
-    cache.timing_enable(2 * args.steps + 8)
+    cache.timing_enable(3 * args.steps + 8)
     for _ in range(args.steps):
         step(u, True)
         u += 1
@@ -412,7 +413,9 @@ def main():
     lk_a = COND + (HIST + 1) * (LU + AUDIO)
     fv = video_flop(LU, lk_v)
     fa = 4.0 * H * AUDIO * lk_a * D
-    t_video, t_audio, t_append = avg_us("video"), avg_us("audio"), avg_us("append")
+    # the append launch from the library's own events (the events around the
+    # call would also take in the host's time to issue it)
+    t_video, t_audio, t_append = avg_us("video"), avg_us("audio"), kernel_us("append", "attn_us")
     audio_bytes = 2.0 * lk_a * H * D * 2 + 2.0 * AUDIO * H * D * 2
     append_bytes = 4.0 * (COND + LU + AUDIO) * H * D * 2 + 2.0 * (LU + AUDIO) * H * D * 2
 
@@ -470,6 +473,9 @@ def main():
                                f"over {lk_a} keys; cond slice {COND}; 64-token pages",
                    "global_batch": 1, "seq_len": lk_v, "parallelism": "single GPU"},
         "us_per_unit": ms_per_step * 1e3,
+        # host (Python + library) time to enqueue one step; the step is
+        # GPU-bound while this stays below us_per_unit
+        "host_enqueue_us_per_step": enqueued * 1e6 / args.steps,
         "video_attention": {"us": t_video, "tflops": fv / (t_video * 1e-6) / 1e12, "flop": fv,
                             "kernel_us": t_vkern, "merge_us": t_vmerge, "splits": v_splits},
         "audio_attention": {"us_warm": t_audio, "gbps_warm": audio_bytes / (t_audio * 1e-6) / 1e9,

@@ -321,11 +321,13 @@ WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t val
  * profilers).  While enabled, every ws_unit_attention / ws_audio_attention
  * call records three HIP events on its own stream: before its attention
  * kernel, between that kernel and the split-KV merge kernel, and after the
- * merge.  The cache keeps the events of the last `capacity` calls in a ring
- * (older calls are overwritten); recording adds no synchronization. */
+ * merge; every append call (ws_kv_append, ws_kv_append_many, ws_step_append)
+ * records events before its first and after its last launch (merge time 0).
+ * The cache keeps the events of the last `capacity` calls in a ring (older
+ * calls are overwritten); recording adds no synchronization. */
 typedef struct ws_call_timing {
-  int32_t path;      /* 0 = ws_unit_attention (video), 1 = ws_audio_attention */
-  int32_t n_splits;  /* audio: key-range splits; video: workgroup groups */
+  int32_t path;      /* 0 = video attention, 1 = audio attention, 2 = append */
+  int32_t n_splits;  /* audio: key-range splits; video: workgroup groups; append: items */
   float attn_us;     /* attention kernel, microseconds */
   float merge_us;    /* merge kernel, microseconds (0 when there is none) */
 } ws_call_timing;

@@ -492,16 +492,20 @@ hipError_t launch_plan_kernel(const AttnPlan& p, hipStream_t stream) {
 }
 
 // Timing ring slot of the next call (or -1), with its first event recorded.
-ws_status timing_begin(ws_cache* c, const AttnPlan& p, hipStream_t stream, int* slot) {
+ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot) {
   TimingRing& tr = c->timing;
   *slot = tr.cap > 0 ? tr.next : -1;
   if (*slot >= 0) {
-    tr.meta[*slot] = ws_call_timing{p.audio ? 1 : 0, p.splits, 0.f, 0.f};
+    tr.meta[*slot] = ws_call_timing{path, splits, 0.f, 0.f};
     WS_HIP(hipEventRecord(tr.ev[3 * *slot], stream));
     tr.next = (tr.next + 1) % tr.cap;
     tr.count = std::min(tr.count + 1, tr.cap);
   }
   return WS_OK;
+}
+
+ws_status timing_begin(ws_cache* c, const AttnPlan& p, hipStream_t stream, int* slot) {
+  return timing_begin_path(c, p.audio ? 1 : 0, p.splits, stream, slot);
 }
 
 ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream) {
@@ -669,6 +673,11 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
   a.rope = c->rope;
   a.flags = c->flags_dev;
   int n_segs = 0;
+  int tslot = -1;
+  if (ws_status st = timing_begin_path(c, 2, n + n_q, stream, &tslot); st != WS_OK) {
+    roll_back();
+    return st;
+  }
   auto flush = [&]() -> hipError_t {
     if (a.n_blocks == 0) return hipSuccess;
     const hipError_t e = ws::launch_kv_append(a, stream);
@@ -760,7 +769,8 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
     roll_back();
     return hip_fail(e, "kv_append launch");
   }
-  return WS_OK;
+  if (ws_status st = timing_mark(c, tslot, 1, stream); st != WS_OK) return st;
+  return timing_mark(c, tslot, 2, stream);
 }
 
 ws_status ws_unit_commit(ws_cache* c, int32_t unit) {

@@ -428,9 +428,10 @@ class Cache:
 
     def timing_read(self):
         """Per-call launch timing recorded since the last read, oldest first:
-        dicts with path ('video'/'audio'), n_splits, attn_us, merge_us."""
+        dicts with path ('video'/'audio'/'append'), n_splits, attn_us, merge_us."""
         out = ws_cache_timing_read(self.handle, getattr(self, "_timing_cap", 0))
-        return [dict(path="audio" if t.path else "video", n_splits=t.n_splits, attn_us=t.attn_us,
+        names = {0: "video", 1: "audio", 2: "append"}
+        return [dict(path=names.get(t.path, str(t.path)), n_splits=t.n_splits, attn_us=t.attn_us,
                      merge_us=t.merge_us) for t in out]
 
 

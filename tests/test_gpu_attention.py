@@ -398,6 +398,10 @@ def test_launch_timing_ring(ws):
         for _ in range(6):  # ring of 4 keeps the last 4
             L.run("audio", st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
         assert len(L.cache.timing_read()) == 4
+        # append calls record their launches too (an in-place rewrite here)
+        L.append(st.segments[0])
+        rec = L.cache.timing_read()
+        assert [r["path"] for r in rec] == ["append"] and rec[0]["attn_us"] > 0
         L.cache.timing_enable(0)
         with pytest.raises(ws.WsError):
             L.cache.timing_read()
