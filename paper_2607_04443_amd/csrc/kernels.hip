@@ -787,6 +787,7 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
   // P words: w[0..3] keys 0-15 of a tile (chunk 0 or 2), w[4..7] keys 16-31
   u32x4 pp2, pp3, p0, p1;  // tile 1 of p-1 (chunks 2, 3); tile 0 of p (chunks 0, 1)
   float e_lo = 0.f;        // first exponential of a pair, waiting for its partner
+  float e2_lo = 0.f, e3_lo = 0.f;  // the same for the two halves of the previous tile 1
   auto exp_one = [&](const f32x16& sc, int r, u32x4& dst, int word) {
     const float e = fast_exp2(sc[r]);
     if ((r & 1) == 0) {
@@ -819,14 +820,24 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
       }
     } else {
       if (o < 8) {
+        // all of the previous page's tile 1 is exponentiated here, so that
+        // its registers are free before this page's tile 1 is accumulated
         s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
-        exp_one(ps.s1, o, pp2, o >> 1);
+        const float ea = fast_exp2(ps.s1[o]), eb = fast_exp2(ps.s1[8 + o]);
+        if ((o & 1) == 0) {
+          e2_lo = ea;
+          e3_lo = eb;
+        } else {
+          const uint32_t wa = pack_bf16(e2_lo, ea), wb = pack_bf16(e3_lo, eb);
+          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wa), ones, l, false);
+          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wb), ones, l, false);
+          pp2[o >> 1] = wa;
+          pp3[o >> 1] = wb;
+        }
       } else if (o < 12) {
         st.o[o - 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp2), st.o[o - 8], 0, 0, 0);
-        exp_one(ps.s1, 8 + o - 8, pp3, (o - 8) >> 1);
       } else if (o < 16) {
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 12], o == 12 ? s_init : s1, 0, 0, 0);
-        exp_one(ps.s1, 8 + o - 8, pp3, (o - 8) >> 1);
       } else if (o < 20) {
         st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp3), st.o[o - 16], 0, 0, 0);
         exp_one(s0, o - 16, p0, (o - 16) >> 1);
