@@ -61,6 +61,8 @@ def parse():
     ap.add_argument("--audio-splits", type=int, default=0)
     ap.add_argument("--cold-audio-reps", type=int, default=20)
     ap.add_argument("--long-reps", type=int, default=5)
+    ap.add_argument("--no-peak-probes", dest="peak_probes", action="store_false",
+                    help="skip the calibration probes (measured MFMA and HBM read ceilings)")
     ap.add_argument("--pmc-driver", action="store_true",
                     help="run one step, then the video and audio attention and a 256 MiB device "
                          "copy three times each, untimed (the program rocprofv3 --pmc runs)")
@@ -277,6 +279,39 @@ def pmc_driver(ws, cache, step, u, q_v, out_v, q_a, out_a, vpos, apos, gamma, ep
     log("pmc driver: 1 step, 3 video, 3 audio, 3 copies of", COPY_BYTES >> 20, "MiB")
 
 
+def measured_peaks(ws, torch, stream, dev):
+    """The ceilings this GPU sustains, from the library's calibration probes:
+    a bf16 MFMA loop (2048 workgroups of 4 waves, register operands, about
+    10 ms) and one streaming read of a 2 GiB buffer; medians of 7 timed runs
+    after 3 untimed ones."""
+    sink = torch.zeros(2, dtype=torch.float32, device=dev)
+    buf = torch.zeros(1 << 31, dtype=torch.uint8, device=dev)
+    h = stream.cuda_stream
+
+    def timed(launch):
+        t = []
+        for i in range(10):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            launch()
+            b.record(stream)
+            b.synchronize()
+            if i >= 3:
+                t.append(a.elapsed_time(b) * 1e-3)
+        return sorted(t)[len(t) // 2]
+
+    flop = [0.0]
+
+    def mfma():
+        flop[0] = ws.ws_probe_mfma(2048, 20000, sink.data_ptr(), h)
+
+    t_m = timed(mfma)
+    t_r = timed(lambda: ws.ws_probe_read(buf.data_ptr(), buf.numel(), 4096, sink.data_ptr() + 4, h))
+    del buf
+    return {"mfma_bf16_tflops": flop[0] / t_m / 1e12, "mfma_frac_of_published": flop[0] / t_m / 1e12 / PEAK_BF16_TFLOPS,
+            "hbm_read_gbps": (1 << 31) / t_r / 1e9, "hbm_frac_of_published": (1 << 31) / t_r / 1e9 / PEAK_HBM_GBS}
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -451,6 +486,7 @@ def main():
         del scrub
 
     long_hist = long_history(args, ws, sets, gamma, eps, stream, dev) if args.long_reps > 0 else None
+    peaks = measured_peaks(ws, torch, stream, dev) if args.peak_probes else None
 
     t_vkern, t_vmerge = kernel_us("video", "attn_us"), kernel_us("video", "merge_us")
     v_splits = sorted({c["n_splits"] for c in calls if c["path"] == "video"})
@@ -487,6 +523,11 @@ def main():
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic()},
         "cpu_baseline": None,
     }
+    if peaks is not None:
+        peaks["video_kernel_frac"] = achieved / peaks["mfma_bf16_tflops"]
+        if cold is not None:
+            peaks["audio_cold_frac"] = cold["gbps"] / peaks["hbm_read_gbps"]
+        result["measured_peaks"] = peaks
     cache.close()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline()

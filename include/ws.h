@@ -343,6 +343,26 @@ WS_API ws_status ws_cache_timing_enable(ws_cache* cache, int32_t capacity);
 WS_API ws_status ws_cache_timing_read(ws_cache* cache, ws_call_timing* out, int32_t max,
                                       int32_t* n);
 
+/* Calibration probes: the bf16 MFMA rate and the HBM read rate the GPU
+ * sustains, so that measured rates can be set against measured ceilings as
+ * well as the published peaks.  Each enqueues one kernel on hip_stream and
+ * returns; the caller times it (HIP events on that stream).  Invalid
+ * arguments return WS_ERR_INVALID_ARG before anything is enqueued.
+ *
+ * ws_probe_mfma: `workgroups` (1..65536) workgroups of 4 waves; each wave
+ * issues iters (1..2^24) rounds of 4 independent 32x32x16 bf16 MFMAs on
+ * register operands.  *flop (host) receives the launch's FLOP count.  sink is
+ * a device float[1], written only in a case the arithmetic never reaches.
+ *
+ * ws_probe_read: reads the `bytes` bytes at device address buf once
+ * (16-byte aligned, bytes a positive multiple of 16) with `workgroups`
+ * (1..65536) workgroups of 256 threads; sink is a device uint32[1], likewise
+ * written only in a case that does not occur for ordinary data. */
+WS_API ws_status ws_probe_mfma(int32_t workgroups, int32_t iters, float* sink, double* flop,
+                               void* hip_stream);
+WS_API ws_status ws_probe_read(const void* buf, int64_t bytes, int32_t workgroups, uint32_t* sink,
+                               void* hip_stream);
+
 /* Thread-local message for the last non-OK status ("" if none). */
 WS_API const char* ws_last_error(void);
 

@@ -1,6 +1,7 @@
 """Build of the native libraries, in-tree.
 
-  libws.so       the product: HIP kernels for gfx950 + the C ABI (hipcc)
+  libws.so       the product: HIP kernels for gfx950 (kernels.hip; peaks.hip holds
+                 the calibration probes) + the C ABI (hipcc)
   libws_host.so  host-only page-table entry points for CPU tests (g++)
 """
 import os
@@ -16,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libws.so")
 HOST_LIB_PATH = os.path.join(PKG, "libws_host.so")
 
-HIP_SOURCES = ["kernels.hip", "ws_api.cpp", "pagetable.cpp"]
+HIP_SOURCES = ["kernels.hip", "peaks.hip", "ws_api.cpp", "pagetable.cpp"]
 # Packed fp32 ops are kept out of the generated code on purpose.  The kernels
 # never form NaNs from finite inputs (masked logits are -inf, and no -inf - -inf
 # is evaluated), so NaN-quieting canonicalisations are not needed.

@@ -1,0 +1,78 @@
+// Calibration kernels: the bf16 MFMA rate and the HBM read rate this GPU
+// sustains, so that measured attention rates can be set against measured
+// ceilings as well as the published ones (the published bf16 peak assumes the
+// 2.4 GHz peak engine clock; under a long MFMA load the clock runs lower).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "ws_kernels.hpp"
+
+namespace ws {
+namespace {
+
+using bf16x8 = __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16;
+using f32x16 = __attribute__((__vector_size__(16 * sizeof(float)))) float;
+using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+
+constexpr int kProbeThreads = 256;
+constexpr int kMfmaChains = 4;  // independent accumulators per wave
+
+// Each wave runs iters rounds of kMfmaChains independent 32x32x16 bf16 MFMAs
+// on register operands.  The result is stored only if it equals a value the
+// arithmetic cannot produce (kept so the loop is not removed).
+__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, float* sink) {
+  bf16x8 a, b;
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(float)((threadIdx.x + i) & 7);
+    b[i] = (__bf16)(float)((threadIdx.x * 3 + i) & 7);
+  }
+  f32x16 acc[kMfmaChains];
+  for (int c = 0; c < kMfmaChains; ++c)
+    for (int r = 0; r < 16; ++r) acc[c][r] = 0.0f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < kMfmaChains; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  float s = 0.0f;
+  for (int c = 0; c < kMfmaChains; ++c)
+    for (int r = 0; r < 16; ++r) s += acc[c][r];
+  if (s == -1.0f) sink[0] = s;
+}
+
+// Streams n16 16-byte words once (grid-stride, four independent loads in
+// flight per thread) and folds them with XOR.
+__global__ __launch_bounds__(kProbeThreads) void read_probe_kernel(const u32x4* __restrict__ p,
+                                                                   int64_t n16, uint32_t* sink) {
+  const int64_t stride = int64_t(gridDim.x) * kProbeThreads;
+  int64_t i = int64_t(blockIdx.x) * kProbeThreads + threadIdx.x;
+  u32x4 x = {0u, 0u, 0u, 0u};
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const u32x4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
+    x ^= a ^ b ^ c ^ d;
+  }
+  for (; i < n16; i += stride) x ^= p[i];
+  const uint32_t v = x.x ^ x.y ^ x.z ^ x.w;
+  if (v == 0x9e3779b9u) sink[0] = v;
+}
+
+}  // namespace
+
+hipError_t launch_mfma_probe(int workgroups, int iters, float* sink, hipStream_t stream) {
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_read_probe(const void* buf, int64_t n16, int workgroups, uint32_t* sink,
+                             hipStream_t stream) {
+  hipLaunchKernelGGL(read_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream,
+                     static_cast<const u32x4*>(buf), n16, sink);
+  return hipGetLastError();
+}
+
+double mfma_probe_flop(int workgroups, int iters) {
+  return double(workgroups) * (kProbeThreads / 64) * double(iters) * kMfmaChains * (2.0 * 32 * 32 * 16);
+}
+
+}  // namespace ws

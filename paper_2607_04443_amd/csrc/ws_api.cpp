@@ -962,6 +962,27 @@ ws_status ws_cache_timing_read(ws_cache* c, ws_call_timing* out, int32_t max, in
   return WS_OK;
 }
 
+ws_status ws_probe_mfma(int32_t workgroups, int32_t iters, float* sink, double* flop,
+                        void* hip_stream) {
+  if (!sink || !flop) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (workgroups < 1 || workgroups > 65536 || iters < 1 || iters > (1 << 24))
+    return fail(WS_ERR_INVALID_ARG, "workgroups must be in [1, 65536] and iters in [1, 2^24]");
+  *flop = ws::mfma_probe_flop(workgroups, iters);
+  WS_HIP(ws::launch_mfma_probe(workgroups, iters, sink, static_cast<hipStream_t>(hip_stream)));
+  return WS_OK;
+}
+
+ws_status ws_probe_read(const void* buf, int64_t bytes, int32_t workgroups, uint32_t* sink,
+                        void* hip_stream) {
+  if (!buf || !sink) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (bytes <= 0 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(buf) % 16 != 0)
+    return fail(WS_ERR_INVALID_ARG, "buf must be 16-byte aligned and bytes a positive multiple of 16");
+  if (workgroups < 1 || workgroups > 65536)
+    return fail(WS_ERR_INVALID_ARG, "workgroups must be in [1, 65536]");
+  WS_HIP(ws::launch_read_probe(buf, bytes / 16, workgroups, sink, static_cast<hipStream_t>(hip_stream)));
+  return WS_OK;
+}
+
 const char* ws_last_error(void) { return g_last_error.c_str(); }
 
 }  // extern "C"

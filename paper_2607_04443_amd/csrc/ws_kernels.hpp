@@ -172,6 +172,11 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 // The merges of a video call (n_groups > 0) and an audio call (num_heads > 0)
 // in one launch; either may be absent (zero-initialised).
 hipError_t launch_step_combine(const CombineArgs& video, const CombineArgs& audio, hipStream_t stream);
+// Calibration probes (peaks.hip).
+hipError_t launch_mfma_probe(int workgroups, int iters, float* sink, hipStream_t stream);
+hipError_t launch_read_probe(const void* buf, int64_t n16, int workgroups, uint32_t* sink,
+                             hipStream_t stream);
+double mfma_probe_flop(int workgroups, int iters);
 
 constexpr int kVideoQTile = 256;
 constexpr int kMaxVideoSplits = 8;  // key-range splits of the video kernel

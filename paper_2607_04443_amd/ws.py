@@ -123,6 +123,8 @@ _SIGS = {
     "ws_cache_set_option": [_vp, _i32, _i32],
     "ws_cache_timing_enable": [_vp, _i32],
     "ws_cache_timing_read": [_vp, _P(ws_call_timing), _i32, _P(_i32)],
+    "ws_probe_mfma": [_i32, _i32, _vp, _P(ctypes.c_double), _vp],
+    "ws_probe_read": [_vp, _i64, _i32, _vp, _vp],
 }
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -246,6 +248,19 @@ def ws_cache_timing_read(cache, max_calls):
     n = _i32()
     _check(_lib.ws_cache_timing_read(cache, buf, max_calls, ctypes.byref(n)), "ws_cache_timing_read")
     return [buf[i] for i in range(n.value)]
+
+
+def ws_probe_mfma(workgroups, iters, sink, stream):
+    """Enqueues the bf16 MFMA calibration loop; returns its FLOP count.
+    sink: device address of a float; stream: HIP stream handle."""
+    flop = ctypes.c_double()
+    _check(_lib.ws_probe_mfma(workgroups, iters, sink, ctypes.byref(flop), stream), "ws_probe_mfma")
+    return flop.value
+
+
+def ws_probe_read(buf, nbytes, workgroups, sink, stream):
+    """Enqueues one streaming read of nbytes at device address buf."""
+    _check(_lib.ws_probe_read(buf, nbytes, workgroups, sink, stream), "ws_probe_read")
 
 
 def ws_last_error() -> str:
