@@ -542,3 +542,55 @@ def test_step_attention_equals_separate_calls(ws, name, splits):
         assert_gates(bf16_f64(from_dev(step_a)), ref, label=f"{name} step audio")
     finally:
         L.close()
+
+
+def test_bench_step_at_full_size(ws):
+    """The step as the benchmark issues it, at full size (H = 40; video: 920
+    queries over 8536 keys; audio: 4 queries over 8572 keys).  One
+    ws_step_append holds the current unit's video and audio K/V and the
+    preparation of both query sets, then one ws_step_attention runs on the
+    prepared queries.  Video heads 0, 13, 26 and 39 and every audio head are
+    checked against the oracle.  A second step with the same inputs (an
+    in-place rewrite) must be bit-identical."""
+    import torch
+    wl = synth.make_workload("audio_c256")
+    L = Loaded(ws, wl, step_segments=False)
+    try:
+        st = wl.steps[0]
+        items = []
+        for seg in st.segments:
+            k, v, p = to_dev(seg.k), to_dev(seg.v), dev_i32(seg.positions)
+            L._keep += [k, v, p]
+            items.append(dict(unit=seg.unit, kind=seg.kind, k=k, v=v, mode=ws.WS_APPEND_NORM_ROPE,
+                              positions=p, gamma=L.gk, eps=wl.eps))
+            L.ocache.append(seg.unit, seg.kind, seg.k, seg.v, oracle.MODE_NORM_ROPE, seg.positions,
+                            wl.gamma_k.astype(np.float64), wl.eps)
+        assert {seg.kind for seg in st.segments} == {synth.KIND_VIDEO, synth.KIND_AUDIO}
+        qv, qa = to_dev(st.q_video), to_dev(st.q_audio)
+        pv, pa = dev_i32(st.q_video_pos), dev_i32(st.q_audio_pos)
+        L._keep += [qv, qa, pv, pa]
+        vmask = ws.mask_spec(wl.current_unit, -(2 ** 31), VIDEO_KINDS)
+        amask = ws.mask_spec(wl.current_unit, -(2 ** 31), ALL_KINDS)
+        outs = []
+        for rep in range(2):
+            print(f"bench step at full size: repetition {rep}", flush=True)
+            qv2, qa2 = torch.full_like(qv, float("nan")), torch.full_like(qa, float("nan"))
+            L.cache.step_append(items, [
+                dict(q=qv, q_out=qv2, mode=ws.WS_APPEND_NORM_ROPE, positions=pv, gamma=L.gq,
+                     eps=wl.eps, scale=0.0),
+                dict(q=qa, q_out=qa2, mode=ws.WS_APPEND_NORM_ROPE, positions=pa, gamma=L.gq,
+                     eps=wl.eps, scale=0.0)])
+            ov, oa = torch.full_like(qv, float("nan")), torch.full_like(qa, float("nan"))
+            L.cache.step_attention(dict(q=qv2, out=ov, mask=vmask, mode=ws.WS_QUERY_PREPARED),
+                                   dict(q=qa2, out=oa, mask=amask, mode=ws.WS_QUERY_PREPARED))
+            torch.cuda.synchronize()
+            outs.append((from_dev(ov), from_dev(oa)))
+        np.testing.assert_array_equal(outs[0][0], outs[1][0])
+        np.testing.assert_array_equal(outs[0][1], outs[1][1])
+        heads = [0, 13, 26, 39]
+        refv = L.oracle(st.q_video, st.q_video_pos, wl.current_unit, VIDEO_KINDS, heads=heads)
+        print("video", assert_gates(bf16_f64(outs[0][0])[:, heads], refv, label="bench step video"))
+        refa = L.oracle(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+        print("audio", assert_gates(bf16_f64(outs[0][1]), refa, label="bench step audio"))
+    finally:
+        L.close()
