@@ -220,13 +220,13 @@ def pmc_summary(fetch_dir, write_dir):
     lines = ["# HBM traffic: unit_attn_kernel and audio_attn_kernel, v0.2 unit with an 8-unit history",
              "",
              "Counters per dispatch (median over the driver's dispatches of each kernel), from two",
-             "runs of the same committed program, one counter each (from the repo root on the GPU box):",
+             "runs of the same committed program, one counter each (from the repository root):",
              "",
-             "    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc FETCH_SIZE -d <repo>/gpurun_out/pmc_fetch "
+             f"    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc FETCH_SIZE -d <repo>/{fetch_dir} "
              "-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver",
-             "    cd /tmp && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -d <repo>/gpurun_out/pmc_write "
+             f"    cd /tmp && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -d <repo>/{write_dir} "
              "-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver",
-             "    python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write",
+             f"    python3 bench.py --pmc-summary {fetch_dir} {write_dir}",
              "",
              f"Calibration: the {COPY_BYTES >> 20} MiB device copy (__amd_rocclr_copyBuffer) reads "
              f"FETCH_SIZE {f_copy:.0f} KiB and WRITE_SIZE {w_copy:.0f} KiB, i.e. "
