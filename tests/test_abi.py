@@ -43,6 +43,29 @@ def test_library_exports_every_declared_symbol():
     assert exported == declared_functions()
 
 
+def test_probe_arguments_rejected_before_any_device_call():
+    """The calibration probes validate on the host: bad sizes and alignments
+    return WS_ERR_INVALID_ARG (1) without touching a device (the fake,
+    non-null addresses below are never dereferenced)."""
+    b = _ensure_built()
+    lib = ctypes.CDLL(b.LIB_PATH)
+    lib.ws_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                  ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    lib.ws_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                  ctypes.c_void_p]
+    lib.ws_last_error.restype = ctypes.c_char_p
+    flop = ctypes.c_double()
+    fake = ctypes.c_void_p(4096)
+    for wg, it in [(0, 1), (65537, 1), (1, 0), (1, (1 << 24) + 1)]:
+        assert lib.ws_probe_mfma(wg, it, fake, ctypes.byref(flop), None) == 1, (wg, it)
+    assert lib.ws_probe_mfma(1, 1, None, ctypes.byref(flop), None) == 1
+    assert lib.ws_probe_read(fake, 0, 1, fake, None) == 1
+    assert lib.ws_probe_read(fake, 24, 1, fake, None) == 1          # not a multiple of 16
+    assert lib.ws_probe_read(ctypes.c_void_p(4104), 32, 1, fake, None) == 1  # misaligned
+    assert lib.ws_probe_read(fake, 32, 0, fake, None) == 1
+    assert b"workgroups" in lib.ws_last_error()
+
+
 def test_last_error_callable_without_device():
     b = _ensure_built()
     lib = ctypes.CDLL(b.LIB_PATH)

@@ -276,3 +276,20 @@ def test_append_many_failures_take_nothing(ws):
         assert c.check() == 0
     finally:
         c.close()
+
+
+def test_calibration_probes(ws):
+    """ws_probe_mfma reports the FLOP count of its launch (workgroups x 4 waves
+    x iters x 4 MFMAs x 32768) and finishes; ws_probe_read finishes on a small
+    zero buffer; neither writes its sink for these inputs."""
+    import torch
+    sink = torch.full((4,), 7.0, dtype=torch.float32, device="cuda")
+    buf = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    h = torch.cuda.current_stream().cuda_stream
+    flop = ws.ws_probe_mfma(8, 16, sink.data_ptr(), h)
+    assert flop == 8 * 4 * 16 * 4 * 2.0 * 32 * 32 * 16
+    ws.ws_probe_read(buf.data_ptr(), buf.numel(), 64, sink.data_ptr() + 4, h)
+    torch.cuda.synchronize()
+    assert (sink.cpu() == 7.0).all()
+    with pytest.raises(ws.WsError):
+        ws.ws_probe_read(buf.data_ptr() + 8, 64, 1, sink.data_ptr(), h)
