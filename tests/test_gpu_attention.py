@@ -372,6 +372,33 @@ def test_video_tight_bound_shift(ws):
         L.close()
 
 
+@pytest.mark.parametrize("splits", [1, 7])
+@pytest.mark.parametrize("n_q", [17, 64])
+def test_audio_query_tiles(ws, splits, n_q):
+    """The audio path with more than one 16-query tile: a ragged count (17:
+    two tiles, the second holding one query) and the largest count a call
+    takes (64: four full tiles), against the oracle."""
+    wl = synth.make_workload(TINY)
+    L = Loaded(ws, wl)
+    try:
+        L.cache.set_option(ws.WS_OPT_AUDIO_KV_SPLITS, splits)
+        st = wl.steps[0]
+        reps = -(-n_q // st.q_video.shape[0])
+        q = np.concatenate([st.q_video] * reps)[:n_q]
+        pos = np.concatenate([st.q_video_pos] * reps)[:n_q]
+        print(f"audio query tiles: splits={splits} n_q={n_q}", flush=True)
+        got = L.run("audio", q, pos, wl.current_unit, ALL_KINDS)
+        ref = L.oracle(q, pos, wl.current_unit, ALL_KINDS)
+        assert_gates(got, ref, label=f"audio n_q={n_q} splits={splits}")
+        if n_q == 64:  # one query more than a call takes: rejected before any launch
+            q65 = np.concatenate([q, q[:1]])
+            pos65 = np.concatenate([pos, pos[:1]])
+            with pytest.raises(ws.WsError):
+                L.run("audio", q65, pos65, wl.current_unit, ALL_KINDS)
+    finally:
+        L.close()
+
+
 def test_launch_timing_ring(ws):
     """ws_cache_timing_*: one record per attention call, oldest first, with
     the attention kernel and the merge timed separately; disabled -> error."""
