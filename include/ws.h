@@ -5,8 +5,9 @@
  * The library owns one paged K/V cache per ws_cache handle and runs the
  * performer's per-denoising-step attention of the next streaming unit over it
  * (Wan-Streamer v0.2, arXiv 2607.04443):
- *   - each performer rank writes incoming K/V into a pre-allocated local cache
- *     (Abstract; Sec. 3, "Performer" item and the unit-k schedule paragraph);
+ *   - a per-rank K/V cache, allocated up front, receives the thinker's slices
+ *     and the generated units' K/V (Abstract; Sec. 3, the performer item and
+ *     the unit-k schedule paragraph);
  *   - generated latents are committed into history after every unit
  *     (Sec. 2.1); the full-history cache is updated per unit (Sec. 3);
  *   - attention is block-causal on one timeline, the block being the 160 ms
@@ -306,6 +307,13 @@ WS_API ws_status ws_cache_export(ws_cache* cache, int32_t unit, ws_kind kind, vo
 
 /* Token count of a segment (WS_ERR_UNKNOWN_UNIT if absent). */
 WS_API ws_status ws_segment_tokens(ws_cache* cache, int32_t unit, ws_kind kind, int32_t* n_tokens);
+
+/* Debug: the pool page ids of segment (unit, kind) in token order (page i
+ * holds tokens 64 i .. 64 i + 63).  Writes min(count, max) ids to pages (host
+ * int32 array owned by the caller; may be NULL when max is 0) and the
+ * segment's page count to *n_pages.  Host-only; WS_ERR_UNKNOWN_UNIT if absent. */
+WS_API ws_status ws_segment_pages(ws_cache* cache, int32_t unit, ws_kind kind, int32_t* pages,
+                                  int32_t max, int32_t* n_pages);
 
 /* Page-pool occupancy.  Host-only. */
 WS_API ws_status ws_cache_info(ws_cache* cache, ws_cache_stats* stats);

@@ -744,11 +744,26 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
   const uint16_t* skn = stage_k<kNext>();
   pi = __builtin_amdgcn_readfirstlane(pi);
   const int ahead = c.pages[ahead3(pi, p_end)].x;
+  const int n_valid = c.pages[pi].y;
   pin_sgpr(ahead);
+  pin_sgpr(n_valid);
   __syncthreads();
   stage_dma(c, ahead, stage_k<(kCur + 3) % kStages>(), stage_v<(kCur + 3) % kStages>());
   __builtin_amdgcn_sched_barrier(0);
   const int half = c.half, l32 = c.l32;
+  // Page tail (only a segment's last page is partly filled): logits of slots
+  // at or past n_valid become -inf before their exponentials, so they weigh
+  // exactly 0.  Register r of lane half h holds key 16 (r / 8) + 8 h + r % 8
+  // (+32 in tile 1).  A correction subtracted from the row sum afterwards
+  // would cancel catastrophically for rows whose logits all sit far below
+  // the shift.
+  const bool tail = n_valid < kPageTokens;
+  auto mask_tail = [&](f32x16& sc, int key0) {
+    const int lim = n_valid - key0 - 8 * half;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (16 * (r >> 3) + (r & 7) >= lim) sc[r] = kNegInf;
+  };
   auto kread_at = [&](const uint16_t* k, int n) {  // S k-step n % 8 of tile n / 8
     const int row = n < 8 ? l32 : 32 + l32;
     return as_bf16x8(*reinterpret_cast<const u32x4*>(k + row * kHeadDim + 8 * ((2 * (n & 7) + half) ^ (l32 & 15))));
@@ -810,6 +825,7 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
         s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
       } else if (o < 16) {
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 8], o == 8 ? s_init : s1, 0, 0, 0);
+        if (o == 8 && tail) mask_tail(s0, 0);
         exp_one(s0, o - 8, p0, (o - 8) >> 1);
       } else if (o < 20) {
         st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p0), st.o[o - 16], 0, 0, 0);
@@ -840,6 +856,7 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 12], o == 12 ? s_init : s1, 0, 0, 0);
       } else if (o < 20) {
         st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp3), st.o[o - 16], 0, 0, 0);
+        if (o == 16 && tail) mask_tail(s0, 0);
         exp_one(s0, o - 16, p0, (o - 16) >> 1);
       } else if (o < 24) {
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[4 + o - 20], s1, 0, 0, 0);
@@ -855,6 +872,7 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
     __builtin_amdgcn_sched_barrier(0);
   }
   st.l_run += l;
+  if (tail) mask_tail(s1, 32);
   ps.s1 = s1;
   wait_dma_all_but_last_page();
 }
@@ -932,11 +950,11 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   int3 qpos = make_int3(0, 0, 0);
   if (norm_rope && q_ok) qpos = make_int3(a.positions[3 * q], a.positions[3 * q + 1], a.positions[3 * q + 2]);
   // the segment's page-list entries (two per lane in the first pass)
-  int2 pgl[2];
+  int pgl[2];
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int pi = p_begin + lane + 64 * k;
-    pgl[k] = pi < p_end ? make_int2(c.pages[pi].x, c.pages[pi].y) : make_int2(-1, kPageTokens);
+    pgl[k] = pi < p_end ? c.pages[pi].x : -1;
   }
   u32x4 qraw[8];
   const uint16_t* qp = a.q + q * a.q_tok_stride + head * a.q_head_stride + 8 * half;
@@ -959,21 +977,13 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
     stage_dma(c, pg_first[1], g_k1, g_v1);
     stage_dma(c, pg_first[2], g_k2, g_v2);
   }
-  // key norms of the segment's pages, and the count of their empty tail slots
+  // key norms of the segment's pages
   float kn2 = 0.f;
-  int n_empty = 0;
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    if (pgl[k].x >= 0) {
-      kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pgl[k].x) * a.num_heads + head]);
-      n_empty += kPageTokens - pgl[k].y;
-    }
-  }
-  for (int pi = p_begin + lane + 128; pi < p_end; pi += 64) {  // segments longer than 128 pages
-    const int2 pg = make_int2(c.pages[pi].x, c.pages[pi].y);
-    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pg.x) * a.num_heads + head]);
-    n_empty += kPageTokens - pg.y;
-  }
+  for (int k = 0; k < 2; ++k)
+    if (pgl[k] >= 0) kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pgl[k]) * a.num_heads + head]);
+  for (int pi = p_begin + lane + 128; pi < p_end; pi += 64)  // segments longer than 128 pages
+    kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(c.pages[pi].x) * a.num_heads + head]);
 
   // ---- Q prologue: lane holds Q''[q][16s + 8h + j], s = 0..7, j = 0..7 ----
   if (norm_rope) {
@@ -1028,10 +1038,7 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   // maximum is raised lazily: only when a 32-key tile exceeds it by more than
   // kLazyTau (p then stays below 2^kLazyTau), which makes the O rescale rare.
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    kn2 = fmaxf(kn2, __shfl_xor(kn2, o));
-    n_empty += __shfl_xor(n_empty, o);
-  }
+  for (int o = 1; o < 64; o <<= 1) kn2 = fmaxf(kn2, __shfl_xor(kn2, o));
   float qn2 = 0.f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
@@ -1042,7 +1049,6 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   qn2 += __shfl_xor(qn2, 32);
   const float bound = sqrtf(qn2 * kn2);
   const bool fixed_shift = a.fixed_shift != 0 && __all(bound <= kShiftBoundMax);
-  n_empty = __builtin_amdgcn_readfirstlane(n_empty);  // uniform after the reduction
 
   // ---- main loop over this segment's pages ----
   VideoState st;
@@ -1070,13 +1076,6 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
         if (pi + 4 < p_end) video_iter<0, false>(c, st, ps, s_init, pi + 4, p_end);
       }
       video_flush(c, st, ps, (p_end - 1 - p_begin) % kStages);
-      // Tail slots past a page's valid tokens are not masked: their stored
-      // keys and values are zero, so each logit is exactly -m_run (exp2
-      // argument) and adds nothing to O, but its weight, rounded to bf16 as
-      // the MFMAs see it, went into the row sum.  Take those weights out
-      // (split between the two lane halves that share a row).
-      const float p_empty = bf16_lo(pack_bf16(fast_exp2(-st.m_run), 0.f));
-      st.l_run -= 0.5f * static_cast<float>(n_empty) * p_empty;
     }
   } else if (c.active) {
     for (int pi = p_begin; pi < p_end; pi += 5) {

@@ -79,6 +79,7 @@ struct ws_cache {
   int2* arena_host = nullptr;  // pinned
   size_t arena_cap = 0;
   size_t arena_used = 0;
+  uint64_t arena_wraps = 0;  // times the arena started over (every cached list dropped)
   ListCacheEntry lists[4];
   int list_next = 0;
   float* part_o = nullptr;    // video key-range partials
@@ -143,6 +144,7 @@ ws_status upload_list(ws_cache* c, const std::vector<ws::PageRef>& list, hipStre
   if (c->arena_used + n > c->arena_cap) {
     WS_HIP(hipDeviceSynchronize());
     c->arena_used = 0;
+    ++c->arena_wraps;
     for (auto& e : c->lists) e.valid = false;
   }
   const size_t off = c->arena_used;
@@ -813,16 +815,26 @@ ws_status ws_step_attention(ws_cache* c, const ws_attn_call* video, const ws_att
   if (!c || !video || !audio) return fail(WS_ERR_INVALID_ARG, "NULL argument");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   AttnPlan pv, pa;
-  if (ws_status st = plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, video->n_q,
-                                    &video->desc, c, &video->mask, video->out, video->out_tok_stride,
-                                    video->out_head_stride, stream, &pv);
-      st != WS_OK)
-    return st;
+  auto plan_video = [&]() {
+    return plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, video->n_q,
+                          &video->desc, c, &video->mask, video->out, video->out_tok_stride,
+                          video->out_head_stride, stream, &pv);
+  };
+  if (ws_status st = plan_video(); st != WS_OK) return st;
+  const uint64_t wraps = c->arena_wraps;
   if (ws_status st = plan_attention(true, audio->q, audio->q_tok_stride, audio->q_head_stride, audio->n_q,
                                     &audio->desc, c, &audio->mask, audio->out, audio->out_tok_stride,
                                     audio->out_head_stride, stream, &pa);
       st != WS_OK)
     return st;
+  // A page list uploaded by the audio plan that started the arena over may
+  // sit where the video plan's list was: plan the video call again (its list
+  // then goes in after the audio one; the arena holds at least 16 lists of
+  // the longest possible length, so it cannot start over a second time).
+  if (c->arena_wraps != wraps) {
+    if (ws_status st = plan_video(); st != WS_OK) return st;
+    if (c->arena_wraps != wraps + 1) return fail(WS_ERR_SHAPE, "page-list arena too small for one step");
+  }
   // video kernel, audio kernel, then one launch merging both
   int sv = -1, sa = -1;
   if (ws_status st = timing_begin(c, pv, stream, &sv); st != WS_OK) return st;
@@ -878,6 +890,18 @@ ws_status ws_segment_tokens(ws_cache* c, int32_t unit, ws_kind kind, int32_t* n_
   const ws::Segment* s = c->pt.find(unit, kind);
   if (!s) return fail(WS_ERR_UNKNOWN_UNIT, "no segment for unit %d kind %d", unit, static_cast<int>(kind));
   *n_tokens = s->n_tokens;
+  return WS_OK;
+}
+
+ws_status ws_segment_pages(ws_cache* c, int32_t unit, ws_kind kind, int32_t* pages, int32_t max,
+                           int32_t* n_pages) {
+  if (!c || !n_pages || max < 0 || (max > 0 && !pages)) return fail(WS_ERR_INVALID_ARG, "bad argument");
+  if (ws_status st = check_kind(kind); st != WS_OK) return st;
+  const ws::Segment* s = c->pt.find(unit, kind);
+  if (!s) return fail(WS_ERR_UNKNOWN_UNIT, "no segment for unit %d kind %d", unit, static_cast<int>(kind));
+  const int32_t n = static_cast<int32_t>(s->pages.size());
+  for (int32_t i = 0; i < std::min(n, max); ++i) pages[i] = s->pages[static_cast<size_t>(i)];
+  *n_pages = n;
   return WS_OK;
 }
 

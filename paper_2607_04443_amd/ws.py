@@ -118,6 +118,7 @@ _SIGS = {
     "ws_step_attention": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_cache_export": [_vp, _i32, _i32, _vp, _vp],
     "ws_segment_tokens": [_vp, _i32, _i32, _P(_i32)],
+    "ws_segment_pages": [_vp, _i32, _i32, _P(_i32), _i32, _P(_i32)],
     "ws_cache_info": [_vp, _P(ws_cache_stats)],
     "ws_cache_check": [_vp, _P(_u32)],
     "ws_cache_set_option": [_vp, _i32, _i32],
@@ -221,6 +222,14 @@ def ws_segment_tokens(cache, unit, kind) -> int:
     n = _i32()
     _check(_lib.ws_segment_tokens(cache, unit, kind, ctypes.byref(n)), "ws_segment_tokens")
     return n.value
+
+
+def ws_segment_pages(cache, unit, kind) -> list:
+    n = _i32()
+    _check(_lib.ws_segment_pages(cache, unit, kind, None, 0, ctypes.byref(n)), "ws_segment_pages")
+    buf = (_i32 * max(n.value, 1))()
+    _check(_lib.ws_segment_pages(cache, unit, kind, buf, n.value, ctypes.byref(n)), "ws_segment_pages")
+    return [buf[i] for i in range(n.value)]
 
 
 def ws_cache_info(cache) -> ws_cache_stats:
@@ -427,6 +436,10 @@ class Cache:
         v = np.empty_like(k)
         ws_cache_export(self.handle, unit, kind, k.ctypes.data, v.ctypes.data)
         return k, v
+
+    def pages(self, unit, kind):
+        """Pool page ids of a segment, in token order."""
+        return ws_segment_pages(self.handle, unit, kind)
 
     def info(self):
         return ws_cache_info(self.handle)
