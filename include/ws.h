@@ -299,6 +299,24 @@ typedef struct ws_attn_call {
 WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, const ws_attn_call* audio,
                                    void* hip_stream);
 
+/* ws_step_attention for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and the same outputs, bit for bit, but the two
+ * calls' split-KV partials go to a static workspace in the library's code
+ * object (32 MiB per device, kept until the process ends) instead of the
+ * cache's workspaces.  The call itself allocates nothing.
+ * Limit: the partials of both calls must fit the 32 MiB: video (ranges per
+ * head) x H x n_q rows of 260 bytes, audio (key ranges) x H x n_q rows of
+ * 516 bytes, each region rounded up to 256 bytes; a larger step returns
+ * WS_ERR_SHAPE before anything is enqueued.  (The v0.2 unit at 640x368 with
+ * an 8-unit window needs about 30 MB.)  Every call on a device shares that
+ * device's workspace: calls that overlap in time on one device (different
+ * streams, or different threads) race and must be ordered by the caller.
+ * Nothing in it has to start at zero: each call writes every partial row it
+ * reads. */
+WS_API ws_status ws_step_attention_noalloc(ws_cache* cache, const ws_attn_call* video,
+                                           const ws_attn_call* audio, void* hip_stream);
+
 /* Debug read-back of one segment in logical order: k_host and v_host receive
  * bf16 [n_tokens][H][128] (contiguous host buffers owned by the caller).
  * Waits for the device.  k_host or v_host may be NULL to skip it. */

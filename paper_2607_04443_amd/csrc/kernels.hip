@@ -15,6 +15,7 @@
 // (Wan-Streamer v0.2, Sec. 3); block-causal visibility (Fig. 1 caption) is
 // resolved on the host into the list of visible pages.
 #include <cstddef>
+#include <mutex>
 #include <type_traits>
 
 #include "ws_kernels.hpp"
@@ -1598,6 +1599,30 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const CombineArgs v, 
 }
 
 }  // namespace
+
+// The no-allocation entry point's split-KV workspace.  Host code never
+// passes this name to a kernel or a copy (in host code it is only a stand-in
+// for the symbol): it uses the device address static_scratch() looks up.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+hipError_t static_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
   dim3 grid(a.n_blocks, a.num_heads);

@@ -92,6 +92,7 @@ struct ws_cache {
   int32_t opt_running_max = 0;
   float* knorm2 = nullptr;  // [max_pages][H] squared key-norm maxima
   uint16_t* zeros = nullptr;  // 1 KB of zeros (direct-load source of empty blocks)
+  void* static_ws = nullptr;  // device address of the static split-KV workspace on this device
   std::vector<ws::PageRef> scratch_list;
   TimingRing timing;
 
@@ -292,6 +293,8 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
   if ((e = hipMalloc(&c->zeros, 1024)) != hipSuccess) return bail(hip_fail(e, "hipMalloc(zeros)"));
   if ((e = hipMemset(c->zeros, 0, 1024)) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
   if (ws_status st = fill_rope(c); st != WS_OK) return bail(st);
+  if ((e = ws::static_scratch(&c->static_ws)) != hipSuccess)
+    return bail(hip_fail(e, "hipGetSymbolAddress(static split-KV workspace)"));
   if ((e = hipMalloc(&c->flags_dev, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMalloc"));
   if ((e = hipMemset(c->flags_dev, 0, sizeof(uint32_t))) != hipSuccess) return bail(hip_fail(e, "hipMemset"));
   c->arena_cap = std::max<size_t>(65536, 16 * static_cast<size_t>(cfg->max_pages));
@@ -373,6 +376,7 @@ struct AttnPlan {
   bool merge = false;
   ws::CombineArgs cb{};
   int splits = 1;  // audio: key ranges; video: workgroup groups
+  int64_t part_rows = 0;  // (range, head, query) partial rows the kernel may write
 };
 
 ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
@@ -452,6 +456,7 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
     if (cap < splits) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
     a.n_splits = splits;
     a.pages_per_split = pps;
+    plan->part_rows = static_cast<int64_t>(splits) * H * n_q;
   } else {
     const int groups = choose_video_groups(c, H, a.n_qtiles, n_pages);
     // ranges per head: exactly the forced split count, else at most
@@ -460,6 +465,7 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
     const int64_t max_ranges = c->opt_video_splits > 0 ? c->opt_video_splits
                                : std::max<int64_t>(2, (groups + H - 1) / H + 1);
     if (cap < max_ranges) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
+    plan->part_rows = max_ranges * H * n_q;
     a.n_groups = groups;
     // forced splits keep equal ranges per head
     a.seg_cost = c->opt_video_splits > 0 ? 0 : kVideoSegCostPages;
@@ -535,6 +541,85 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
     if (e != hipSuccess) return hip_fail(e, "combine launch");
   }
   return timing_mark(c, slot, 2, stream);
+}
+
+// Puts both calls' split-KV partials into the static workspace: video bf16
+// O rows, audio fp32 O rows, and their fp32 log-sum-exp, each region
+// 256-byte aligned.  Fails (before anything is enqueued) when they do not fit.
+ws_status use_static_workspace(ws_cache* c, AttnPlan& pv, AttnPlan& pa) {
+  if (!c->static_ws) return fail(WS_ERR_HIP, "static split-KV workspace unavailable");
+  uint8_t* base = static_cast<uint8_t*>(c->static_ws);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    uint8_t* p = base + off;
+    off += (bytes + 255) & ~size_t(255);
+    return p;
+  };
+  const size_t rv = static_cast<size_t>(pv.part_rows), ra = static_cast<size_t>(pa.part_rows);
+  float* vo = reinterpret_cast<float*>(take(rv * ws::kHeadDim * sizeof(uint16_t)));
+  float* vl = reinterpret_cast<float*>(take(rv * sizeof(float)));
+  float* ao = reinterpret_cast<float*>(take(ra * ws::kHeadDim * sizeof(float)));
+  float* al = reinterpret_cast<float*>(take(ra * sizeof(float)));
+  if (off > ws::kStaticScratchBytes)
+    return fail(WS_ERR_SHAPE,
+                "this step needs %zu bytes of split-KV workspace (%zu video and %zu audio partial rows); "
+                "the static workspace holds %zu",
+                off, rv, ra, ws::kStaticScratchBytes);
+  pv.a.part_o = vo;
+  pv.a.part_lse = vl;
+  pa.a.part_o = ao;
+  pa.a.part_lse = al;
+  pv.cb.part_o = vo;
+  pv.cb.part_lse = vl;
+  pa.cb.part_o = ao;
+  pa.cb.part_lse = al;
+  return WS_OK;
+}
+
+ws_status step_attention_impl(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio,
+                              void* hip_stream, bool static_workspace) {
+  if (!c || !video || !audio) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  AttnPlan pv, pa;
+  auto plan_video = [&]() {
+    return plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, video->n_q,
+                          &video->desc, c, &video->mask, video->out, video->out_tok_stride,
+                          video->out_head_stride, stream, &pv);
+  };
+  if (ws_status st = plan_video(); st != WS_OK) return st;
+  const uint64_t wraps = c->arena_wraps;
+  if (ws_status st = plan_attention(true, audio->q, audio->q_tok_stride, audio->q_head_stride, audio->n_q,
+                                    &audio->desc, c, &audio->mask, audio->out, audio->out_tok_stride,
+                                    audio->out_head_stride, stream, &pa);
+      st != WS_OK)
+    return st;
+  // A page list uploaded by the audio plan that started the arena over may
+  // sit where the video plan's list was: plan the video call again (its list
+  // then goes in after the audio one; the arena holds at least 16 lists of
+  // the longest possible length, so it cannot start over a second time).
+  if (c->arena_wraps != wraps) {
+    if (ws_status st = plan_video(); st != WS_OK) return st;
+    if (c->arena_wraps != wraps + 1) return fail(WS_ERR_SHAPE, "page-list arena too small for one step");
+  }
+  if (static_workspace)
+    if (ws_status st = use_static_workspace(c, pv, pa); st != WS_OK) return st;
+  // video kernel, audio kernel, then one launch merging both
+  int sv = -1, sa = -1;
+  if (ws_status st = timing_begin(c, pv, stream, &sv); st != WS_OK) return st;
+  hipError_t e = launch_plan_kernel(pv, stream);
+  if (e != hipSuccess) return hip_fail(e, "unit_attn launch");
+  if (ws_status st = timing_mark(c, sv, 1, stream); st != WS_OK) return st;
+  if (ws_status st = timing_mark(c, sv, 2, stream); st != WS_OK) return st;
+  if (ws_status st = timing_begin(c, pa, stream, &sa); st != WS_OK) return st;
+  e = launch_plan_kernel(pa, stream);
+  if (e != hipSuccess) return hip_fail(e, "audio_attn launch");
+  if (ws_status st = timing_mark(c, sa, 1, stream); st != WS_OK) return st;
+  if (pv.merge || pa.merge) {
+    ws::CombineArgs none{};
+    e = ws::launch_step_combine(pv.merge ? pv.cb : none, pa.merge ? pa.cb : none, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine launch");
+  }
+  return timing_mark(c, sa, 2, stream);
 }
 
 }  // namespace
@@ -812,46 +897,12 @@ ws_status ws_audio_attention(const void* q, int64_t q_tok_stride, int64_t q_head
 }
 
 ws_status ws_step_attention(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio, void* hip_stream) {
-  if (!c || !video || !audio) return fail(WS_ERR_INVALID_ARG, "NULL argument");
-  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  AttnPlan pv, pa;
-  auto plan_video = [&]() {
-    return plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, video->n_q,
-                          &video->desc, c, &video->mask, video->out, video->out_tok_stride,
-                          video->out_head_stride, stream, &pv);
-  };
-  if (ws_status st = plan_video(); st != WS_OK) return st;
-  const uint64_t wraps = c->arena_wraps;
-  if (ws_status st = plan_attention(true, audio->q, audio->q_tok_stride, audio->q_head_stride, audio->n_q,
-                                    &audio->desc, c, &audio->mask, audio->out, audio->out_tok_stride,
-                                    audio->out_head_stride, stream, &pa);
-      st != WS_OK)
-    return st;
-  // A page list uploaded by the audio plan that started the arena over may
-  // sit where the video plan's list was: plan the video call again (its list
-  // then goes in after the audio one; the arena holds at least 16 lists of
-  // the longest possible length, so it cannot start over a second time).
-  if (c->arena_wraps != wraps) {
-    if (ws_status st = plan_video(); st != WS_OK) return st;
-    if (c->arena_wraps != wraps + 1) return fail(WS_ERR_SHAPE, "page-list arena too small for one step");
-  }
-  // video kernel, audio kernel, then one launch merging both
-  int sv = -1, sa = -1;
-  if (ws_status st = timing_begin(c, pv, stream, &sv); st != WS_OK) return st;
-  hipError_t e = launch_plan_kernel(pv, stream);
-  if (e != hipSuccess) return hip_fail(e, "unit_attn launch");
-  if (ws_status st = timing_mark(c, sv, 1, stream); st != WS_OK) return st;
-  if (ws_status st = timing_mark(c, sv, 2, stream); st != WS_OK) return st;
-  if (ws_status st = timing_begin(c, pa, stream, &sa); st != WS_OK) return st;
-  e = launch_plan_kernel(pa, stream);
-  if (e != hipSuccess) return hip_fail(e, "audio_attn launch");
-  if (ws_status st = timing_mark(c, sa, 1, stream); st != WS_OK) return st;
-  if (pv.merge || pa.merge) {
-    ws::CombineArgs none{};
-    e = ws::launch_step_combine(pv.merge ? pv.cb : none, pa.merge ? pa.cb : none, stream);
-    if (e != hipSuccess) return hip_fail(e, "combine launch");
-  }
-  return timing_mark(c, sa, 2, stream);
+  return step_attention_impl(c, video, audio, hip_stream, false);
+}
+
+ws_status ws_step_attention_noalloc(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio,
+                                    void* hip_stream) {
+  return step_attention_impl(c, video, audio, hip_stream, true);
 }
 
 ws_status ws_cache_export(ws_cache* c, int32_t unit, ws_kind kind, void* k_host, void* v_host) {

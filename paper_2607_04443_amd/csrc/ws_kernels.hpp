@@ -10,7 +10,8 @@
 // Both tiles are arranged so that the 16-key x 32-d (K) and 16-d x 32-key
 // (V^T) operand blocks of one MFMA step cover whole 128-byte lines, and the
 // video kernel's direct-to-LDS loads keep a constant per-lane source offset.
-// Slots past a segment's last token hold zeros, so masked keys never carry
+// Slots past a segment's last token hold zeros (every append writes all 64
+// slots of its pages), so a masked key's zero weight never meets stale data.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -177,6 +178,13 @@ hipError_t launch_mfma_probe(int workgroups, int iters, float* sink, hipStream_t
 hipError_t launch_read_probe(const void* buf, int64_t n16, int workgroups, uint32_t* sink,
                              hipStream_t stream);
 double mfma_probe_flop(int workgroups, int iters);
+
+// Split-KV workspace of the no-allocation step entry point: a static device
+// array of this many bytes in the library's code object (one per device).
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+// Device address of that array on the current device, looked up once per
+// device (hipGetSymbolAddress) and kept.
+hipError_t static_scratch(void** ptr);
 
 constexpr int kVideoQTile = 256;
 constexpr int kMaxVideoSplits = 8;  // key-range splits of the video kernel

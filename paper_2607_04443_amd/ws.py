@@ -116,6 +116,7 @@ _SIGS = {
     "ws_audio_attention": [_vp, _i64, _i64, _i32, _P(ws_query_desc), _vp, _P(ws_mask_spec), _vp,
                            _i64, _i64, _vp],
     "ws_step_attention": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
+    "ws_step_attention_noalloc": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_cache_export": [_vp, _i32, _i32, _vp, _vp],
     "ws_segment_tokens": [_vp, _i32, _i32, _P(_i32)],
     "ws_segment_pages": [_vp, _i32, _i32, _P(_i32), _i32, _P(_i32)],
@@ -212,6 +213,11 @@ def ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, 
 def ws_step_attention(cache, video: ws_attn_call, audio: ws_attn_call, stream):
     _check(_lib.ws_step_attention(cache, ctypes.byref(video), ctypes.byref(audio), stream),
            "ws_step_attention")
+
+
+def ws_step_attention_noalloc(cache, video: ws_attn_call, audio: ws_attn_call, stream):
+    _check(_lib.ws_step_attention_noalloc(cache, ctypes.byref(video), ctypes.byref(audio), stream),
+           "ws_step_attention_noalloc")
 
 
 def ws_cache_export(cache, unit, kind, k_host, v_host):
@@ -408,6 +414,12 @@ class Cache:
         audio_attention (q, out, mask, mode, positions, gamma, eps, scale)."""
         ws_step_attention(self.handle, self._call(**video), self._call(**audio),
                           _stream_handle(stream))
+
+    def step_attention_noalloc(self, video, audio, stream=None):
+        """step_attention with the split-KV partials in the library's static
+        workspace (no device allocation by the call)."""
+        ws_step_attention_noalloc(self.handle, self._call(**video), self._call(**audio),
+                                  _stream_handle(stream))
 
     def unit_attention(self, q, out, mask, mode=WS_APPEND_NORM_ROPE, positions=None, gamma=None,
                        eps=1e-6, scale=0.0, stream=None):
