@@ -32,6 +32,7 @@ calls' stream around the kernel itself.
 """
 import argparse
 import json
+import subprocess
 import os
 import sys
 import time
@@ -66,6 +67,9 @@ def parse():
     ap.add_argument("--pmc-driver", action="store_true",
                     help="run one step, then the video and audio attention and a 256 MiB device "
                          "copy three times each, untimed (the program rocprofv3 --pmc runs)")
+    ap.add_argument("--cpu-v01-point", action="store_true",
+                    help="time the fp64 oracle on the whole v0.1-scale workload (CPU only) and print "
+                         "one JSON line")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc -f csv runs of --pmc-driver (FETCH_SIZE, "
                          "WRITE_SIZE) as markdown")
@@ -74,6 +78,40 @@ def parse():
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_v01_point():
+    """The fp64 oracle on the whole 192x336-scale workload (12 heads, 252
+    queries over 64 + 3 x 252 = 820 keys, with its Q/K RMS-norm and rotary),
+    run in this process; called in a child process with one OpenMP thread."""
+    import numpy as np
+    import oracle
+    from paper_2607_04443_amd import synth
+    wl = synth.make_workload("v01")
+    oc = oracle.OracleCache(num_heads=wl.config.heads)
+    for seg in wl.cached + wl.steps[0].segments:
+        oc.append(seg.unit, seg.kind, seg.k, seg.v, seg.mode, seg.positions,
+                  wl.gamma_k.astype(np.float64), wl.eps)
+    st = wl.steps[0]
+    t0 = time.perf_counter()
+    oracle.unit_attention(oc, st.q_video, wl.current_unit, positions=st.q_video_pos,
+                          gamma=wl.gamma_q.astype(np.float64), eps=wl.eps)
+    dt = time.perf_counter() - t0
+    cfg = wl.config
+    lk = cfg.video_keys
+    flop = 4.0 * cfg.heads * cfg.unit_tokens * lk * D
+    return {"threads": oracle.num_threads(), "seconds": dt, "tflops": flop / dt / 1e12,
+            "workload": f"v0.1 scale: {cfg.heads} heads, {cfg.unit_tokens} queries x {lk} keys, fp64"}
 
 
 def cpu_baseline(budget_s=12.0):
@@ -99,10 +137,19 @@ def cpu_baseline(budget_s=12.0):
         dt += time.perf_counter() - t0
         heads += 1
     flop = video_flop(LU, lk) / H * heads
+    single = None
+    try:
+        env = dict(os.environ, OMP_NUM_THREADS="1")
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-v01-point"], env=env,
+                           capture_output=True, text=True, timeout=300)
+        single = json.loads(r.stdout.strip().splitlines()[-1]) if r.returncode == 0 else None
+    except (subprocess.SubprocessError, ValueError, IndexError):
+        single = None
     return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{heads} of {H} heads of the video attention ({LU} queries x {lk} keys, "
-                      f"fp64, with those heads' Q/K RMS-norm and rotary): {dt:.1f} s"}
+                      f"fp64, with those heads' Q/K RMS-norm and rotary): {dt:.1f} s",
+            "single_thread_v01": single}
 
 
 def long_history(args, ws, sets, gamma, eps, stream, dev):
@@ -153,6 +200,53 @@ def long_history(args, ws, sets, gamma, eps, stream, dev):
     lk = COND + (hist_l + 1) * LU
     return {"keys": lk, "us_4_steps": med, "us_per_step": med / 4,
             "tflops": 4 * video_flop(LU, lk) / (med * 1e-6) / 1e12}
+
+
+def cold_audio(args, ws, sets, vpos, apos, gamma, eps, stream, dev, cond):
+    """ws_audio_attention with cold caches: a cache of `cond` conditioning
+    tokens, 8 committed history units and the current unit (920 video + 4
+    audio tokens each), the 4 prepared audio queries over all of it.  Between
+    repetitions a 1 GiB buffer is read (a reduction), which evicts the 256 MB
+    cache with clean lines, so the timed call neither hits that cache nor pays
+    for writing back a dirty scrub; events around the audio call only."""
+    import numpy as np
+    import torch
+    from paper_2607_04443_amd import synth
+    cache = ws.Cache(H, cond // 64 + 2 + (HIST + 1) * 16, max_q_tokens=1024)
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 3))
+    ck = torch.from_numpy(synth.normal_bf16(rng, (cond, H, D)).view(np.int16)).view(torch.bfloat16).to(dev)
+    cv = torch.from_numpy(synth.normal_bf16(rng, (cond, H, D)).view(np.int16)).view(torch.bfloat16).to(dev)
+    cache.append(0, ws.WS_KIND_COND, ck, cv, ws.WS_APPEND_RAW)
+    for u in range(HIST + 1):
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma, eps)
+        if u < HIST:
+            cache.commit(u)
+    q_a = torch.empty((AUDIO, H, D), dtype=torch.bfloat16, device=dev)
+    out_a = torch.empty((AUDIO, H, D), dtype=torch.bfloat16, device=dev)
+    cache.step_append([], [dict(q=sets[0]["qa"], q_out=q_a, positions=apos[HIST], gamma=gamma, eps=eps)])
+    amask = ws.mask_spec(HIST, 0, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
+    scrub = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    scrub_sum = torch.empty((), dtype=torch.float32, device=dev)
+    times = []
+    for _ in range(args.cold_audio_reps):
+        torch.sum(scrub, dim=0, out=scrub_sum)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b) * 1e3)
+    cache.close()
+    del scrub
+    times.sort()
+    med = times[len(times) // 2]
+    keys = cond + (HIST + 1) * (LU + AUDIO)
+    nbytes = 2.0 * keys * H * D * 2 + 2.0 * AUDIO * H * D * 2
+    return {"keys": keys, "cond": cond, "bytes": nbytes, "us_median": med,
+            "us_p10": times[len(times) // 10], "us_p90": times[(9 * len(times)) // 10],
+            "gbps": nbytes / (med * 1e-6) / 1e9, "frac_hbm": nbytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBS}
 
 
 COPY_BYTES = 256 << 20
@@ -317,6 +411,9 @@ def main():
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary)
         return
+    if args.cpu_v01_point:
+        print(json.dumps(cpu_v01_point()), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
               "multi-GPU path", file=sys.stderr)
@@ -454,36 +551,13 @@ def main():
     audio_bytes = 2.0 * lk_a * H * D * 2 + 2.0 * AUDIO * H * D * 2
     append_bytes = 4.0 * (COND + LU + AUDIO) * H * D * 2 + 2.0 * (LU + AUDIO) * H * D * 2
 
-    # audio path with cold caches: between repetitions a 1 GiB buffer is read
-    # (a reduction), which evicts the cache with clean lines, so the timed
-    # call neither hits the 256 MB cache nor pays for writing back a dirty
-    # scrub; events around the audio call only
-    cold = None
+    # audio path with cold caches, on the graded key count (a 336-token
+    # conditioning slice: 336 + 9 x 924 = 8652 keys) and on the bench step's
+    # 256-token slice (8572 keys)
+    cold = cold_256 = None
     if args.cold_audio_reps > 0:
-        scrub = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        scrub_sum = torch.empty((), dtype=torch.float32, device=dev)
-        s = sets[u % 2]
-        cache.step_append([
-            dict(unit=u, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"], mode=ws.WS_APPEND_NORM_ROPE,
-                 positions=vpos[u], gamma=gamma, eps=eps),
-            dict(unit=u, kind=ws.WS_KIND_AUDIO, k=s["ka"], v=s["va"], mode=ws.WS_APPEND_NORM_ROPE,
-                 positions=apos[u], gamma=gamma, eps=eps)],
-            [dict(q=s["qa"], q_out=q_a, positions=apos[u], gamma=gamma, eps=eps)])
-        amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
-        times = []
-        for _ in range(args.cold_audio_reps):
-            torch.sum(scrub, dim=0, out=scrub_sum)
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
-            b.record(stream)
-            b.synchronize()
-            times.append(a.elapsed_time(b) * 1e3)
-        times.sort()
-        med = times[len(times) // 2]
-        cold = {"us_median": med, "gbps": audio_bytes / (med * 1e-6) / 1e9,
-                "frac_hbm": audio_bytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBS, "keys": lk_a}
-        del scrub
+        cold = cold_audio(args, ws, sets, vpos, apos, gamma, eps, stream, dev, 336)
+        cold_256 = cold_audio(args, ws, sets, vpos, apos, gamma, eps, stream, dev, COND)
 
     long_hist = long_history(args, ws, sets, gamma, eps, stream, dev) if args.long_reps > 0 else None
     peaks = measured_peaks(ws, torch, stream, dev) if args.peak_probes else None
@@ -515,7 +589,8 @@ def main():
         "video_attention": {"us": t_video, "tflops": fv / (t_video * 1e-6) / 1e12, "flop": fv,
                             "kernel_us": t_vkern, "merge_us": t_vmerge, "splits": v_splits},
         "audio_attention": {"us_warm": t_audio, "gbps_warm": audio_bytes / (t_audio * 1e-6) / 1e9,
-                            "bytes": audio_bytes, "cold": cold},
+                            "bytes": audio_bytes, "keys": lk_a, "cold": cold,
+                            "cold_cond256": cold_256},
         "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
         "long_history": long_hist,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,

@@ -262,6 +262,37 @@ def query_prologue(q_bits_head, mode, positions, gamma, eps, band_pairs=(22, 21,
     return q
 
 
+def unit_attention_groups(cache: OracleCache, q_bits, groups, *, mode=MODE_NORM_ROPE,
+                          positions=None, gamma=None, eps=1e-6, scale=None, heads=None):
+    """Attention of query rows that belong to several units (block-causal
+    queries from more than one unit in one call, Fig. 1 caption; Sec. 2.1).
+
+    groups: sequence of (q_unit, min_visible_unit, kind_mask, n_rows); the
+    rows of q_bits [n_q, H, D] are the groups' rows in order, and group g's
+    rows see exactly what a unit_attention call with that group's mask sees.
+    Returns (out [n_q, len(heads), D], lse [len(heads), n_q]) in float64."""
+    q_bits = np.asarray(q_bits, dtype=np.uint16)
+    n_q, H, D = q_bits.shape
+    if sum(int(g[3]) for g in groups) != n_q:
+        raise ValueError("group row counts must add up to the query rows")
+    heads = list(range(H)) if heads is None else list(heads)
+    out = np.zeros((n_q, len(heads), D))
+    lse = np.full((len(heads), n_q), -np.inf)
+    r0 = 0
+    for q_unit, min_unit, kind_mask, n in groups:
+        n = int(n)
+        if n > 0:
+            rows = slice(r0, r0 + n)
+            pos = None if positions is None else np.asarray(positions)[rows]
+            o, l = unit_attention(cache, q_bits[rows], q_unit, mode=mode, positions=pos,
+                                  gamma=gamma, eps=eps, scale=scale, min_visible_unit=min_unit,
+                                  kind_mask=kind_mask, heads=heads)
+            out[rows] = o
+            lse[:, rows] = l
+        r0 += n
+    return out, lse
+
+
 def unit_attention(cache: OracleCache, q_bits, q_unit, *, mode=MODE_NORM_ROPE, positions=None,
                    gamma=None, eps=1e-6, scale=None, min_visible_unit=-(2 ** 31),
                    kind_mask=0b011, heads=None):

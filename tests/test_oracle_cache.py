@@ -129,3 +129,85 @@ def test_empty_visible_set_gives_zero():
     out, lse = oracle.unit_attention(cache, qb, 5, positions=synth.video_positions(5, (1, 2)),
                                      min_visible_unit=4, kind_mask=0b110)
     assert (out == 0).all() and np.isneginf(lse).all()
+
+
+# --------------------------------------------------------------------------- #
+# queries from several units in one call (block-causal across units)
+# --------------------------------------------------------------------------- #
+def test_groups_identical_keys_give_mean_of_visible_values():
+    """Closed form: when every stored key is the same RAW vector, each query
+    row's output is the plain mean of the values its group sees.  Three query
+    groups (units 0, 1 and 2, the last with a window that hides units 0-1, and
+    a fourth group that sees nothing) over a cache of one conditioning key and
+    one key per unit."""
+    rng = np.random.default_rng(301)
+    key = synth.normal_bf16(rng, (1, H, D))
+    c = oracle.OracleCache(num_heads=H)
+    vals = {}
+    for u, kind in ((0, oracle.KIND_COND), (0, oracle.KIND_VIDEO), (1, oracle.KIND_VIDEO),
+                    (2, oracle.KIND_VIDEO)):
+        v = synth.normal_bf16(rng, (1, H, D))
+        vals[(u, kind)] = synth.bf16_to_f32(v[0]).astype(np.float64)
+        c.append(u, kind, key, v, oracle.MODE_RAW)
+    groups = [(0, -(2 ** 31), 0b011, 2), (1, -(2 ** 31), 0b011, 3), (2, 2, 0b011, 1),
+              (1, 5, 0b010, 2)]
+    q = synth.normal_bf16(rng, (8, H, D))
+    out, lse = oracle.unit_attention_groups(c, q, groups, mode=oracle.MODE_RAW)
+    want = [np.mean([vals[(0, 0)], vals[(0, 1)]], axis=0)] * 2 + \
+        [np.mean([vals[(0, 0)], vals[(0, 1)], vals[(1, 1)]], axis=0)] * 3 + \
+        [np.mean([vals[(0, 0)], vals[(2, 1)]], axis=0)] + [np.zeros((H, D))] * 2
+    np.testing.assert_allclose(out, np.stack(want), rtol=0, atol=1e-12)
+    assert np.isneginf(lse[:, 6:]).all() and np.isfinite(lse[:, :6]).all()
+
+
+def test_groups_masked_equals_deleted():
+    """I4 per group: a group's rows over the full cache equal the same rows
+    over a cache from which the segments its mask hides were deleted."""
+    rng = np.random.default_rng(302)
+    cache, segs = _tiny_cache(rng)
+    groups = [(0, -(2 ** 31), 0b011, 3), (2, 1, 0b111, 4), (1, -(2 ** 31), 0b101, 2)]
+    qb = synth.normal_bf16(rng, (9, H, D))
+    qpos = np.concatenate([synth.video_positions(g[0], (1, g[3])) for g in groups])
+    out, lse = oracle.unit_attention_groups(cache, qb, groups, positions=qpos, gamma=np.ones(D))
+    r0 = 0
+    for q_unit, min_unit, kind_mask, n in groups:
+        pruned = oracle.OracleCache(num_heads=H)
+        for u, kind, k, v, pos in _visible(segs, q_unit, min_unit, kind_mask):
+            pruned.append(u, kind, k, v, oracle.MODE_RAW if kind == oracle.KIND_COND
+                          else oracle.MODE_NORM_ROPE, pos, np.ones(D), 1e-6)
+        o, l = oracle.unit_attention(pruned, qb[r0:r0 + n], q_unit, positions=qpos[r0:r0 + n],
+                                     gamma=np.ones(D), kind_mask=0b111)
+        np.testing.assert_allclose(out[r0:r0 + n], o, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse[:, r0:r0 + n], l, rtol=0, atol=1e-12)
+        r0 += n
+
+
+def test_groups_match_per_row_visibility_matrix():
+    """The groups' result against dense attention over every stored key with
+    an explicit per-(row, key) visibility matrix (the C routine's mask path,
+    not the segment selection), on the tiny cache: rows of units 0, 1 and 2
+    with different windows and kinds."""
+    rng = np.random.default_rng(303)
+    cache, segs = _tiny_cache(rng)
+    groups = [(2, 2, 0b111, 2), (0, -(2 ** 31), 0b011, 3), (1, 1, 0b110, 2)]
+    qb = synth.normal_bf16(rng, (7, H, D))
+    qpos = np.concatenate([synth.video_positions(g[0], (1, g[3])) for g in groups])
+    out, _ = oracle.unit_attention_groups(cache, qb, groups, positions=qpos, gamma=np.ones(D))
+    row_group = np.repeat(np.arange(len(groups)), [g[3] for g in groups])
+    for h in range(H):
+        ks, vs, labels = [], [], []
+        for s in cache.segments:
+            k, v = cache.segment_kv(s, h)
+            ks.append(k)
+            vs.append(v)
+            labels += [(s.unit, s.kind)] * k.shape[0]
+        k, v = np.concatenate(ks), np.concatenate(vs)
+        vis = np.zeros((qb.shape[0], k.shape[0]), np.uint8)
+        for i, g in enumerate(row_group):
+            q_unit, min_unit, kind_mask, _ = groups[g]
+            for j, (u, kind) in enumerate(labels):
+                vis[i, j] = ((kind_mask >> kind) & 1) and u <= q_unit and \
+                    (kind == oracle.KIND_COND or u >= min_unit)
+        q = oracle.query_prologue(qb[:, h], oracle.MODE_NORM_ROPE, qpos, np.ones(D), 1e-6)
+        o, _ = oracle.attention(q, k, v, 1.0 / math.sqrt(D), visible=vis)
+        np.testing.assert_allclose(out[:, h], o, rtol=0, atol=1e-12)
