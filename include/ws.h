@@ -265,6 +265,32 @@ WS_API ws_status ws_unit_attention(const void* q, int64_t q_tok_stride, int64_t 
                             const ws_mask_spec* mask, void* out, int64_t out_tok_stride,
                             int64_t out_head_stride, void* hip_stream);
 
+/* Queries of several units in one call (Fig. 1 caption: block-causal
+ * attention on one timeline; Sec. 2.1: units committed into history), e.g. a
+ * catch-up after a stall or re-encoding committed units.  The call's query
+ * rows are the groups' rows in order: group g holds groups[g].n_q >= 0 rows
+ * (at least one group has rows) and its rows see exactly what
+ * ws_unit_attention with groups[g].mask would let them see.  Each group's
+ * visible page list is built on the host and walked only by that group's
+ * query tiles, so pages a group's mask hides cost it nothing; a group that
+ * sees nothing gets zero rows.  Arguments as ws_unit_attention, with n_q =
+ * the sum of the groups' rows (at most max_q_tokens) and qdesc's positions
+ * covering all rows; 1 <= n_groups <= WS_MAX_QUERY_GROUPS.  groups: host
+ * array, read before the call returns.  With a single group the call is
+ * ws_unit_attention. */
+typedef struct ws_query_group {
+  int32_t n_q;
+  ws_mask_spec mask;
+} ws_query_group;
+
+#define WS_MAX_QUERY_GROUPS 8
+
+WS_API ws_status ws_unit_attention_groups(const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+                                          int32_t n_groups, const ws_query_group* groups,
+                                          const ws_query_desc* qdesc, ws_cache* cache, void* out,
+                                          int64_t out_tok_stride, int64_t out_head_stride,
+                                          void* hip_stream);
+
 /* The same attention for the few audio latent queries of a unit (Sec. 3:
  * short, unsharded).  Memory-bound split-KV kernel: fp32 partials over key
  * ranges, merged by log-sum-exp.  Arguments as ws_unit_attention;

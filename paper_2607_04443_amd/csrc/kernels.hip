@@ -895,17 +895,18 @@ __device__ __forceinline__ void video_flush(const VideoCtx& c, VideoState& st, c
   }
 }
 
-// One segment of a video workgroup's work: query tile `qtile` of head `head`
-// against pages [p_begin, p_end) of the visible list, which is key range `seg`
-// of the n_seg ranges that split this head's pages.  With one range the
-// output is written in bf16; otherwise the softmax-normalised fp32 partial and
-// its log-sum-exp go to the split-KV workspace for the combine kernel.
+// One segment of a video workgroup's work: the query tile of rows
+// [q_lo, min(q_lo + 256, q_hi)) of head `head` against entries
+// [p_begin, p_end) of the call's page list, which is key range `seg` of the
+// n_seg ranges that split this head's pages (q_hi ends the tile's query
+// class).  With one range the output is written in bf16; otherwise the
+// softmax-normalised partial and its log-sum-exp go to the split-KV
+// workspace for the combine kernel.
 struct VideoSeg {
-  int head, p_begin, p_end, seg, n_seg;
+  int head, p_begin, p_end, seg, n_seg, q_lo, q_hi;
 };
 
-__device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg& sg, int qtile,
-                                              bool first_segment) {
+__device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg& sg, bool first_segment) {
   // Lane-derived values (LDS and load offsets) are recomputed per segment:
   // kept live across the segment loop they would push the page loop into
   // register spills.
@@ -921,7 +922,7 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
   c.kpool = a.kpool + head * kPageHeadElems;
   c.vpool = a.vpool + head * kPageHeadElems;
-  c.active = qtile * kVideoQTile + wave * 32 < a.n_q;
+  c.active = sg.q_lo + wave * 32 < sg.q_hi;
   c.wave = wave;
   c.half = half;
   c.l32 = l32;
@@ -945,8 +946,8 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 #pragma unroll
     for (int k = 0; k < 3; ++k) pg_first[k] = c.pages[min(p_begin + k, p_end - 1)].x;
   }
-  const int q = qtile * kVideoQTile + wave * 32 + l32;
-  const bool q_ok = q < a.n_q;
+  const int q = sg.q_lo + wave * 32 + l32;
+  const bool q_ok = q < sg.q_hi;
   const bool norm_rope = a.mode == 1;
   int3 qpos = make_int3(0, 0, 0);
   if (norm_rope && q_ok) qpos = make_int3(a.positions[3 * q], a.positions[3 * q + 1], a.positions[3 * q + 2]);
@@ -1137,27 +1138,47 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   if (half == 0) a.part_lse[row] = l_tot > 0.f ? st.m_run + __log2f(l_tot) : kNegInf;
 }
 
+// The call's query classes, read in place from the kernel arguments (the
+// kernel's only argument is the AttnArgs; indexing the by-value argument at a
+// run-time class would make the compiler copy it to private memory).
+typedef const __attribute__((address_space(4))) AttnClass* const_class_table;
+__device__ __forceinline__ const_class_table class_table() {
+  const __attribute__((address_space(4))) char* seg =
+      (const __attribute__((address_space(4))) char*)__builtin_amdgcn_kernarg_segment_ptr();
+  return (const_class_table)(seg + offsetof(AttnArgs, cls));
+}
+
 __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
-  // Work decode.  The grid is n_groups groups of n_qtiles workgroups; group g
-  // takes a contiguous share of the (head, page) units in head-major order
-  // (VideoPartition: even shares of pages plus a cost per head started), one
-  // workgroup per query tile, so the work fits a single round, and a share
-  // that crosses a head boundary is processed as two segments.  Workgroups are dispatched round-robin over the 8 XCDs;
-  // renumber so that consecutive work items (the query tiles of a group,
-  // which read the same pages at the same time, and neighbouring groups) run
-  // on one XCD and share its L2.
+  // Work decode.  Each query class (the rows of one unit's queries, with the
+  // pages its mask leaves visible) owns a block of workgroups: n_groups
+  // groups of n_qtiles workgroups; group g takes a contiguous share of the
+  // class's (head, page) units in head-major order (VideoPartition: even
+  // shares of pages plus a cost per head started), one workgroup per query
+  // tile, so the work fits a single round, and a share that crosses a head
+  // boundary is processed as two segments.  Workgroups are dispatched
+  // round-robin over the 8 XCDs; renumber so that consecutive work items
+  // (the query tiles of a group, which read the same pages at the same time,
+  // and neighbouring groups) run on one XCD and share its L2.
   const int nblk = gridDim.x, bid = blockIdx.x;
   const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
   const int item = xcd * per + min(xcd, rem) + (bid >> 3);
-  const int qtile = item % a.n_qtiles;
-  const int64_t group = item / a.n_qtiles;
-  const int64_t n_pages = a.n_pages;
+  const const_class_table tab = class_table();
+  int ci = 0;
+  for (int k = 1; k < a.n_classes; ++k)
+    if (item >= tab[k].wg0) ci = k;
+  const int local = item - tab[ci].wg0;
+  const int n_qtiles = tab[ci].n_qtiles;
+  const int q0 = tab[ci].q0, q_hi = q0 + tab[ci].n_q;
+  const int page0 = tab[ci].page0;
+  const int q_lo = q0 + (local % n_qtiles) * kVideoQTile;
+  const int64_t group = local / n_qtiles;
+  const int64_t n_pages = tab[ci].n_pages;
   if (n_pages == 0) {  // nothing visible: one empty segment per head, output 0
     if (group < a.num_heads)
-      video_segment(a, VideoSeg{static_cast<int>(group), 0, 0, 0, 1}, qtile, true);
+      video_segment(a, VideoSeg{static_cast<int>(group), 0, 0, 0, 1, q_lo, q_hi}, true);
     return;
   }
-  const VideoPartition part{a.num_heads, n_pages, a.seg_cost, a.n_groups};
+  const VideoPartition part{a.num_heads, n_pages, a.seg_cost, tab[ci].n_groups};
   const int64_t lo = video_group_lo(part, group), hi = video_group_lo(part, group + 1);
   bool first = true;
   for (int64_t x = lo; x < hi; first = false) {
@@ -1165,9 +1186,9 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
     const int64_t x_end = min(hi, h0 + n_pages);
     const int64_t g_first = video_group_of(part, h0);
     const int64_t g_last = video_group_of(part, h0 + n_pages - 1);
-    const VideoSeg sg{static_cast<int>(head), static_cast<int>(x - h0), static_cast<int>(x_end - h0),
-                      static_cast<int>(group - g_first), static_cast<int>(g_last - g_first + 1)};
-    video_segment(a, sg, qtile, first);
+    const VideoSeg sg{static_cast<int>(head), page0 + static_cast<int>(x - h0), page0 + static_cast<int>(x_end - h0),
+                      static_cast<int>(group - g_first), static_cast<int>(g_last - g_first + 1), q_lo, q_hi};
+    video_segment(a, sg, first);
     x = x_end;
   }
 }
@@ -1532,14 +1553,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
 // rows per block; all of a row's (at most kMaxVideoSplits) partials are
 // requested before any is used.
 // ------------------------------------------------------------------------- //
-__device__ __forceinline__ void video_combine_block(const CombineArgs& a, int bid) {
+__device__ __forceinline__ void video_combine_block(const CombineArgs& a, const_class_table tab, int bid) {
   const int lane = threadIdx.x & 15;
   const int row = bid * 16 + (threadIdx.x >> 4);
   if (row >= a.num_heads * a.n_q) return;
   const int head = row / a.n_q, q = row % a.n_q;
-  const VideoPartition part{a.num_heads, a.n_pages, a.seg_cost, a.n_groups};
-  const int64_t h0 = static_cast<int64_t>(head) * a.n_pages;
-  const int n_ranges = static_cast<int>(video_group_of(part, h0 + a.n_pages - 1) - video_group_of(part, h0) + 1);
+  int ci = 0;  // the row's query class
+  for (int k = 1; k < a.n_classes; ++k)
+    if (q >= tab[k].q0) ci = k;
+  const int64_t n_pages = tab[ci].n_pages;
+  if (n_pages == 0) return;
+  const VideoPartition part{a.num_heads, n_pages, a.seg_cost, tab[ci].n_groups};
+  const int64_t h0 = static_cast<int64_t>(head) * n_pages;
+  const int n_ranges = static_cast<int>(video_group_of(part, h0 + n_pages - 1) - video_group_of(part, h0) + 1);
   if (n_ranges < 2) return;
   const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
@@ -1583,8 +1609,16 @@ __device__ __forceinline__ void video_combine_block(const CombineArgs& a, int bi
   *reinterpret_cast<u32x4*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = o;
 }
 
+// The class table of the video CombineArgs, which is the first kernel
+// argument of both merge kernels below, read in place.
+__device__ __forceinline__ const_class_table combine_class_table() {
+  const __attribute__((address_space(4))) char* seg =
+      (const __attribute__((address_space(4))) char*)__builtin_amdgcn_kernarg_segment_ptr();
+  return (const_class_table)(seg + offsetof(CombineArgs, cls));
+}
+
 __global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a) {
-  video_combine_block(a, blockIdx.x);
+  video_combine_block(a, combine_class_table(), blockIdx.x);
 }
 
 // The merges of one step's video and audio calls in one launch: blocks below
@@ -1593,7 +1627,7 @@ template <int kGroups>
 __global__ __launch_bounds__(256) void step_combine_kernel(const CombineArgs v, const CombineArgs au,
                                                            int n_video) {
   if (static_cast<int>(blockIdx.x) < n_video)
-    video_combine_block(v, blockIdx.x);
+    video_combine_block(v, combine_class_table(), blockIdx.x);
   else
     combine_block<kGroups>(au, blockIdx.x - n_video);
 }
@@ -1631,7 +1665,7 @@ hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_qtiles * a.n_groups);
+  dim3 grid(a.n_wg);
   hipLaunchKernelGGL(unit_attn_kernel, grid, dim3(kVideoWaves * 64), 0, stream, a);
   return hipGetLastError();
 }

@@ -113,6 +113,10 @@ bool PageTable::segment_visible(const Segment& s, const MaskSpec& mask) {
 
 void PageTable::visible_pages(const MaskSpec& mask, std::vector<PageRef>* out) const {
   out->clear();
+  visible_pages_append(mask, out);
+}
+
+void PageTable::visible_pages_append(const MaskSpec& mask, std::vector<PageRef>* out) const {
   for (const auto& s : segments_) {
     if (!segment_visible(s, mask)) continue;
     int32_t left = s.n_tokens;

@@ -61,6 +61,9 @@ class PageTable {
 
   // Pages visible to a query set of mask.q_unit, in segment creation order.
   void visible_pages(const MaskSpec& mask, std::vector<PageRef>* out) const;
+  // The same list, appended to *out (for the concatenated lists of a call
+  // whose queries belong to several units).
+  void visible_pages_append(const MaskSpec& mask, std::vector<PageRef>* out) const;
   static bool segment_visible(const Segment& s, const MaskSpec& mask);
 
  private:

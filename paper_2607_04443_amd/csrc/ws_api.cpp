@@ -55,13 +55,27 @@ struct TimingRing {
   std::vector<ws_call_timing> meta;
 };
 
+// A call's query groups: rows of one unit each, with that unit's mask.
+struct QueryGroup {
+  ws::MaskSpec mask;
+  int32_t n_q;
+};
+
+// A page list uploaded to the device arena: the concatenated visible lists
+// of a call's query groups (one per group with rows), kept while the cache
+// structure does not change.
 struct ListCacheEntry {
   bool valid = false;
-  ws::MaskSpec mask{};
+  int32_t n_masks = 0;
+  ws::MaskSpec masks[ws::kMaxClasses]{};
   uint64_t version = 0;
   size_t offset = 0;
   int32_t n = 0;
 };
+
+bool same_mask(const ws::MaskSpec& a, const ws::MaskSpec& b) {
+  return a.q_unit == b.q_unit && a.min_visible_unit == b.min_visible_unit && a.kind_mask == b.kind_mask;
+}
 
 }  // namespace
 
@@ -160,31 +174,33 @@ ws_status upload_list(ws_cache* c, const std::vector<ws::PageRef>& list, hipStre
   return WS_OK;
 }
 
-ws_status visible_list(ws_cache* c, const ws_mask_spec* m, hipStream_t stream, const int2** dev,
-                       int32_t* n) {
-  const ws::MaskSpec mask{m->q_unit, m->min_visible_unit, m->kind_mask};
+// The concatenated visible page lists of masks[0..n_masks) (c->scratch_list
+// holds them, built by the caller) in the device arena: reused while the
+// cache structure and the masks are unchanged, else uploaded once.
+ws_status arena_list(ws_cache* c, const ws::MaskSpec* masks, int n_masks, hipStream_t stream,
+                     const int2** dev) {
   const uint64_t ver = c->pt.version();
   for (auto& e : c->lists) {
-    if (e.valid && e.version == ver && e.mask.q_unit == mask.q_unit &&
-        e.mask.min_visible_unit == mask.min_visible_unit && e.mask.kind_mask == mask.kind_mask) {
+    if (!e.valid || e.version != ver || e.n_masks != n_masks) continue;
+    bool same = true;
+    for (int i = 0; i < n_masks && same; ++i) same = same_mask(e.masks[i], masks[i]);
+    if (same) {
       *dev = c->arena_dev + e.offset;
-      *n = e.n;
       return WS_OK;
     }
   }
-  c->pt.visible_pages(mask, &c->scratch_list);
   size_t off = 0;
   ws_status st = upload_list(c, c->scratch_list, stream, &off);
   if (st != WS_OK) return st;
   ListCacheEntry& e = c->lists[c->list_next];
   c->list_next = (c->list_next + 1) % 4;
   e.valid = true;
-  e.mask = mask;
+  e.n_masks = n_masks;
+  for (int i = 0; i < n_masks; ++i) e.masks[i] = masks[i];
   e.version = ver;
   e.offset = off;
   e.n = static_cast<int32_t>(c->scratch_list.size());
   *dev = c->arena_dev + off;
-  *n = e.n;
   return WS_OK;
 }
 
@@ -330,13 +346,13 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
 // pipeline refill) takes about as long as six pages of the main loop.
 constexpr int kVideoSegCostPages = 6;
 
-int choose_video_groups(const ws_cache* c, int n_heads, int n_qtiles, int n_pages) {
+int choose_video_groups(const ws_cache* c, int n_heads, int n_qtiles, int n_pages, int n_cus) {
   if (n_pages == 0) return n_heads;
   if (c->opt_video_splits > 0) return n_heads * c->opt_video_splits;
   constexpr double kSegCostPages = 9.5;
   constexpr int64_t kMinGroupPages = 4;
   const int64_t units = static_cast<int64_t>(n_heads) * n_pages;
-  const int64_t one_round = std::max<int64_t>(1, c->num_cus / n_qtiles);
+  const int64_t one_round = std::max<int64_t>(1, n_cus / n_qtiles);
   // at most kMaxVideoSplits ranges per head: ceil(G / H) + 1 <= kMaxVideoSplits
   const int64_t g_max = std::min<int64_t>({static_cast<int64_t>(n_heads) * (kMaxVideoSplits - 1),
                                            std::max<int64_t>(1, units / kMinGroupPages), 4 * one_round});
@@ -380,11 +396,18 @@ struct AttnPlan {
 };
 
 ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
-                         int32_t n_q, const ws_query_desc* qd, ws_cache* c, const ws_mask_spec* m,
+                         int32_t n_groups, const QueryGroup* groups, const ws_query_desc* qd, ws_cache* c,
                          void* out, int64_t out_tok_stride, int64_t out_head_stride,
                          hipStream_t stream, AttnPlan* plan) {
-  if (!c || !qd || !m) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (!c || !qd || !groups) return fail(WS_ERR_INVALID_ARG, "NULL argument");
   if (ws_status st = check_device(c); st != WS_OK) return st;
+  if (n_groups < 1 || n_groups > (audio ? 1 : ws::kMaxClasses))
+    return fail(WS_ERR_INVALID_ARG, "query group count %d outside [1, %d]", n_groups, audio ? 1 : ws::kMaxClasses);
+  int32_t n_q = 0;
+  for (int g = 0; g < n_groups; ++g) {
+    if (groups[g].n_q < 0) return fail(WS_ERR_SHAPE, "query group %d has a negative row count", g);
+    n_q += groups[g].n_q;
+  }
   const int H = c->cfg.num_heads;
   const int max_q = audio ? std::min(c->cfg.max_q_tokens, kMaxAudioQ) : c->cfg.max_q_tokens;
   if (n_q < 1 || n_q > max_q) return fail(WS_ERR_SHAPE, "n_q %d out of range [1, %d]", n_q, max_q);
@@ -401,22 +424,36 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
   if (!std::isfinite(qd->softmax_scale) || qd->softmax_scale < 0.f)
     return fail(WS_ERR_INVALID_ARG, "bad softmax_scale");
 
-  // The visible page list goes into the kernel arguments when it fits, else
-  // into the device arena (one upload per distinct list).
+  // Each group with rows is a query class with its own visible page list;
+  // the lists are concatenated.  The whole list goes into the kernel
+  // arguments when it fits, else into the device arena (one upload per
+  // distinct list).
   plan->audio = audio;
   ws::AttnArgs& a = plan->a;
   a = ws::AttnArgs{};
   const int2* plist = nullptr;
-  int32_t n_pages = 0;
-  c->pt.visible_pages(ws::MaskSpec{m->q_unit, m->min_visible_unit, m->kind_mask}, &c->scratch_list);
-  if (c->scratch_list.size() <= static_cast<size_t>(ws::AttnArgs::kInlinePages)) {
-    n_pages = static_cast<int32_t>(c->scratch_list.size());
+  ws::MaskSpec masks[ws::kMaxClasses];
+  int n_cls = 0;
+  c->scratch_list.clear();
+  for (int g = 0, r0 = 0; g < n_groups; r0 += groups[g].n_q, ++g) {
+    if (groups[g].n_q == 0) continue;
+    ws::AttnClass& cl = a.cls[n_cls];
+    masks[n_cls++] = groups[g].mask;
+    cl.q0 = r0;
+    cl.n_q = groups[g].n_q;
+    cl.page0 = static_cast<int32_t>(c->scratch_list.size());
+    c->pt.visible_pages_append(groups[g].mask, &c->scratch_list);
+    cl.n_pages = static_cast<int32_t>(c->scratch_list.size()) - cl.page0;
+  }
+  const int32_t n_pages = static_cast<int32_t>(c->scratch_list.size());
+  if (n_pages <= ws::AttnArgs::kInlinePages) {
     for (int32_t i = 0; i < n_pages; ++i)
       a.inline_pages[i] = make_int2(c->scratch_list[static_cast<size_t>(i)].page,
                                     c->scratch_list[static_cast<size_t>(i)].n_valid);
-  } else if (ws_status st = visible_list(c, m, stream, &plist, &n_pages); st != WS_OK) {
+  } else if (ws_status st = arena_list(c, masks, n_cls, stream, &plist); st != WS_OK) {
     return st;
   }
+  a.n_classes = n_cls;
   a.q = static_cast<const uint16_t*>(q);
   a.q_tok_stride = q_tok_stride;
   a.q_head_stride = q_head_stride;
@@ -458,20 +495,47 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
     a.pages_per_split = pps;
     plan->part_rows = static_cast<int64_t>(splits) * H * n_q;
   } else {
-    const int groups = choose_video_groups(c, H, a.n_qtiles, n_pages);
-    // ranges per head: exactly the forced split count, else at most
-    // ceil(groups / H) + 1 (a share of at most one head's pages meets at
-    // most two heads); a single range writes bf16 directly
-    const int64_t max_ranges = c->opt_video_splits > 0 ? c->opt_video_splits
-                               : std::max<int64_t>(2, (groups + H - 1) / H + 1);
+    // Per class: query tiles, and groups of workgroups sharing the class's
+    // (head, page) units.  Several classes share the CUs in proportion to
+    // their work (query tiles x pages).
+    int64_t work = 0;
+    for (int k = 0; k < n_cls; ++k) {
+      a.cls[k].n_qtiles = (a.cls[k].n_q + ws::kVideoQTile - 1) / ws::kVideoQTile;
+      work += static_cast<int64_t>(a.cls[k].n_qtiles) * a.cls[k].n_pages;
+    }
+    int64_t max_ranges = 1;
+    int32_t wg = 0, total_groups = 0;
+    merge = false;
+    for (int k = 0; k < n_cls; ++k) {
+      ws::AttnClass& cl = a.cls[k];
+      const int64_t w = static_cast<int64_t>(cl.n_qtiles) * cl.n_pages;
+      const int cus = n_cls == 1 || work == 0
+                          ? c->num_cus
+                          : static_cast<int>(std::max<int64_t>(cl.n_qtiles, c->num_cus * w / work));
+      cl.n_groups = choose_video_groups(c, H, cl.n_qtiles, cl.n_pages, cus);
+      cl.wg0 = wg;
+      wg += cl.n_groups * cl.n_qtiles;
+      total_groups += cl.n_groups;
+      // ranges per head: exactly the forced split count, else at most
+      // ceil(groups / H) + 1 (a share of at most one head's pages meets at
+      // most two heads); a single range writes bf16 directly
+      if (cl.n_pages > 0 && cl.n_groups != H) {
+        merge = true;
+        max_ranges = std::max<int64_t>(max_ranges, c->opt_video_splits > 0
+                                                       ? c->opt_video_splits
+                                                       : std::max(2, (cl.n_groups + H - 1) / H + 1));
+      }
+    }
     if (cap < max_ranges) return fail(WS_ERR_SHAPE, "split-KV workspace too small");
     plan->part_rows = max_ranges * H * n_q;
-    a.n_groups = groups;
+    a.n_groups = total_groups;
+    a.n_wg = wg;
+    a.n_qtiles = 0;
+    for (int k = 0; k < n_cls; ++k) a.n_qtiles += a.cls[k].n_qtiles;
     // forced splits keep equal ranges per head
     a.seg_cost = c->opt_video_splits > 0 ? 0 : kVideoSegCostPages;
     a.n_splits = 1;
-    splits = groups;
-    merge = n_pages > 0 && groups != H;
+    splits = total_groups;
   }
 
   plan->splits = splits;
@@ -481,10 +545,11 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
     cb = ws::CombineArgs{};
     cb.part_o = a.part_o;
     cb.part_lse = a.part_lse;
-    cb.n_splits = audio ? splits : static_cast<int>(std::min<int64_t>(
-                                       kMaxVideoSplits, (splits + H - 1) / H + 1));
+    cb.n_splits = audio ? splits : kMaxVideoSplits;
     cb.n_groups = audio ? 0 : splits;
-    cb.n_pages = n_pages;
+    cb.n_classes = audio ? 0 : a.n_classes;
+    if (!audio)
+      for (int k = 0; k < a.n_classes; ++k) cb.cls[k] = a.cls[k];
     cb.seg_cost = a.seg_cost;
     cb.n_q = n_q;
     cb.num_heads = H;
@@ -522,13 +587,13 @@ ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream) {
 }
 
 ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
-                         int32_t n_q, const ws_query_desc* qd, ws_cache* c, const ws_mask_spec* m,
+                         int32_t n_groups, const QueryGroup* groups, const ws_query_desc* qd, ws_cache* c,
                          void* out, int64_t out_tok_stride, int64_t out_head_stride,
                          void* hip_stream) {
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   AttnPlan p;
-  if (ws_status st = plan_attention(audio, q, q_tok_stride, q_head_stride, n_q, qd, c, m, out, out_tok_stride,
-                                    out_head_stride, stream, &p);
+  if (ws_status st = plan_attention(audio, q, q_tok_stride, q_head_stride, n_groups, groups, qd, c, out,
+                                    out_tok_stride, out_head_stride, stream, &p);
       st != WS_OK)
     return st;
   int slot = -1;
@@ -581,16 +646,19 @@ ws_status step_attention_impl(ws_cache* c, const ws_attn_call* video, const ws_a
   if (!c || !video || !audio) return fail(WS_ERR_INVALID_ARG, "NULL argument");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   AttnPlan pv, pa;
+  const QueryGroup gv{ws::MaskSpec{video->mask.q_unit, video->mask.min_visible_unit, video->mask.kind_mask},
+                      video->n_q};
+  const QueryGroup ga{ws::MaskSpec{audio->mask.q_unit, audio->mask.min_visible_unit, audio->mask.kind_mask},
+                      audio->n_q};
   auto plan_video = [&]() {
-    return plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, video->n_q,
-                          &video->desc, c, &video->mask, video->out, video->out_tok_stride,
-                          video->out_head_stride, stream, &pv);
+    return plan_attention(false, video->q, video->q_tok_stride, video->q_head_stride, 1, &gv, &video->desc, c,
+                          video->out, video->out_tok_stride, video->out_head_stride, stream, &pv);
   };
   if (ws_status st = plan_video(); st != WS_OK) return st;
   const uint64_t wraps = c->arena_wraps;
-  if (ws_status st = plan_attention(true, audio->q, audio->q_tok_stride, audio->q_head_stride, audio->n_q,
-                                    &audio->desc, c, &audio->mask, audio->out, audio->out_tok_stride,
-                                    audio->out_head_stride, stream, &pa);
+  if (ws_status st = plan_attention(true, audio->q, audio->q_tok_stride, audio->q_head_stride, 1, &ga,
+                                    &audio->desc, c, audio->out, audio->out_tok_stride, audio->out_head_stride,
+                                    stream, &pa);
       st != WS_OK)
     return st;
   // A page list uploaded by the audio plan that started the arena over may
@@ -884,16 +952,36 @@ ws_status ws_unit_attention(const void* q, int64_t q_tok_stride, int64_t q_head_
                             const ws_query_desc* qdesc, ws_cache* cache, const ws_mask_spec* mask,
                             void* out, int64_t out_tok_stride, int64_t out_head_stride,
                             void* hip_stream) {
-  return attention_impl(false, q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
-                        out_tok_stride, out_head_stride, hip_stream);
+  if (!mask) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  const QueryGroup g{ws::MaskSpec{mask->q_unit, mask->min_visible_unit, mask->kind_mask}, n_q};
+  return attention_impl(false, q, q_tok_stride, q_head_stride, 1, &g, qdesc, cache, out, out_tok_stride,
+                        out_head_stride, hip_stream);
+}
+
+ws_status ws_unit_attention_groups(const void* q, int64_t q_tok_stride, int64_t q_head_stride,
+                                   int32_t n_groups, const ws_query_group* groups, const ws_query_desc* qdesc,
+                                   ws_cache* cache, void* out, int64_t out_tok_stride, int64_t out_head_stride,
+                                   void* hip_stream) {
+  if (!groups) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  if (n_groups < 1 || n_groups > WS_MAX_QUERY_GROUPS)
+    return fail(WS_ERR_INVALID_ARG, "query group count %d outside [1, %d]", n_groups, WS_MAX_QUERY_GROUPS);
+  QueryGroup g[WS_MAX_QUERY_GROUPS];
+  for (int i = 0; i < n_groups; ++i)
+    g[i] = QueryGroup{ws::MaskSpec{groups[i].mask.q_unit, groups[i].mask.min_visible_unit,
+                                   groups[i].mask.kind_mask},
+                      groups[i].n_q};
+  return attention_impl(false, q, q_tok_stride, q_head_stride, n_groups, g, qdesc, cache, out, out_tok_stride,
+                        out_head_stride, hip_stream);
 }
 
 ws_status ws_audio_attention(const void* q, int64_t q_tok_stride, int64_t q_head_stride, int32_t n_q,
                              const ws_query_desc* qdesc, ws_cache* cache, const ws_mask_spec* mask,
                              void* out, int64_t out_tok_stride, int64_t out_head_stride,
                              void* hip_stream) {
-  return attention_impl(true, q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, out,
-                        out_tok_stride, out_head_stride, hip_stream);
+  if (!mask) return fail(WS_ERR_INVALID_ARG, "NULL argument");
+  const QueryGroup g{ws::MaskSpec{mask->q_unit, mask->min_visible_unit, mask->kind_mask}, n_q};
+  return attention_impl(true, q, q_tok_stride, q_head_stride, 1, &g, qdesc, cache, out, out_tok_stride,
+                        out_head_stride, hip_stream);
 }
 
 ws_status ws_step_attention(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio, void* hip_stream) {

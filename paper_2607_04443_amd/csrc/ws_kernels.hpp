@@ -109,6 +109,17 @@ struct AppendArgs {
   uint8_t blk_seg[kMaxAppendPages];
 };
 
+// Query class of a video attention call: the rows of one unit's queries in a
+// call that holds queries of several units.  Rows [q0, q0 + n_q) of the call
+// walk entries [page0, page0 + n_pages) of the call's page list (the pages
+// their block-causal mask leaves visible), with n_groups groups of n_qtiles
+// workgroups starting at workgroup wg0 (VideoPartition over this class's
+// pages).  A call with queries of one unit is one class.
+struct AttnClass {
+  int32_t q0, n_q, page0, n_pages, n_groups, n_qtiles, wg0, pad;
+};
+constexpr int kMaxClasses = 8;
+
 struct AttnArgs {
   // Visible page lists up to this length travel in the kernel arguments
   // (no upload, no copy dispatch ahead of the kernel); longer ones are
@@ -135,9 +146,12 @@ struct AttnArgs {
   int32_t n_pages;
   int32_t n_splits;      // audio: key-range splits (the combine kernel merges them)
   int32_t pages_per_split;
-  int32_t n_groups;      // video: workgroup groups sharing the (head, page) units
+  int32_t n_groups;      // video: workgroup groups sharing the (head, page) units (all classes)
   int32_t seg_cost;      // video: partition cost of starting a head (VideoPartition)
-  int32_t n_qtiles;
+  int32_t n_qtiles;      // audio: query tiles; video: all classes' query tiles
+  int32_t n_classes;     // video: query classes (1..kMaxClasses)
+  int32_t n_wg;          // video: workgroups of the launch (all classes)
+  AttnClass cls[kMaxClasses];
   uint16_t* out;
   int64_t out_tok_stride;
   int64_t out_head_stride;
@@ -152,8 +166,10 @@ struct CombineArgs {
   const float* part_lse;
   int32_t n_splits;      // key ranges per head (when n_groups == 0)
   int32_t n_groups;      // > 0: video schedule, ranges per head follow from
-  int32_t n_pages;       //      the groups' shares (VideoPartition)
+                         //      each class's shares (VideoPartition)
+  int32_t n_classes;     // video: the call's query classes (AttnArgs::cls)
   int32_t seg_cost;
+  AttnClass cls[kMaxClasses];
   int32_t n_q;
   int32_t num_heads;
   uint16_t* out;

@@ -89,6 +89,13 @@ class ws_attn_call(ctypes.Structure):
                 ("out_tok_stride", ctypes.c_int64), ("out_head_stride", ctypes.c_int64)]
 
 
+class ws_query_group(ctypes.Structure):
+    _fields_ = [("n_q", ctypes.c_int32), ("mask", ws_mask_spec)]
+
+
+WS_MAX_QUERY_GROUPS = 8
+
+
 class ws_cache_stats(ctypes.Structure):
     _fields_ = [("pages_total", ctypes.c_int32), ("pages_free", ctypes.c_int32),
                 ("n_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
@@ -115,6 +122,8 @@ _SIGS = {
                           _i64, _i64, _vp],
     "ws_audio_attention": [_vp, _i64, _i64, _i32, _P(ws_query_desc), _vp, _P(ws_mask_spec), _vp,
                            _i64, _i64, _vp],
+    "ws_unit_attention_groups": [_vp, _i64, _i64, _i32, _P(ws_query_group), _P(ws_query_desc), _vp,
+                                 _vp, _i64, _i64, _vp],
     "ws_step_attention": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_step_attention_noalloc": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_cache_export": [_vp, _i32, _i32, _vp, _vp],
@@ -208,6 +217,15 @@ def ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, qdesc, cache, mask, 
     _check(_lib.ws_audio_attention(q, q_tok_stride, q_head_stride, n_q, ctypes.byref(qdesc), cache,
                                    ctypes.byref(mask), out, out_tok_stride, out_head_stride,
                                    stream), "ws_audio_attention")
+
+
+def ws_unit_attention_groups(q, q_tok_stride, q_head_stride, groups, qdesc, cache, out,
+                             out_tok_stride, out_head_stride, stream):
+    """groups: a sequence of ws_query_group."""
+    arr = (ws_query_group * max(len(groups), 1))(*groups)
+    _check(_lib.ws_unit_attention_groups(q, q_tok_stride, q_head_stride, len(groups), arr,
+                                         ctypes.byref(qdesc), cache, out, out_tok_stride,
+                                         out_head_stride, stream), "ws_unit_attention_groups")
 
 
 def ws_step_attention(cache, video: ws_attn_call, audio: ws_attn_call, stream):
@@ -425,6 +443,26 @@ class Cache:
                        eps=1e-6, scale=0.0, stream=None):
         return self._attn(ws_unit_attention, q, out, mask, mode, positions, gamma, eps, scale,
                           stream)
+
+    def unit_attention_groups(self, q, out, groups, mode=WS_APPEND_NORM_ROPE, positions=None,
+                              gamma=None, eps=1e-6, scale=0.0, stream=None):
+        """groups: (n_rows, ws_mask_spec) pairs; q's rows are the groups' rows in order."""
+        import torch
+        _check_tensor("q", q, torch.bfloat16)
+        _check_tensor("out", out, torch.bfloat16)
+        qd = ws_query_desc()
+        qd.mode = mode
+        qd.positions = positions.data_ptr() if positions is not None else None
+        qd.gamma = gamma.data_ptr() if gamma is not None else None
+        qd.eps, qd.softmax_scale = eps, scale
+        gs = []
+        for n, m in groups:
+            g = ws_query_group()
+            g.n_q, g.mask = n, m
+            gs.append(g)
+        ws_unit_attention_groups(q.data_ptr(), q.stride(0), q.stride(1), gs, qd, self.handle,
+                                 out.data_ptr(), out.stride(0), out.stride(1), _stream_handle(stream))
+        return out
 
     def audio_attention(self, q, out, mask, mode=WS_APPEND_NORM_ROPE, positions=None,
                         gamma=None, eps=1e-6, scale=0.0, stream=None):

@@ -1,0 +1,144 @@
+"""Queries of several units in one call (ws_unit_attention_groups): each
+group of query rows attends under its own unit's block-causal mask (Fig. 1
+caption: block-causal attention on one timeline; Sec. 2.1: units committed
+into history), as in a catch-up after a stall.  Against the oracle's
+unit_attention_groups, and against one ws_unit_attention call per group."""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import assert_gates, bf16_f64, dev_f32, dev_i32, from_dev, to_dev
+from paper_2607_04443_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+VIDEO = (synth.KIND_COND, synth.KIND_VIDEO)
+
+
+def _build(ws, H, grid, cond, units, seed, max_q=4096):
+    """A cache with a cond slice and `units` committed video units (NORM_ROPE
+    keys), mirrored in an oracle cache."""
+    import torch
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + seed))
+    lu = grid[0] * grid[1]
+    cache = ws.Cache(H, cond // 64 + 2 + units * (-(-lu // 64)), max_q_tokens=max_q)
+    oc = oracle.OracleCache(num_heads=H)
+    g = dev_f32(np.ones(128, np.float32))
+    keep = [g]
+    ck, cv = synth.normal_bf16(rng, (cond, H, 128)), synth.normal_bf16(rng, (cond, H, 128))
+    dk, dv = to_dev(ck), to_dev(cv)
+    keep += [dk, dv]
+    cache.append(0, ws.WS_KIND_COND, dk, dv, ws.WS_APPEND_RAW)
+    oc.append(0, oracle.KIND_COND, ck, cv, oracle.MODE_RAW)
+    for u in range(units):
+        k, v = synth.normal_bf16(rng, (lu, H, 128)), synth.normal_bf16(rng, (lu, H, 128))
+        pos = synth.video_positions(u, grid)
+        dk, dv, dp = to_dev(k), to_dev(v), dev_i32(pos)
+        keep += [dk, dv, dp]
+        cache.append(u, ws.WS_KIND_VIDEO, dk, dv, ws.WS_APPEND_NORM_ROPE, dp, g, 1e-6)
+        oc.append(u, oracle.KIND_VIDEO, k, v, oracle.MODE_NORM_ROPE, pos, np.ones(128), 1e-6)
+        cache.commit(u)
+        oc.commit(u)
+    torch.cuda.synchronize()
+    return cache, oc, rng, keep
+
+
+def _queries(rng, H, spec, grid):
+    """spec: (q_unit, min_visible_unit, kind_mask, n_rows) per group."""
+    q = synth.normal_bf16(rng, (sum(s[3] for s in spec), H, 128))
+    # a group longer than the unit's grid repeats its positions
+    pos = np.concatenate([np.resize(synth.video_positions(s[0], grid), (s[3], 3)) for s in spec])
+    return q, pos
+
+
+def _run_groups(ws, cache, q, pos, spec, H):
+    import torch
+    dq, dp = to_dev(q), dev_i32(pos)
+    g = dev_f32(np.ones(128, np.float32))
+    out = torch.full_like(dq, float("nan"))
+    groups = [(n, ws.mask_spec(u, mn, [k for k in range(3) if (km >> k) & 1])) for u, mn, km, n in spec]
+    cache.unit_attention_groups(dq, out, groups, ws.WS_APPEND_NORM_ROPE, dp, g, 1e-6)
+    torch.cuda.synchronize()
+    return from_dev(out)
+
+
+def test_catch_up_three_units_and_an_empty_group(ws):
+    """Rows of units 7, 8 and 9 (920 each, each with its own 8-unit window)
+    and a group that sees nothing, over a cond slice and 10 units."""
+    H, grid = 8, (23, 40)
+    cache, oc, rng, keep = _build(ws, H, grid, 256, 10, 51)
+    try:
+        spec = [(7, -1, 0b011, 920), (8, 0, 0b011, 920), (3, 5, 0b010, 40), (9, 1, 0b011, 920)]
+        q, pos = _queries(rng, H, spec, grid)
+        got = bf16_f64(_run_groups(ws, cache, q, pos, spec, H))
+        ref, _ = oracle.unit_attention_groups(oc, q, spec, positions=pos, gamma=np.ones(128), eps=1e-6)
+        assert (got[1840:1880] == 0).all()
+        for lo, hi, lab in ((0, 920, "unit 7"), (920, 1840, "unit 8"), (1880, 2800, "unit 9")):
+            print(lab, assert_gates(got[lo:hi], ref[lo:hi], label=f"catch-up {lab}"))
+    finally:
+        cache.close()
+
+
+def test_groups_equal_separate_calls_with_one_range_per_head(ws):
+    """With one key range per head (forced), every group's rows are computed
+    exactly as a ws_unit_attention call of that group alone: bit for bit."""
+    import torch
+    H, grid = 4, (5, 7)
+    cache, oc, rng, keep = _build(ws, H, grid, 10, 6, 52)
+    try:
+        cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, 1)
+        spec = [(2, -1, 0b011, 35), (5, 3, 0b011, 300), (0, -1, 0b001, 7), (4, 2, 0b010, 35)]
+        q, pos = _queries(rng, H, spec, grid)
+        got = _run_groups(ws, cache, q, pos, spec, H)
+        g = dev_f32(np.ones(128, np.float32))
+        r0 = 0
+        for u, mn, km, n in spec:
+            dq, dp = to_dev(q[r0:r0 + n]), dev_i32(pos[r0:r0 + n])
+            out = torch.full_like(dq, float("nan"))
+            cache.unit_attention(dq, out, ws.mask_spec(u, mn, [k for k in range(3) if (km >> k) & 1]),
+                                 ws.WS_APPEND_NORM_ROPE, dp, g, 1e-6)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(got[r0:r0 + n], from_dev(out), err_msg=str((u, mn, km, n)))
+            r0 += n
+    finally:
+        cache.close()
+
+
+@pytest.mark.parametrize("splits", [0, 3])
+def test_ragged_groups_against_oracle(ws, splits):
+    """Group sizes that end inside query tiles (1, 33, 257, 128) and a group
+    whose window hides all but the conditioning slice, with the automatic and
+    a forced key-range split, against the oracle."""
+    H, grid = 4, (5, 7)
+    cache, oc, rng, keep = _build(ws, H, grid, 10, 6, 53)
+    try:
+        if splits:
+            cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, splits)
+        spec = [(5, -1, 0b011, 1), (3, 2, 0b011, 33), (5, 9, 0b011, 257), (1, -1, 0b011, 128)]
+        q, pos = _queries(rng, H, spec, grid)
+        got = bf16_f64(_run_groups(ws, cache, q, pos, spec, H))
+        ref, _ = oracle.unit_attention_groups(oc, q, spec, positions=pos, gamma=np.ones(128), eps=1e-6)
+        print(assert_gates(got, ref, label=f"ragged groups, splits={splits}"))
+    finally:
+        cache.close()
+
+
+def test_group_argument_errors(ws):
+    import torch
+    H, grid = 2, (5, 7)
+    cache, oc, rng, keep = _build(ws, H, grid, 10, 2, 54, max_q=64)
+    try:
+        dq = to_dev(synth.normal_bf16(rng, (70, H, 128)))
+        out = torch.zeros_like(dq)
+        m = ws.mask_spec(1)
+        cases = [([], ws.WS_ERR_INVALID_ARG), ([(1, m)] * 9, ws.WS_ERR_INVALID_ARG),
+                 ([(0, m), (0, m)], ws.WS_ERR_SHAPE), ([(40, m), (30, m)], ws.WS_ERR_SHAPE),
+                 ([(-1, m), (2, m)], ws.WS_ERR_SHAPE)]
+        for groups, status in cases:
+            with pytest.raises(ws.WsError) as e:
+                cache.unit_attention_groups(dq, out, groups, ws.WS_APPEND_RAW)
+            assert e.value.status == status, (groups, e.value)
+        torch.cuda.synchronize()
+        assert (from_dev(out) == 0).all()
+    finally:
+        cache.close()
