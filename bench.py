@@ -249,6 +249,60 @@ def cold_audio(args, ws, sets, vpos, apos, gamma, eps, stream, dev, cond):
             "gbps": nbytes / (med * 1e-6) / 1e9, "frac_hbm": nbytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBS}
 
 
+def catch_up(args, ws, sets, vpos, gamma, eps, stream, dev, n_units=3):
+    """Catch-up after a stall: the queries of n_units consecutive 920-token
+    units in one ws_unit_attention_groups call, each unit under its own
+    8-unit window (256 + 9 x 920 = 8536 keys per unit), against the same work
+    as one ws_unit_attention call per unit.  Queries prepared beforehand;
+    medians of `long_reps` repetitions (events around the call(s))."""
+    import torch
+    first = HIST
+    cache = ws.Cache(H, 4 + (HIST + n_units + 1) * 16, max_q_tokens=LU * n_units)
+    s0 = sets[0]
+    cache.append(0, ws.WS_KIND_COND, s0["ck"], s0["cv"], ws.WS_APPEND_RAW)
+    for u in range(first + n_units):
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.commit(u)
+    q_all = torch.empty((LU * n_units, H, D), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q_all)
+    cache.step_append([], [dict(q=sets[i % 2]["q"], q_out=q_all[i * LU:(i + 1) * LU],
+                                positions=vpos[first + i], gamma=gamma, eps=eps) for i in range(n_units)])
+    masks = [ws.mask_spec(first + i, first + i - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
+             for i in range(n_units)]
+    groups = [(LU, m) for m in masks]
+
+    def one_call():
+        cache.unit_attention_groups(q_all, out, groups, ws.WS_QUERY_PREPARED)
+
+    def separate():
+        for i, m in enumerate(masks):
+            cache.unit_attention(q_all[i * LU:(i + 1) * LU], out[i * LU:(i + 1) * LU], m,
+                                 ws.WS_QUERY_PREPARED)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        t = []
+        for _ in range(max(args.long_reps, 1)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            t.append(a.elapsed_time(b) * 1e3)
+        t.sort()
+        return t[len(t) // 2]
+
+    t1, t3 = timed(one_call), timed(separate)
+    cache.close()
+    lk = COND + (HIST + 1) * LU
+    flop = n_units * video_flop(LU, lk)
+    return {"units": n_units, "queries": LU * n_units, "keys_per_unit": lk, "flop": flop,
+            "us": t1, "tflops": flop / (t1 * 1e-6) / 1e12, "us_separate_calls": t3,
+            "tflops_separate_calls": flop / (t3 * 1e-6) / 1e12}
+
+
 COPY_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "unit_attn_traffic.md")
 KERNELS_SRC = os.path.join(ROOT, "paper_2607_04443_amd", "csrc", "kernels.hip")
@@ -560,6 +614,7 @@ def main():
         cold_256 = cold_audio(args, ws, sets, vpos, apos, gamma, eps, stream, dev, COND)
 
     long_hist = long_history(args, ws, sets, gamma, eps, stream, dev) if args.long_reps > 0 else None
+    catch = catch_up(args, ws, sets, vpos, gamma, eps, stream, dev) if args.long_reps > 0 else None
     peaks = measured_peaks(ws, torch, stream, dev) if args.peak_probes else None
 
     t_vkern, t_vmerge = kernel_us("video", "attn_us"), kernel_us("video", "merge_us")
@@ -593,6 +648,7 @@ def main():
                             "cold_cond256": cold_256},
         "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
         "long_history": long_hist,
+        "catch_up": catch,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic()},

@@ -69,6 +69,7 @@ def _load():
         lib.ws_oracle_lse_merge.argtypes = [_dp, _dp, ctypes.c_int64, ctypes.c_int64,
                                             ctypes.c_int64, _dp, _dp]
         lib.ws_oracle_num_threads.restype = ctypes.c_int
+        lib.ws_oracle_bf16_round.argtypes = [_dp, ctypes.c_int64, ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -94,6 +95,14 @@ def bf16_decode(bits) -> np.ndarray:
     b = np.ascontiguousarray(bits, dtype=np.uint16)
     out = np.empty(b.shape, dtype=np.float64)
     _load().ws_oracle_bf16_decode(b.ctypes.data, b.size, _ptr(out))
+    return out
+
+
+def bf16_round(x) -> np.ndarray:
+    """float64 values -> bf16 bit patterns, one rounding to nearest (ties to even)."""
+    x = _f64(x)
+    out = np.empty(x.shape, dtype=np.uint16)
+    _load().ws_oracle_bf16_round(_ptr(x), x.size, out.ctypes.data)
     return out
 
 
@@ -319,3 +328,47 @@ def unit_attention(cache: OracleCache, q_bits, q_unit, *, mode=MODE_NORM_ROPE, p
         out[:, hi, :] = o
         lse[hi] = l
     return out, lse
+
+
+# --------------------------------------------------------------------------- #
+# The attention sub-block of one performer layer at one denoising step
+# --------------------------------------------------------------------------- #
+def block_step(cache: OracleCache, x_bits, n_video, w_qkv_bits, w_out_bits, unit, *,
+               video_positions, audio_positions, gamma_q, gamma_k, eps, video_mask, audio_mask):
+    """The performer's attention sub-block for one unit at one denoising step
+    (Sec. 3: the performer generates the next unit conditioned on the K/V
+    cache, and writes the unit's own K/V into it each step):
+
+      [Q | K | V] = X W_qkv        (X [n, hidden]: the unit's n_video video then
+                                     audio tokens; columns head-major, 128 per head)
+      Q, K, V rounded to bf16 (the tensors the cache append and the attention take)
+      the unit's video and audio K/V appended (RMS-norm + rotary on K), with
+        the same rewrite rule as OracleCache.append
+      O = attention of the video rows (video_mask) and audio rows (audio_mask)
+      Y = O W_out                   (float64, O not rounded)
+
+    video_mask / audio_mask: (min_visible_unit, kind_mask) of each query set;
+    both query sets belong to `unit`.  Mutates the cache (the append).
+    Returns (Y [n, hidden], O [n, H, 128]) in float64."""
+    x = bf16_decode(x_bits)
+    n, hidden = x.shape
+    H = hidden // cache.head_dim
+    qkv = x @ bf16_decode(w_qkv_bits)
+    qkv_bits = bf16_round(qkv).reshape(n, 3, H, cache.head_dim)
+    q, k, v = qkv_bits[:, 0], qkv_bits[:, 1], qkv_bits[:, 2]
+    n_audio = n - n_video
+    cache.append(unit, KIND_VIDEO, k[:n_video], v[:n_video], MODE_NORM_ROPE, video_positions,
+                 gamma_k, eps)
+    if n_audio:
+        cache.append(unit, KIND_AUDIO, k[n_video:], v[n_video:], MODE_NORM_ROPE, audio_positions,
+                     gamma_k, eps)
+    o = np.zeros((n, H, cache.head_dim))
+    o[:n_video], _ = unit_attention(cache, q[:n_video], unit, positions=video_positions,
+                                    gamma=gamma_q, eps=eps, min_visible_unit=video_mask[0],
+                                    kind_mask=video_mask[1])
+    if n_audio:
+        o[n_video:], _ = unit_attention(cache, q[n_video:], unit, positions=audio_positions,
+                                        gamma=gamma_q, eps=eps, min_visible_unit=audio_mask[0],
+                                        kind_mask=audio_mask[1])
+    y = o.reshape(n, hidden) @ bf16_decode(w_out_bits)
+    return y, o

@@ -164,3 +164,24 @@ WS_ORACLE_API void ws_oracle_lse_merge(const double* o_parts, const double* lse_
     if (lse) lse[i] = M + log(wsum);
   }
 }
+
+/* Round n doubles to the nearest bfloat16 (8 significant bits, ties to
+ * even), returned as bf16 bit patterns (the upper half of the binary32 with
+ * the same value).  The rounding is taken once, from the double itself:
+ * x = m * 2^e with m in [0.5, 1), m * 2^8 rounded to the nearest integer
+ * (ties to even, the default rounding mode of rint), scaled back.  Finite
+ * values inside the normal binary32 range only (the block step's products). */
+WS_ORACLE_API void ws_oracle_bf16_round(const double* x, int64_t n, uint16_t* out) {
+  for (int64_t i = 0; i < n; ++i) {
+    double r = 0.0;
+    if (x[i] != 0.0) {
+      int e;
+      double m = frexp(x[i], &e);
+      r = ldexp(rint(ldexp(m, 8)), e - 8);
+    }
+    float f = (float)r; /* exact: r has 8 significant bits */
+    uint32_t bits;
+    memcpy(&bits, &f, sizeof bits);
+    out[i] = (uint16_t)(bits >> 16);
+  }
+}

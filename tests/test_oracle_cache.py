@@ -211,3 +211,73 @@ def test_groups_match_per_row_visibility_matrix():
         q = oracle.query_prologue(qb[:, h], oracle.MODE_NORM_ROPE, qpos, np.ones(D), 1e-6)
         o, _ = oracle.attention(q, k, v, 1.0 / math.sqrt(D), visible=vis)
         np.testing.assert_allclose(out[:, h], o, rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------- #
+# the attention sub-block of one performer layer (projections around the attention)
+# --------------------------------------------------------------------------- #
+def test_block_step_with_selection_weights_reduces_to_attention():
+    """With W_qkv = [I I I] (Q = K = V = X, head h in columns 128 h ..) and
+    W_out = I, the sub-block's output is the unit attention of X's bits used
+    as Q, K and V: the projection's column layout, the bf16 rounding of its
+    output (exact here), the append and the two query sets are pinned by the
+    already-pinned unit attention."""
+    rng = np.random.default_rng(11)
+    H, D, nv, na = 2, 128, 5, 2
+    hid, n = H * D, nv + na
+    x = synth.normal_bf16(rng, (n, hid))
+    w3 = oracle.bf16_round(np.concatenate([np.eye(hid)] * 3, axis=1))
+    w_out = oracle.bf16_round(np.eye(hid))
+    kc, vc = synth.normal_bf16(rng, (3, H, D)), synth.normal_bf16(rng, (3, H, D))
+    vpos, apos = synth.video_positions(1, (1, nv)), synth.audio_positions(1, na)
+    g = np.ones(D)
+
+    def fresh():
+        c = oracle.OracleCache(num_heads=H)
+        c.append(0, oracle.KIND_COND, kc, vc, oracle.MODE_RAW)
+        return c
+
+    y, o = oracle.block_step(fresh(), x, nv, w3, w_out, 1, video_positions=vpos,
+                             audio_positions=apos, gamma_q=g, gamma_k=g, eps=1e-6,
+                             video_mask=(-(2 ** 31), 0b011), audio_mask=(-(2 ** 31), 0b111))
+    c2 = fresh()
+    xb = x.reshape(n, H, D)
+    c2.append(1, oracle.KIND_VIDEO, xb[:nv], xb[:nv], oracle.MODE_NORM_ROPE, vpos, g, 1e-6)
+    c2.append(1, oracle.KIND_AUDIO, xb[nv:], xb[nv:], oracle.MODE_NORM_ROPE, apos, g, 1e-6)
+    ov, _ = oracle.unit_attention(c2, xb[:nv], 1, positions=vpos, gamma=g, kind_mask=0b011)
+    oa, _ = oracle.unit_attention(c2, xb[nv:], 1, positions=apos, gamma=g, kind_mask=0b111)
+    np.testing.assert_allclose(o, np.concatenate([ov, oa]), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(y, np.concatenate([ov, oa]).reshape(n, hid), rtol=0, atol=1e-12)
+
+
+def test_block_step_projections_are_linear():
+    """Y scales with W_out (Y(2 W_out) = 2 Y(W_out), exact in binary), and a
+    zero W_qkv makes every logit zero: O is then the plain mean of the values
+    each query set sees, i.e. of the conditioning values only (the unit's own
+    values are zero) weighted by their count."""
+    rng = np.random.default_rng(12)
+    H, D, nv, na = 2, 128, 4, 1
+    hid, n = H * D, 5
+    x = synth.normal_bf16(rng, (n, hid))
+    w_qkv = synth.bf16_bits(rng.standard_normal((hid, 3 * hid)).astype(np.float32) / 16)
+    w_out = synth.bf16_bits(rng.standard_normal((hid, hid)).astype(np.float32) / 16)
+    w_out2 = oracle.bf16_round(2.0 * oracle.bf16_decode(w_out))
+    kc, vc = synth.normal_bf16(rng, (3, H, D)), synth.normal_bf16(rng, (3, H, D))
+    vpos, apos = synth.video_positions(0, (1, nv)), synth.audio_positions(0, na)
+    g = np.ones(D)
+    kw = dict(video_positions=vpos, audio_positions=apos, gamma_q=g, gamma_k=g, eps=1e-6,
+              video_mask=(-(2 ** 31), 0b011), audio_mask=(-(2 ** 31), 0b111))
+    outs = []
+    for w in (w_out, w_out2):
+        c = oracle.OracleCache(num_heads=H)
+        c.append(0, oracle.KIND_COND, kc, vc, oracle.MODE_RAW)
+        outs.append(oracle.block_step(c, x, nv, w_qkv, w, 0, **kw)[0])
+    np.testing.assert_allclose(outs[1], 2.0 * outs[0], rtol=1e-14, atol=1e-14)
+    c = oracle.OracleCache(num_heads=H)
+    c.append(0, oracle.KIND_COND, np.zeros_like(kc), vc, oracle.MODE_RAW)
+    _, o = oracle.block_step(c, x, nv, np.zeros_like(w_qkv), w_out, 0, **kw)
+    vcond = oracle.bf16_decode(vc)
+    np.testing.assert_allclose(o[:nv], np.broadcast_to(vcond.sum(0) / (3 + nv), (nv, H, D)),
+                               rtol=0, atol=1e-12)
+    np.testing.assert_allclose(o[nv:], np.broadcast_to(vcond.sum(0) / (3 + nv + na), (na, H, D)),
+                               rtol=0, atol=1e-12)

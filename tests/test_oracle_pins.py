@@ -350,3 +350,23 @@ def test_planted_mistakes(plant):
         except AssertionError:
             failed.append(pin.__name__)
     assert failed, f"planted mistake {plant} passed every pin"
+
+
+# --------------------------------------------------------------------------- #
+# bf16 rounding of float64 values, and the attention sub-block
+# --------------------------------------------------------------------------- #
+def test_bf16_round_exact_values():
+    """Ties to even and ordinary rounding at 8 significant bits, exact powers
+    of two and signs, against hand-worked bit patterns; and agreement with
+    the two-step float32 path where float32 holds the value exactly."""
+    cases = [(1.0, 0x3F80), (1.0 + 2 ** -8, 0x3F80), (1.0 + 3 * 2 ** -8, 0x3F82),
+             (1.0 + 2 ** -8 + 2 ** -30, 0x3F81), (-2.0, 0xC000), (0.0, 0x0000),
+             (1.5 * 2 ** -100, 0x0DC0), (255.0, 0x437F), (255.5, 0x4380), (256.5, 0x4380),
+             (257.0, 0x4380), (259.0, 0x4382)]
+    got = oracle.bf16_round(np.array([c[0] for c in cases]))
+    assert [int(g) for g in got] == [c[1] for c in cases], [hex(int(g)) for g in got]
+    rng = np.random.default_rng(7)
+    f = rng.standard_normal(4096).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    want = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    np.testing.assert_array_equal(oracle.bf16_round(f.astype(np.float64)), want)
