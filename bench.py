@@ -303,6 +303,86 @@ def catch_up(args, ws, sets, vpos, gamma, eps, stream, dev, n_units=3):
             "tflops_separate_calls": flop / (t3 * 1e-6) / 1e12}
 
 
+def block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev, steps=50, warmup=20):
+    """The attention sub-block of one performer layer per unit at 640x368
+    (ws_block_step: QKV projection [924 x 5120] x [5120 x 15360], the unit's
+    K/V append and query preparation, video and audio attention over the
+    8-unit window, output projection [924 x 5120] x [5120 x 5120]), at steady
+    state: each step is a new unit, committed and evicted as in the main
+    loop.  Random weights (N(0, 1/5120) in bf16): timing only.  Events
+    around `steps` steps, and the library's per-launch timing ring for the
+    breakdown."""
+    import numpy as np
+    import torch
+    from paper_2607_04443_amd import synth
+    hid = H * D
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 5))
+
+    def dev_w(shape):
+        w = rng.standard_normal(shape, dtype=np.float32) / np.sqrt(hid)
+        return torch.from_numpy(synth.bf16_bits(w).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    w_qkv, w_out = dev_w((hid, 3 * hid)), dev_w((hid, hid))
+    x = torch.from_numpy(synth.normal_bf16(rng, (LU + AUDIO, hid)).view(np.int16)).view(torch.bfloat16).to(dev)
+    y = torch.empty_like(x)
+    cache = ws.Cache(H, 4 + (HIST + 2) * 16 + 8, max_q_tokens=1024)
+    s0 = sets[0]
+    cache.append(0, ws.WS_KIND_COND, s0["ck"], s0["cv"], ws.WS_APPEND_RAW)
+    for u in range(HIST):
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, eps)
+        cache.append(u, ws.WS_KIND_AUDIO, s["ka"], s["va"], ws.WS_APPEND_NORM_ROPE, apos[u], gamma, eps)
+        cache.commit(u)
+    block = ws.Block(cache, w_qkv, w_out, max_rows=LU + AUDIO)
+    u = HIST
+
+    def one(u):
+        block.step(x, LU, u, vpos[u], apos[u], gamma, gamma, y,
+                   ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
+                   ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO)),
+                   eps=eps)
+        cache.commit(u)
+        cache.evict_before(u - HIST + 1)
+
+    for _ in range(warmup):
+        one(u)
+        u += 1
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        one(u)
+        u += 1
+    b.record(stream)
+    b.synchronize()
+    us = a.elapsed_time(b) * 1e3 / steps
+    cache.timing_enable(8 * steps)
+    for _ in range(steps):
+        one(u)
+        u += 1
+    torch.cuda.synchronize()
+    rec = cache.timing_read()
+    cache.timing_enable(0)
+    block.close()
+    cache.close()
+
+    def avg(path, key="attn_us"):
+        v = [r[key] for r in rec if r["path"] == path]
+        return sum(v) / len(v) if v else None
+
+    rows = LU + AUDIO
+    f_qkv, f_out = 2.0 * rows * hid * 3 * hid, 2.0 * rows * hid * hid
+    t_qkv, t_out = avg("qkv_gemm"), avg("out_gemm")
+    t_app, t_vid, t_aud = avg("append"), avg("video"), avg("audio")
+    t_merge = avg("audio", "merge_us")
+    attn_us = t_app + t_vid + t_aud + t_merge
+    return {"us_per_step": us, "rows": rows, "hidden": hid,
+            "qkv_gemm_us": t_qkv, "qkv_gemm_tflops": f_qkv / (t_qkv * 1e-6) / 1e12,
+            "out_gemm_us": t_out, "out_gemm_tflops": f_out / (t_out * 1e-6) / 1e12,
+            "append_us": t_app, "video_kernel_us": t_vid, "audio_kernel_us": t_aud, "merge_us": t_merge,
+            "attention_share": attn_us / (attn_us + t_qkv + t_out)}
+
+
 COPY_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "unit_attn_traffic.md")
 KERNELS_SRC = os.path.join(ROOT, "paper_2607_04443_amd", "csrc", "kernels.hip")
@@ -503,7 +583,7 @@ def main():
     sets = [dict(ck=dev_bf16((COND, H, D)), cv=dev_bf16((COND, H, D)), k=dev_bf16((LU, H, D)),
                  v=dev_bf16((LU, H, D)), ka=dev_bf16((AUDIO, H, D)), va=dev_bf16((AUDIO, H, D)),
                  q=dev_bf16((LU, H, D)), qa=dev_bf16((AUDIO, H, D))) for _ in range(2)]
-    last_unit = HIST + n_steps_total + args.steps + 2
+    last_unit = HIST + max(n_steps_total + args.steps, 130) + 2
     vpos = [torch.from_numpy(synth.video_positions(u, GRID)).to(dev) for u in range(last_unit + 1)]
     apos = [torch.from_numpy(synth.audio_positions(u, AUDIO)).to(dev) for u in range(last_unit + 1)]
     out_v = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
@@ -615,6 +695,7 @@ def main():
 
     long_hist = long_history(args, ws, sets, gamma, eps, stream, dev) if args.long_reps > 0 else None
     catch = catch_up(args, ws, sets, vpos, gamma, eps, stream, dev) if args.long_reps > 0 else None
+    block = block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev) if args.long_reps > 0 else None
     peaks = measured_peaks(ws, torch, stream, dev) if args.peak_probes else None
 
     t_vkern, t_vmerge = kernel_us("video", "attn_us"), kernel_us("video", "merge_us")
@@ -649,6 +730,7 @@ def main():
         "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
         "long_history": long_hist,
         "catch_up": catch,
+        "block_step": block,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic()},

@@ -343,6 +343,64 @@ WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, c
 WS_API ws_status ws_step_attention_noalloc(ws_cache* cache, const ws_attn_call* video,
                                            const ws_attn_call* audio, void* hip_stream);
 
+/* The attention sub-block of one performer layer at one denoising step
+ * (Sec. 3: the performer generates the next unit conditioned on its K/V
+ * cache and writes the unit's own K/V into it; the whole performer step and
+ * the K/V and latent transfers must fit one 160 ms unit).  A ws_block holds
+ * the layer's two projection weights and the buffers of one step:
+ *   [Q | K | V] = X W_qkv   (hipBLASLt GEMM, bf16 in and out, fp32 accumulation)
+ *   ws_step_append: the unit's video and audio K/V (NORM_ROPE) and the
+ *                   preparation of both query sets
+ *   ws_step_attention (or ws_unit_attention without audio rows)
+ *   Y = O W_out             (hipBLASLt GEMM)
+ * X holds the unit's n_video video tokens followed by its n_audio audio
+ * tokens.  Column block j of W_qkv (j = 0 Q, 1 K, 2 V) holds columns
+ * [j hidden, (j + 1) hidden), head h in its columns 128 h .. 128 h + 127.
+ * The weights are random here: the call measures the time of the sub-block
+ * and the share of attention in it. */
+typedef struct ws_block ws_block; /* opaque; owned by the library */
+
+/* Creates a block over `cache` (hidden = 128 * num_heads of the cache):
+ *   w_qkv: device bf16 [hidden][3 hidden] row-major; w_out: device bf16
+ *   [hidden][hidden] row-major; both 16-byte aligned, owned by the caller and
+ *   kept alive and unchanged while the block is used;
+ *   max_rows: most tokens (n_video + n_audio) a step takes, 1..max_q_tokens.
+ * Allocates the GEMM workspace (64 MiB) and the step's Q/K/V, prepared-query
+ * and attention buffers (max_rows rows); ws_block_step allocates nothing.
+ * The cache must outlive the block.  Synchronous. */
+WS_API ws_status ws_block_create(ws_cache* cache, const void* w_qkv, const void* w_out, int32_t max_rows,
+                                 ws_block** out);
+
+/* Waits for the device, then frees what the block owns.  NULL is a no-op. */
+WS_API ws_status ws_block_destroy(ws_block* block);
+
+typedef struct ws_block_step_args {
+  const void* x;              /* device bf16 [n_video + n_audio][hidden], rows contiguous */
+  int32_t n_video;            /* >= 1 */
+  int32_t n_audio;            /* 0..64 */
+  int32_t unit;               /* the unit the tokens belong to (the K/V append's unit) */
+  const int32_t* video_positions;  /* device int32 [n_video][3] */
+  const int32_t* audio_positions;  /* device int32 [n_audio][3] (NULL when n_audio = 0) */
+  const float* gamma_q;       /* device fp32 [128] */
+  const float* gamma_k;       /* device fp32 [128] */
+  float eps;
+  float softmax_scale;        /* 0 selects 1/sqrt(128) */
+  ws_mask_spec video_mask;    /* visibility of the video rows (q_unit = unit) */
+  ws_mask_spec audio_mask;    /* visibility of the audio rows */
+  void* attn_out;             /* optional device bf16 [n][hidden]: the attention output O
+                                 (NULL: kept inside the block) */
+  void* y;                    /* device bf16 [n][hidden], rows contiguous */
+} ws_block_step_args;
+
+/* One sub-block step on hip_stream, in the order above.  The append follows
+ * the rules of ws_kv_append (a first step of a unit takes pages, later steps
+ * rewrite them; committed units are rejected); arguments, pages and the
+ * rewrite rule are checked before anything is enqueued.  With timing enabled
+ * the two projections record ring entries of their own (path 3: QKV
+ * projection, path 4: output projection), besides the append and attention
+ * entries.  args: host struct, read before the call returns. */
+WS_API ws_status ws_block_step(ws_block* block, const ws_block_step_args* args, void* hip_stream);
+
 /* Debug read-back of one segment in logical order: k_host and v_host receive
  * bf16 [n_tokens][H][128] (contiguous host buffers owned by the caller).
  * Waits for the device.  k_host or v_host may be NULL to skip it. */
@@ -378,7 +436,8 @@ WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t val
  * The cache keeps the events of the last `capacity` calls in a ring (older
  * calls are overwritten); recording adds no synchronization. */
 typedef struct ws_call_timing {
-  int32_t path;      /* 0 = video attention, 1 = audio attention, 2 = append */
+  int32_t path;      /* 0 = video attention, 1 = audio attention, 2 = append,
+                        3 = QKV projection, 4 = output projection (ws_block_step) */
   int32_t n_splits;  /* audio: key-range splits; video: workgroup groups; append: items */
   float attn_us;     /* attention kernel, microseconds */
   float merge_us;    /* merge kernel, microseconds (0 when there is none) */

@@ -1,7 +1,8 @@
 """Build of the native libraries, in-tree.
 
   libws.so       the product: HIP kernels for gfx950 (kernels.hip; peaks.hip holds
-                 the calibration probes) + the C ABI (hipcc)
+                 the calibration probes) + the C ABI (hipcc); block.cpp links
+                 hipBLASLt for the projections around the attention
   libws_host.so  host-only page-table entry points for CPU tests (g++)
 """
 import os
@@ -17,7 +18,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libws.so")
 HOST_LIB_PATH = os.path.join(PKG, "libws_host.so")
 
-HIP_SOURCES = ["kernels.hip", "peaks.hip", "ws_api.cpp", "pagetable.cpp"]
+HIP_SOURCES = ["kernels.hip", "peaks.hip", "ws_api.cpp", "pagetable.cpp", "block.cpp"]
+# hipBLASLt runs the two projections of ws_block_step (plain GEMMs)
+LINK_FLAGS = ["-L/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib", "-lhipblaslt"]
 # Packed fp32 ops are kept out of the generated code on purpose.  The kernels
 # never form NaNs from finite inputs (masked logits are -inf, and no -inf - -inf
 # is evaluated), so NaN-quieting canonicalisations are not needed.
@@ -59,7 +62,7 @@ def build(verbose=False):
     with ThreadPoolExecutor(max_workers=4) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
     tmp = LIB_PATH + ".tmp"
-    _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs, verbose)
+    _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs + LINK_FLAGS, verbose)
     os.replace(tmp, LIB_PATH)
     os.replace(host_tmp, HOST_LIB_PATH)
     return LIB_PATH

@@ -17,11 +17,14 @@
 
 #include "pagetable.hpp"
 #include "ws.h"
+#include "ws_internal.hpp"
 #include "ws_kernels.hpp"
 
-namespace {
+namespace ws_internal {
 
+namespace {
 thread_local std::string g_last_error;
+}  // namespace
 
 ws_status fail(ws_status st, const char* fmt, ...) {
   char buf[512];
@@ -36,6 +39,15 @@ ws_status fail(ws_status st, const char* fmt, ...) {
 ws_status hip_fail(hipError_t e, const char* what) {
   return fail(WS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+
+const char* last_error() { return g_last_error.c_str(); }
+
+}  // namespace ws_internal
+
+namespace {
+
+using ws_internal::fail;
+using ws_internal::hip_fail;
 
 #define WS_HIP(call)                                  \
   do {                                                \
@@ -112,6 +124,53 @@ struct ws_cache {
 
   ws_cache(int32_t page_tokens, int32_t max_pages) : pt(page_tokens, max_pages) {}
 };
+
+namespace ws_internal {
+
+// Timing ring slot of the next call (or -1), with its first event recorded.
+ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot) {
+  TimingRing& tr = c->timing;
+  *slot = tr.cap > 0 ? tr.next : -1;
+  if (*slot >= 0) {
+    tr.meta[*slot] = ws_call_timing{path, splits, 0.f, 0.f};
+    WS_HIP(hipEventRecord(tr.ev[3 * *slot], stream));
+    tr.next = (tr.next + 1) % tr.cap;
+    tr.count = std::min(tr.count + 1, tr.cap);
+  }
+  return WS_OK;
+}
+
+ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream) {
+  if (slot >= 0) WS_HIP(hipEventRecord(c->timing.ev[3 * slot + k], stream));
+  return WS_OK;
+}
+
+int32_t cache_heads(const ws_cache* c) { return c->cfg.num_heads; }
+int32_t cache_max_q(const ws_cache* c) { return c->cfg.max_q_tokens; }
+int32_t free_pages(const ws_cache* c) { return c->pt.free_pages(); }
+
+ws_status precheck_append(const ws_cache* c, int32_t unit, ws_kind kind, int32_t n_tokens,
+                          int32_t* pages_needed) {
+  const ws::Segment* seg = c->pt.find(unit, kind);
+  if (!seg) {
+    *pages_needed += (n_tokens + ws::kPageTokens - 1) / ws::kPageTokens;
+    if (*pages_needed > c->pt.free_pages())
+      return fail(WS_ERR_OUT_OF_PAGES, "pool has %d free pages, the step needs %d", c->pt.free_pages(),
+                  *pages_needed);
+    return WS_OK;
+  }
+  if (seg->committed)
+    return fail(WS_ERR_COMMITTED, "unit %d kind %d is committed history", unit, static_cast<int>(kind));
+  if (seg->n_tokens != n_tokens)
+    return fail(WS_ERR_SHAPE, "rewrite of unit %d kind %d with %d tokens (segment has %d)", unit,
+                static_cast<int>(kind), n_tokens, seg->n_tokens);
+  return WS_OK;
+}
+
+}  // namespace ws_internal
+
+using ws_internal::timing_begin_path;
+using ws_internal::timing_mark;
 
 namespace {
 
@@ -564,27 +623,11 @@ hipError_t launch_plan_kernel(const AttnPlan& p, hipStream_t stream) {
   return p.audio ? ws::launch_audio_attention(p.a, stream) : ws::launch_unit_attention(p.a, stream);
 }
 
-// Timing ring slot of the next call (or -1), with its first event recorded.
-ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot) {
-  TimingRing& tr = c->timing;
-  *slot = tr.cap > 0 ? tr.next : -1;
-  if (*slot >= 0) {
-    tr.meta[*slot] = ws_call_timing{path, splits, 0.f, 0.f};
-    WS_HIP(hipEventRecord(tr.ev[3 * *slot], stream));
-    tr.next = (tr.next + 1) % tr.cap;
-    tr.count = std::min(tr.count + 1, tr.cap);
-  }
-  return WS_OK;
-}
 
 ws_status timing_begin(ws_cache* c, const AttnPlan& p, hipStream_t stream, int* slot) {
   return timing_begin_path(c, p.audio ? 1 : 0, p.splits, stream, slot);
 }
 
-ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream) {
-  if (slot >= 0) WS_HIP(hipEventRecord(c->timing.ev[3 * slot + k], stream));
-  return WS_OK;
-}
 
 ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_t q_head_stride,
                          int32_t n_groups, const QueryGroup* groups, const ws_query_desc* qd, ws_cache* c,
@@ -1146,6 +1189,6 @@ ws_status ws_probe_read(const void* buf, int64_t bytes, int32_t workgroups, uint
   return WS_OK;
 }
 
-const char* ws_last_error(void) { return g_last_error.c_str(); }
+const char* ws_last_error(void) { return ws_internal::last_error(); }
 
 }  // extern "C"

@@ -96,6 +96,15 @@ class ws_query_group(ctypes.Structure):
 WS_MAX_QUERY_GROUPS = 8
 
 
+class ws_block_step_args(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("n_video", ctypes.c_int32), ("n_audio", ctypes.c_int32),
+                ("unit", ctypes.c_int32), ("video_positions", ctypes.c_void_p),
+                ("audio_positions", ctypes.c_void_p), ("gamma_q", ctypes.c_void_p),
+                ("gamma_k", ctypes.c_void_p), ("eps", ctypes.c_float),
+                ("softmax_scale", ctypes.c_float), ("video_mask", ws_mask_spec),
+                ("audio_mask", ws_mask_spec), ("attn_out", ctypes.c_void_p), ("y", ctypes.c_void_p)]
+
+
 class ws_cache_stats(ctypes.Structure):
     _fields_ = [("pages_total", ctypes.c_int32), ("pages_free", ctypes.c_int32),
                 ("n_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
@@ -127,6 +136,9 @@ _SIGS = {
     "ws_step_attention": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_step_attention_noalloc": [_vp, _P(ws_attn_call), _P(ws_attn_call), _vp],
     "ws_cache_export": [_vp, _i32, _i32, _vp, _vp],
+    "ws_block_create": [_vp, _vp, _vp, _i32, _P(_vp)],
+    "ws_block_destroy": [_vp],
+    "ws_block_step": [_vp, _P(ws_block_step_args), _vp],
     "ws_segment_tokens": [_vp, _i32, _i32, _P(_i32)],
     "ws_segment_pages": [_vp, _i32, _i32, _P(_i32), _i32, _P(_i32)],
     "ws_cache_info": [_vp, _P(ws_cache_stats)],
@@ -236,6 +248,20 @@ def ws_step_attention(cache, video: ws_attn_call, audio: ws_attn_call, stream):
 def ws_step_attention_noalloc(cache, video: ws_attn_call, audio: ws_attn_call, stream):
     _check(_lib.ws_step_attention_noalloc(cache, ctypes.byref(video), ctypes.byref(audio), stream),
            "ws_step_attention_noalloc")
+
+
+def ws_block_create(cache, w_qkv, w_out, max_rows) -> int:
+    h = _vp()
+    _check(_lib.ws_block_create(cache, w_qkv, w_out, max_rows, ctypes.byref(h)), "ws_block_create")
+    return h.value
+
+
+def ws_block_destroy(block):
+    _check(_lib.ws_block_destroy(block), "ws_block_destroy")
+
+
+def ws_block_step(block, args: ws_block_step_args, stream):
+    _check(_lib.ws_block_step(block, ctypes.byref(args), stream), "ws_block_step")
 
 
 def ws_cache_export(cache, unit, kind, k_host, v_host):
@@ -508,9 +534,48 @@ class Cache:
         """Per-call launch timing recorded since the last read, oldest first:
         dicts with path ('video'/'audio'/'append'), n_splits, attn_us, merge_us."""
         out = ws_cache_timing_read(self.handle, getattr(self, "_timing_cap", 0))
-        names = {0: "video", 1: "audio", 2: "append"}
+        names = {0: "video", 1: "audio", 2: "append", 3: "qkv_gemm", 4: "out_gemm"}
         return [dict(path=names.get(t.path, str(t.path)), n_splits=t.n_splits, attn_us=t.attn_us,
                      merge_us=t.merge_us) for t in out]
+
+
+class Block:
+    """Owns one ws_block over a Cache: the attention sub-block of a performer
+    layer (QKV projection, append, attention, output projection)."""
+
+    def __init__(self, cache, w_qkv, w_out, max_rows):
+        import torch
+        for name, w in (("w_qkv", w_qkv), ("w_out", w_out)):
+            if not w.is_cuda or w.dtype != torch.bfloat16 or not w.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous bf16 device tensor")
+        self._keep = (cache, w_qkv, w_out)
+        self.handle = ws_block_create(cache.handle, w_qkv.data_ptr(), w_out.data_ptr(), max_rows)
+
+    def close(self):
+        if self.handle:
+            ws_block_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def step(self, x, n_video, unit, video_positions, audio_positions, gamma_q, gamma_k, y,
+             video_mask, audio_mask, eps=1e-6, scale=0.0, attn_out=None, stream=None):
+        """x, y (and attn_out): contiguous bf16 [n_video + n_audio, hidden] device tensors."""
+        a = ws_block_step_args()
+        a.x, a.n_video, a.n_audio, a.unit = x.data_ptr(), n_video, x.shape[0] - n_video, unit
+        a.video_positions = video_positions.data_ptr()
+        a.audio_positions = audio_positions.data_ptr() if audio_positions is not None else None
+        a.gamma_q, a.gamma_k = gamma_q.data_ptr(), gamma_k.data_ptr()
+        a.eps, a.softmax_scale = eps, scale
+        a.video_mask, a.audio_mask = video_mask, audio_mask
+        a.attn_out = attn_out.data_ptr() if attn_out is not None else None
+        a.y = y.data_ptr()
+        ws_block_step(self.handle, a, _stream_handle(stream))
+        return y
 
 
 def mask_spec(q_unit, min_visible_unit=INT32_MIN, kinds=(WS_KIND_COND, WS_KIND_VIDEO)):
