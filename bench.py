@@ -295,11 +295,15 @@ def catch_up(args, ws, sets, vpos, gamma, eps, stream, dev, n_units=3):
         return t[len(t) // 2]
 
     t1, t3 = timed(one_call), timed(separate)
+    cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, 1)
+    t1_shared = timed(one_call)
+    cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, 0)
     cache.close()
     lk = COND + (HIST + 1) * LU
     flop = n_units * video_flop(LU, lk)
     return {"units": n_units, "queries": LU * n_units, "keys_per_unit": lk, "flop": flop,
-            "us": t1, "tflops": flop / (t1 * 1e-6) / 1e12, "us_separate_calls": t3,
+            "us": t1, "tflops": flop / (t1 * 1e-6) / 1e12, "us_one_call_shared_round": t1_shared,
+            "us_separate_calls": t3,
             "tflops_separate_calls": flop / (t3 * 1e-6) / 1e12}
 
 

@@ -174,7 +174,11 @@ typedef enum ws_option {
   /* Softmax shift of the video kernel: 0 = automatic (a query row's logit
    * bound |q''| * max |k| when it is at most 40 in log2 units, else a lazily
    * raised running maximum), 1 = always the running maximum. */
-  WS_OPT_VIDEO_RUNNING_MAX = 2
+  WS_OPT_VIDEO_RUNNING_MAX = 2,
+  /* ws_unit_attention_groups: 0 = every query group is partitioned as if
+   * it had all CUs (several rounds of workgroups in one launch), 1 = the
+   * groups share one round of the CUs in proportion to their work. */
+  WS_OPT_VIDEO_CLASS_CUS = 3
 } ws_option;
 
 /* Creates a cache: allocates the K and V page pools (2 * max_pages * H * 64 *

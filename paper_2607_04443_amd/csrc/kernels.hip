@@ -1459,91 +1459,62 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
 }
 
 // ------------------------------------------------------------------------- //
-// combine: kGroups groups of 32 threads per (head, query) row, 4 d per thread.
-// Group g folds splits g, g + kGroups, ... with an online log-sum-exp; the
-// groups of a row then merge through LDS.  Many splits (audio) are read in
-// parallel; few splits with many rows (video) use one group per row.
+// combine (audio key ranges): 16 threads per (head, query) row, 8 d each, 16
+// rows per block.  A thread requests the log-sum-exp and its 8 values of up
+// to kMergeBatch ranges before using any (one memory round trip for the
+// usual range counts), then folds them with a running maximum.
 // ------------------------------------------------------------------------- //
-template <int kGroups>
+constexpr int kMergeBatch = 16;
+
 __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
-  constexpr int kRowsPerBlock = 8 / kGroups;
-  __shared__ float sm_m[8], sm_w[8];
-  __shared__ f32x4 sm_acc[8][32];
-  const int grp = threadIdx.x >> 5;
-  const int lane = threadIdx.x & 31;
-  const int g = grp % kGroups;
-  const int row = bid * kRowsPerBlock + grp / kGroups;
-  const bool row_ok = row < a.num_heads * a.n_q;
-  const int d0 = 4 * lane;
+  const int lane = threadIdx.x & 15;
+  const int row = bid * 16 + (threadIdx.x >> 4);
+  if (row >= a.num_heads * a.n_q) return;
+  const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
   float mx = kNegInf, wsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (row_ok) {
-    // the group's splits g, g + kGroups, ..., kBatch at a time, every load of
-    // a batch issued before any is used
-    constexpr int kBatch = 4;
-    for (int sp0 = g; sp0 < a.n_splits; sp0 += kBatch * kGroups) {
-      float lb[kBatch];
-      f32x4 ob[kBatch];
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int sp0 = 0; sp0 < a.n_splits; sp0 += kMergeBatch) {
+    float lb[kMergeBatch];
+    f32x4 o0[kMergeBatch], o1[kMergeBatch];
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i) {
-        const int sp = sp0 + i * kGroups;
-        lb[i] = sp < a.n_splits ? a.part_lse[sp * split_stride + row] : kNegInf;
-        ob[i] = sp < a.n_splits ? *reinterpret_cast<const f32x4*>(a.part_o + (sp * split_stride + row) * kHeadDim + d0)
-                                : (f32x4){0.f, 0.f, 0.f, 0.f};
-      }
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const int sp = sp0 + i;
+      const bool ok = sp < a.n_splits;
+      const float* po = a.part_o + (sp * split_stride + row) * kHeadDim + d0;
+      lb[i] = ok ? a.part_lse[sp * split_stride + row] : kNegInf;
+      o0[i] = ok ? *reinterpret_cast<const f32x4*>(po) : (f32x4){0.f, 0.f, 0.f, 0.f};
+      o1[i] = ok ? *reinterpret_cast<const f32x4*>(po + 4) : (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+    float bm = mx;
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i) {
-        const float l = lb[i];
-        if (l == kNegInf) continue;
-        if (l > mx) {
-          const float sc = fast_exp2(mx - l);
-          acc *= sc;
-          wsum *= sc;
-          mx = l;
-        }
-        const float w = fast_exp2(l - mx);
-        acc += w * ob[i];
-        wsum += w;
+    for (int i = 0; i < kMergeBatch; ++i) bm = fmaxf(bm, lb[i]);
+    if (bm == kNegInf) continue;
+    const float sc = fast_exp2(mx - bm);  // 0 while nothing was folded yet
+    wsum *= sc;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] *= sc;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const float w = lb[i] == kNegInf ? 0.f : fast_exp2(lb[i] - bm);
+      wsum += w;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc[k] += w * o0[i][k];
+        acc[4 + k] += w * o1[i][k];
       }
     }
+    mx = bm;
   }
-  if (kGroups > 1) {
-    if (lane == 0) {
-      sm_m[grp] = mx;
-      sm_w[grp] = wsum;
-    }
-    sm_acc[grp][lane] = acc;
-    __syncthreads();
-    if (g != 0) return;
-    float big = kNegInf;
-#pragma unroll
-    for (int k = 0; k < kGroups; ++k) big = fmaxf(big, sm_m[grp + k]);
-    wsum = 0.f;
-    acc = (f32x4){0.f, 0.f, 0.f, 0.f};
-    if (big != kNegInf) {
-#pragma unroll
-      for (int k = 0; k < kGroups; ++k) {
-        const float w = fast_exp2(sm_m[grp + k] - big);
-        wsum += w * sm_w[grp + k];
-        acc += w * sm_acc[grp + k][lane];
-      }
-    }
-    mx = big;
-  }
-  if (!row_ok) return;
   const int head = row / a.n_q, q = row % a.n_q;
-  if (mx != kNegInf) acc *= 1.0f / wsum;
-  u32x2 w;
-  w[0] = pack_bf16(acc[0], acc[1]);
-  w[1] = pack_bf16(acc[2], acc[3]);
-  *reinterpret_cast<u32x2*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = w;
+  const float inv = mx != kNegInf ? 1.0f / wsum : 0.f;
+  u32x4 w;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) w[k] = pack_bf16(acc[2 * k] * inv, acc[2 * k + 1] * inv);
+  *reinterpret_cast<u32x4*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = w;
 }
 
-template <int kGroups>
-__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
-  combine_block<kGroups>(a, blockIdx.x);
-}
+__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) { combine_block(a, blockIdx.x); }
 
 // ------------------------------------------------------------------------- //
 // video_combine: merges the key ranges of the video schedule.  A head's
@@ -1623,13 +1594,12 @@ __global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a)
 
 // The merges of one step's video and audio calls in one launch: blocks below
 // n_video merge video rows, the rest audio rows.
-template <int kGroups>
 __global__ __launch_bounds__(256) void step_combine_kernel(const CombineArgs v, const CombineArgs au,
                                                            int n_video) {
   if (static_cast<int>(blockIdx.x) < n_video)
     video_combine_block(v, combine_class_table(), blockIdx.x);
   else
-    combine_block<kGroups>(au, blockIdx.x - n_video);
+    combine_block(au, blockIdx.x - n_video);
 }
 
 }  // namespace
@@ -1676,44 +1646,20 @@ hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-namespace {
-int audio_combine_groups(const CombineArgs& a) {
-  const int rows = a.num_heads * a.n_q;
-  if (rows >= 4096) return 1;
-  return a.n_splits >= 8 ? 8 : a.n_splits >= 4 ? 4 : a.n_splits >= 2 ? 2 : 1;
-}
-}  // namespace
-
 hipError_t launch_step_combine(const CombineArgs& v, const CombineArgs& au, hipStream_t stream) {
   const int n_video = v.n_groups > 0 ? (v.num_heads * v.n_q + 15) / 16 : 0;
-  const int groups = au.num_heads > 0 ? audio_combine_groups(au) : 1;
-  const int n_audio = au.num_heads > 0 ? (au.num_heads * au.n_q + 8 / groups - 1) / (8 / groups) : 0;
+  const int n_audio = au.num_heads > 0 ? (au.num_heads * au.n_q + 15) / 16 : 0;
   if (n_video + n_audio == 0) return hipSuccess;
-  const dim3 grid(n_video + n_audio);
-  switch (groups) {
-    case 8: hipLaunchKernelGGL(step_combine_kernel<8>, grid, dim3(256), 0, stream, v, au, n_video); break;
-    case 4: hipLaunchKernelGGL(step_combine_kernel<4>, grid, dim3(256), 0, stream, v, au, n_video); break;
-    case 2: hipLaunchKernelGGL(step_combine_kernel<2>, grid, dim3(256), 0, stream, v, au, n_video); break;
-    default: hipLaunchKernelGGL(step_combine_kernel<1>, grid, dim3(256), 0, stream, v, au, n_video); break;
-  }
+  hipLaunchKernelGGL(step_combine_kernel, dim3(n_video + n_audio), dim3(256), 0, stream, v, au, n_video);
   return hipGetLastError();
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   const int rows = a.num_heads * a.n_q;
-  if (a.n_groups > 0) {
+  if (a.n_groups > 0)
     hipLaunchKernelGGL(video_combine_kernel, dim3((rows + 15) / 16), dim3(256), 0, stream, a);
-    return hipGetLastError();
-  }
-  const int groups = audio_combine_groups(a);
-  const int rows_per_block = 8 / groups;
-  dim3 grid((rows + rows_per_block - 1) / rows_per_block);
-  switch (groups) {
-    case 8: hipLaunchKernelGGL(combine_kernel<8>, grid, dim3(256), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL(combine_kernel<4>, grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(combine_kernel<2>, grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL(combine_kernel<1>, grid, dim3(256), 0, stream, a); break;
-  }
+  else
+    hipLaunchKernelGGL(combine_kernel, dim3((rows + 15) / 16), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

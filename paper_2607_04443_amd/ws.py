@@ -33,6 +33,7 @@ STATUS_NAMES = {0: "WS_OK", 1: "WS_ERR_INVALID_ARG", 2: "WS_ERR_SHAPE", 3: "WS_E
 WS_KIND_COND, WS_KIND_VIDEO, WS_KIND_AUDIO = 0, 1, 2
 WS_APPEND_RAW, WS_APPEND_NORM_ROPE, WS_QUERY_PREPARED = 0, 1, 2
 WS_OPT_VIDEO_KV_SPLITS, WS_OPT_AUDIO_KV_SPLITS, WS_OPT_VIDEO_RUNNING_MAX = 0, 1, 2
+WS_OPT_VIDEO_CLASS_CUS = 3
 INT32_MIN = -(2 ** 31)
 
 
