@@ -14,8 +14,11 @@ Sec. 2.1 history commit):
   3. video attention: the 920 prepared queries over 256 + 9 x 920 = 8536
      keys;
   4. audio attention: 4 queries over cond + 9 x (920 + 4) = 8572 keys;
-     steps 3 and 4 are one ws_step_attention call (video kernel, audio
-     kernel, one launch merging both calls' key ranges);
+     steps 3 and 4 are one ws_step_attention call: the video kernel, which
+     also computes the 4 audio rows over the pages both calls see (the rows
+     ride in the spare rows of its last query tile), the audio kernel over
+     the 9 audio-token pages only, and one launch merging both calls' key
+     ranges;
   5. unit u is committed to history and the unit that left the window evicted.
 All inputs are synthetic N(0,1) bf16 resident in HBM; H = 40 heads of 128.
 
@@ -28,6 +31,8 @@ per-component fields) and the library's launch timing (ws_cache_timing_*):
 `roofline` is for the video attention kernel (the dominant one), its FLOP
 per launch over its average launch time from HIP events recorded on the
 calls' stream around the kernel itself.
+`us_per_unit_separate_audio` is the contract step with the audio call in
+its own kernel over all of its pages (WS_OPT_STEP_SEPARATE_AUDIO).
 `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
 """
 import argparse
@@ -587,7 +592,7 @@ def main():
     sets = [dict(ck=dev_bf16((COND, H, D)), cv=dev_bf16((COND, H, D)), k=dev_bf16((LU, H, D)),
                  v=dev_bf16((LU, H, D)), ka=dev_bf16((AUDIO, H, D)), va=dev_bf16((AUDIO, H, D)),
                  q=dev_bf16((LU, H, D)), qa=dev_bf16((AUDIO, H, D))) for _ in range(2)]
-    last_unit = HIST + max(n_steps_total + args.steps, 130) + 2
+    last_unit = HIST + max(n_steps_total + 2 * args.steps + 10, 130) + 2
     vpos = [torch.from_numpy(synth.video_positions(u, GRID)).to(dev) for u in range(last_unit + 1)]
     apos = [torch.from_numpy(synth.audio_positions(u, AUDIO)).to(dev) for u in range(last_unit + 1)]
     out_v = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
@@ -661,6 +666,20 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
+    # The same steps with the audio call in its own kernel over all its pages
+    # (the audio rows not riding in the video kernel), timed the same way.
+    cache.set_option(ws.WS_OPT_STEP_SEPARATE_AUDIO, 1)
+    for _ in range(10):
+        step(u, False)
+        u += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(u, False)
+        u += 1
+    torch.cuda.synchronize()
+    us_separate_audio = (time.perf_counter() - t0) * 1e6 / args.steps
+    cache.set_option(ws.WS_OPT_STEP_SEPARATE_AUDIO, 0)
     # A second pass of `steps` steps for the breakdown: events around each
     # component, and the library's launch timing of the attention calls (HIP
     # events on the calls' stream around each kernel).
@@ -726,6 +745,9 @@ def main():
         # host (Python + library) time to enqueue one step; the step is
         # GPU-bound while this stays below us_per_unit
         "host_enqueue_us_per_step": enqueued * 1e6 / args.steps,
+        # the same step with the audio attention as its own kernel over all
+        # of its pages instead of riding in the video kernel
+        "us_per_unit_separate_audio": us_separate_audio,
         "video_attention": {"us": t_video, "tflops": fv / (t_video * 1e-6) / 1e12, "flop": fv,
                             "kernel_us": t_vkern, "merge_us": t_vmerge, "splits": v_splits},
         "audio_attention": {"us_warm": t_audio, "gbps_warm": audio_bytes / (t_audio * 1e-6) / 1e9,

@@ -178,7 +178,10 @@ typedef enum ws_option {
   /* ws_unit_attention_groups: 0 = every query group is partitioned as if
    * it had all CUs (several rounds of workgroups in one launch), 1 = the
    * groups share one round of the CUs in proportion to their work. */
-  WS_OPT_VIDEO_CLASS_CUS = 3
+  WS_OPT_VIDEO_CLASS_CUS = 3,
+  /* ws_step_attention: 0 = the audio rows ride in the video kernel when the
+   * step allows it (see there), 1 = always the separate audio kernel. */
+  WS_OPT_STEP_SEPARATE_AUDIO = 4
 } ws_option;
 
 /* Creates a cache: allocates the K and V page pools (2 * max_pages * H * 64 *
@@ -321,11 +324,25 @@ typedef struct ws_attn_call {
 /* A denoising step's two attentions over the cache (Sec. 3: the long video
  * latent queries and the short audio latent queries of the same unit): the
  * video kernel, the audio kernel, and one launch that merges both calls' key
- * ranges.  Each output equals what ws_unit_attention(video) and
- * ws_audio_attention(audio) write, bit for bit; both calls are validated
- * before anything is enqueued.  video, audio: host structs, read before the
- * call returns.  The audio call's key ranges use a workspace of their own.  With timing enabled the call records two ring entries: the
- * video kernel (merge time 0) and the audio kernel with the shared merge. */
+ * ranges.  Both calls are validated before anything is enqueued.  video,
+ * audio: host structs, read before the call returns.  The audio call's key
+ * ranges use a workspace of their own.
+ *
+ * Audio rows riding in the video kernel: when the audio call is
+ * WS_QUERY_PREPARED, every page the video call sees is visible to the audio
+ * call too, and the audio rows fit the spare rows of the video call's last
+ * 256-query tile (n_audio <= 256 * ceil(n_video / 256) - n_video), the
+ * video kernel also computes the audio rows over
+ * the video call's pages (the pages are streamed once for both), and the
+ * audio kernel walks only the pages the audio call alone sees (the unit
+ * audio tokens); the merge folds both.  WS_OPT_STEP_SEPARATE_AUDIO turns
+ * this off.  The video output always equals what ws_unit_attention(video)
+ * writes, bit for bit; the audio output equals ws_audio_attention(audio) bit
+ * for bit when the rows do not ride, and otherwise differs from it only in
+ * the order of fp32 sums.  With timing enabled the call records two ring
+ * entries: the video kernel (merge time 0), and the audio kernel with the
+ * shared merge (path 1; path 5 when the audio rows ride, with the audio
+ * kernel's range count, 0 when it had no pages to walk and was not launched). */
 WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, const ws_attn_call* audio,
                                    void* hip_stream);
 
@@ -441,7 +458,9 @@ WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t val
  * calls are overwritten); recording adds no synchronization. */
 typedef struct ws_call_timing {
   int32_t path;      /* 0 = video attention, 1 = audio attention, 2 = append,
-                        3 = QKV projection, 4 = output projection (ws_block_step) */
+                        3 = QKV projection, 4 = output projection (ws_block_step),
+                        5 = audio attention with its rows in the video kernel
+                        (ws_step_attention) */
   int32_t n_splits;  /* audio: key-range splits; video: workgroup groups; append: items */
   float attn_us;     /* attention kernel, microseconds */
   float merge_us;    /* merge kernel, microseconds (0 when there is none) */

@@ -14,6 +14,7 @@
 // The attention is the performer's per-step attention over its K/V cache
 // (Wan-Streamer v0.2, Sec. 3); block-causal visibility (Fig. 1 caption) is
 // resolved on the host into the list of visible pages.
+#include <algorithm>
 #include <cstddef>
 #include <mutex>
 #include <type_traits>
@@ -177,17 +178,14 @@ __device__ __forceinline__ void prepare_queries(const RopeTables& rope, uint32_t
 }
 
 // ------------------------------------------------------------------------- //
-// kv_append: grid (blocks of this launch, heads), 256 threads; the blocks
-// may belong to up to AppendArgs::kMaxSegs segments (K/V pages or query
-// chunks).
+// kv_append: one (item, head) tile of an append launch, an item being a K/V
+// page or a 64-token chunk of a query set of one of up to
+// AppendArgs::kMaxSegs segments.  256 threads; vt and wave_norm2 are the
+// block's LDS, free again when the call returns.
 // ------------------------------------------------------------------------- //
-__global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
-  (void)args;  // read in place, through append_args()
-  __shared__ __attribute__((aligned(16))) uint16_t vt[kPageTokens][kHeadDim + 8];
-  __shared__ float wave_norm2[4];
-  const const_append_args A = append_args();
-  const int head = blockIdx.y;
-  const const_append_seg sg = A->seg + A->blk_seg[blockIdx.x];
+__device__ __forceinline__ void append_tile(const_append_args A, int item, int head,
+                                            uint16_t (*vt)[kHeadDim + 8], float* wave_norm2) {
+  const const_append_seg sg = A->seg + A->blk_seg[item];
   RopeTables rope;
 #pragma unroll
   for (int b = 0; b < 3; ++b) {
@@ -197,17 +195,17 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
   }
   uint32_t* const flags = A->flags;
   if (sg->mode & kAppendQuery) {
-    prepare_queries(rope, flags, sg, A->blk_page[blockIdx.x], head);
+    prepare_queries(rope, flags, sg, A->blk_page[item], head);
     return;
   }
   const int num_heads = A->num_heads;
-  const int page = A->pages[blockIdx.x];
+  const int page = A->pages[item];
   const uint16_t* src_k = sg->k;
   const uint16_t* src_v = sg->v;
   const int64_t tok_stride = sg->tok_stride, head_stride = sg->head_stride;
   const int n_tokens = sg->n_tokens;
   const int mode = sg->mode;
-  const int tok0 = A->blk_page[blockIdx.x] * kPageTokens;
+  const int tok0 = A->blk_page[item] * kPageTokens;
   const int64_t tile = (static_cast<int64_t>(page) * num_heads + head) * kPageHeadElems;
   uint16_t* kdst = A->kpool + tile;
   uint16_t* vdst = A->vpool + tile;
@@ -325,6 +323,23 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
   if (t == 0)
     A->knorm2[static_cast<int64_t>(page) * num_heads + head] =
         fmaxf(fmaxf(wave_norm2[0], wave_norm2[1]), fmaxf(wave_norm2[2], wave_norm2[3]));
+}
+
+// The launch: a grid of a few blocks per CU that loop over the launch's
+// (item, head) tiles, consecutive tiles being the heads of one item.  (One
+// block per tile made the launch as long as dispatching its ~1,400 short
+// blocks: their average life was about an eighth of the launch.)
+__global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs args) {
+  (void)args;  // read in place, through append_args()
+  __shared__ __attribute__((aligned(16))) uint16_t vt[kPageTokens][kHeadDim + 8];
+  __shared__ float wave_norm2[4];
+  const const_append_args A = append_args();
+  const int heads = A->num_heads;
+  const int n_tiles = A->n_blocks * heads;
+  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    append_tile(A, tile / heads, tile % heads, vt, wave_norm2);
+    __syncthreads();  // vt and wave_norm2 are rewritten by the next tile
+  }
 }
 
 // ------------------------------------------------------------------------- //
@@ -922,7 +937,11 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   c.page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
   c.kpool = a.kpool + head * kPageHeadElems;
   c.vpool = a.vpool + head * kPageHeadElems;
-  c.active = sg.q_lo + wave * 32 < sg.q_hi;
+  // The wave's rows: video rows of q, and at and past rq_row0 (the end of
+  // the video rows) rider rows, the prepared rows of rq that see the same
+  // pages; a wave may hold both.
+  const int wrow = sg.q_lo + wave * 32;
+  c.active = wrow < sg.q_hi || (a.n_rq > 0 && wrow < a.rq_row0 + a.n_rq && wrow + 32 > a.rq_row0);
   c.wave = wave;
   c.half = half;
   c.l32 = l32;
@@ -946,9 +965,10 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
 #pragma unroll
     for (int k = 0; k < 3; ++k) pg_first[k] = c.pages[min(p_begin + k, p_end - 1)].x;
   }
-  const int q = sg.q_lo + wave * 32 + l32;
-  const bool q_ok = q < sg.q_hi;
-  const bool norm_rope = a.mode == 1;
+  const bool rider = a.n_rq > 0 && wrow + l32 >= a.rq_row0;  // the same in both halves of a row
+  const int q = wrow + l32 - (rider ? a.rq_row0 : 0);
+  const bool q_ok = q < (rider ? a.n_rq : sg.q_hi);
+  const bool norm_rope = !rider && a.mode == 1;
   int3 qpos = make_int3(0, 0, 0);
   if (norm_rope && q_ok) qpos = make_int3(a.positions[3 * q], a.positions[3 * q + 1], a.positions[3 * q + 2]);
   // the segment's page-list entries (two per lane in the first pass)
@@ -959,7 +979,8 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
     pgl[k] = pi < p_end ? c.pages[pi].x : -1;
   }
   u32x4 qraw[8];
-  const uint16_t* qp = a.q + q * a.q_tok_stride + head * a.q_head_stride + 8 * half;
+  const uint16_t* qp = rider ? a.rq + q * a.rq_tok_stride + head * a.rq_head_stride + 8 * half
+                             : a.q + q * a.q_tok_stride + head * a.q_head_stride + 8 * half;
 #pragma unroll
   for (int s = 0; s < 8; ++s)
     qraw[s] = q_ok ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : (u32x4){0u, 0u, 0u, 0u};
@@ -1014,7 +1035,7 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
       }
       c.qreg[s] = as_bf16x8(q_ok ? w : (u32x4){0u, 0u, 0u, 0u});
     }
-  } else if (a.mode == 2) {  // prepared: Q'' as given
+  } else if (a.mode == 2 || rider) {  // prepared: Q'' as given
 #pragma unroll
     for (int s = 0; s < 8; ++s) c.qreg[s] = as_bf16x8(qraw[s]);
   } else {
@@ -1102,6 +1123,21 @@ __device__ __forceinline__ void video_segment(const AttnArgs& a, const VideoSeg&
   // ---- epilogue: lane holds O^T[32t + 8g + 4h + i][q], g = r/4, i = r%4 ----
   const float l_tot = st.l_run + __shfl_xor(st.l_run, 32);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  if (rider) {  // always a partial, fp32, for the rider rows' own merge
+    if (!q_ok) return;
+    const int64_t row = (static_cast<int64_t>(sg.seg) * a.num_heads + head) * a.n_rq + q;
+    float* po = a.rpart_o + row * kHeadDim;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 w = {st.o[t][4 * g] * inv, st.o[t][4 * g + 1] * inv, st.o[t][4 * g + 2] * inv,
+                         st.o[t][4 * g + 3] * inv};
+        *reinterpret_cast<f32x4*>(po + 32 * t + 8 * g + 4 * half) = w;
+      }
+    if (half == 0) a.rpart_lse[row] = l_tot > 0.f ? st.m_run + __log2f(l_tot) : kNegInf;
+    return;
+  }
   if (sg.n_seg == 1) {
     if (!q_ok) return;
     uint16_t* op = a.out + q * a.out_tok_stride + head * a.out_head_stride;
@@ -1460,27 +1496,36 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
 
 // ------------------------------------------------------------------------- //
 // combine (audio key ranges): 16 threads per (head, query) row, 8 d each, 16
-// rows per block.  A thread requests the log-sum-exp and its 8 values of up
-// to kMergeBatch ranges before using any (one memory round trip for the
-// usual range counts), then folds them with a running maximum.
+// rows per block.  A thread requests the log-sum-exp and its 8 values of
+// kMergeBatch ranges before using any (one memory round trip per batch),
+// then folds them with a running maximum.  The batch sets the registers a
+// thread holds: the audio call's own merge takes 16 ranges at once; inside
+// the merge launch of a step, whose video rows need few registers, 3 (more
+// would cap the occupancy of the video rows' blocks).
 // ------------------------------------------------------------------------- //
-constexpr int kMergeBatch = 16;
-
+template <int kMergeBatch>
 __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   const int lane = threadIdx.x & 15;
   const int row = bid * 16 + (threadIdx.x >> 4);
   if (row >= a.num_heads * a.n_q) return;
+  const int head = row / a.n_q, q = row % a.n_q;
+  int n_splits = a.n_splits;
+  if (a.r_groups > 0) {  // the ranges the video kernel wrote for rider rows
+    const VideoPartition part{a.num_heads, a.r_pages, a.seg_cost, a.r_groups};
+    const int64_t h0 = static_cast<int64_t>(head) * a.r_pages;
+    n_splits += static_cast<int>(video_group_of(part, h0 + a.r_pages - 1) - video_group_of(part, h0) + 1);
+  }
   const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
   float mx = kNegInf, wsum = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int sp0 = 0; sp0 < a.n_splits; sp0 += kMergeBatch) {
+  for (int sp0 = 0; sp0 < n_splits; sp0 += kMergeBatch) {
     float lb[kMergeBatch];
     f32x4 o0[kMergeBatch], o1[kMergeBatch];
 #pragma unroll
     for (int i = 0; i < kMergeBatch; ++i) {
       const int sp = sp0 + i;
-      const bool ok = sp < a.n_splits;
+      const bool ok = sp < n_splits;
       const float* po = a.part_o + (sp * split_stride + row) * kHeadDim + d0;
       lb[i] = ok ? a.part_lse[sp * split_stride + row] : kNegInf;
       o0[i] = ok ? *reinterpret_cast<const f32x4*>(po) : (f32x4){0.f, 0.f, 0.f, 0.f};
@@ -1506,7 +1551,6 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
     }
     mx = bm;
   }
-  const int head = row / a.n_q, q = row % a.n_q;
   const float inv = mx != kNegInf ? 1.0f / wsum : 0.f;
   u32x4 w;
 #pragma unroll
@@ -1514,7 +1558,7 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   *reinterpret_cast<u32x4*>(a.out + q * a.out_tok_stride + head * a.out_head_stride + d0) = w;
 }
 
-__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) { combine_block(a, blockIdx.x); }
+__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) { combine_block<16>(a, blockIdx.x); }
 
 // ------------------------------------------------------------------------- //
 // video_combine: merges the key ranges of the video schedule.  A head's
@@ -1599,7 +1643,7 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const CombineArgs v, 
   if (static_cast<int>(blockIdx.x) < n_video)
     video_combine_block(v, combine_class_table(), blockIdx.x);
   else
-    combine_block(au, blockIdx.x - n_video);
+    combine_block<4>(au, blockIdx.x - n_video);
 }
 
 }  // namespace
@@ -1629,8 +1673,9 @@ hipError_t static_scratch(void** ptr) {
 }
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_blocks, a.num_heads);
-  hipLaunchKernelGGL(kv_append_kernel, grid, dim3(256), 0, stream, a);
+  const int tiles = a.n_blocks * a.num_heads;
+  const int grid = std::min(tiles, std::max(1, a.grid_blocks));
+  hipLaunchKernelGGL(kv_append_kernel, dim3(grid), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

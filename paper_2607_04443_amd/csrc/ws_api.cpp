@@ -56,6 +56,8 @@ using ws_internal::hip_fail;
   } while (0)
 
 using ws::kMaxVideoSplits;
+// Blocks per CU of an append launch; each loops over the launch's tiles.
+constexpr int kAppendBlocksPerCu = 4;
 constexpr int kMaxAudioSplits = 512;
 using ws::kMaxAudioQ;
 
@@ -117,10 +119,13 @@ struct ws_cache {
   int32_t opt_audio_splits = 0;
   int32_t opt_running_max = 0;
   int32_t opt_class_cus = 0;  // 0: each query class sized for all CUs, 1: classes share the CUs
+  int32_t opt_separate_audio = 0;  // 1: ws_step_attention never lets audio rows ride in the video kernel
   float* knorm2 = nullptr;  // [max_pages][H] squared key-norm maxima
   uint16_t* zeros = nullptr;  // 1 KB of zeros (direct-load source of empty blocks)
   void* static_ws = nullptr;  // device address of the static split-KV workspace on this device
   std::vector<ws::PageRef> scratch_list;
+  std::vector<ws::PageRef> rider_video, rider_audio;  // the step's two visible lists (host)
+  std::vector<uint8_t> page_mark;                     // per page id, all zero between calls
   TimingRing timing;
 
   ws_cache(int32_t page_tokens, int32_t max_pages) : pt(page_tokens, max_pages) {}
@@ -689,6 +694,92 @@ ws_status use_static_workspace(ws_cache* c, AttnPlan& pv, AttnPlan& pa) {
   return WS_OK;
 }
 
+// Audio rows riding in the video kernel.  The audio queries of a step see
+// the pages the video queries see plus the unit's audio pages (Sec. 3: both
+// latent streams of a unit attend over the same cache; the audio tokens are
+// visible to audio queries only).  When the audio call's visible pages
+// include every page of the video call's, its queries come prepared (Q''),
+// and the spare rows of the video call's last 256-row query tile hold them,
+// the video kernel computes the audio rows over the shared pages while it
+// streams those pages for the video rows, and the audio kernel walks only
+// the pages the video call does not see.  The merge then folds, per (head,
+// row), the audio kernel's ranges and the ranges the video kernel wrote.
+// Fills the fused plans and *rider_ranges (the most video ranges of a head);
+// false (plans untouched) when the step does not qualify.
+bool plan_riders(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio, AttnPlan& pv, AttnPlan& pa,
+                 int* rider_ranges) {
+  if (c->opt_separate_audio || audio->desc.mode != WS_QUERY_PREPARED) return false;
+  if (pv.a.n_classes != 1 || pv.a.cls[0].n_pages == 0) return false;
+  const ws::AttnClass& cl = pv.a.cls[0];
+  const int H = c->cfg.num_heads;
+  const int n_rq = audio->n_q;
+  const int rq_row0 = video->n_q;
+  if (rq_row0 + n_rq > cl.n_qtiles * ws::kVideoQTile) return false;
+  // the audio call's pages that the video call does not see; every video
+  // page must be among the audio call's
+  c->pt.visible_pages(ws::MaskSpec{video->mask.q_unit, video->mask.min_visible_unit, video->mask.kind_mask},
+                      &c->rider_video);
+  c->pt.visible_pages(ws::MaskSpec{audio->mask.q_unit, audio->mask.min_visible_unit, audio->mask.kind_mask},
+                      &c->rider_audio);
+  std::vector<uint8_t>& mark = c->page_mark;
+  if (mark.size() != static_cast<size_t>(c->cfg.max_pages)) mark.assign(static_cast<size_t>(c->cfg.max_pages), 0);
+  for (const ws::PageRef& r : c->rider_video) mark[static_cast<size_t>(r.page)] = 1;
+  size_t shared = 0;
+  c->scratch_list.clear();
+  for (const ws::PageRef& r : c->rider_audio) {
+    if (mark[static_cast<size_t>(r.page)] == 1) {
+      mark[static_cast<size_t>(r.page)] = 2;
+      ++shared;
+    } else {
+      c->scratch_list.push_back(r);
+    }
+  }
+  for (const ws::PageRef& r : c->rider_video) mark[static_cast<size_t>(r.page)] = 0;
+  const int32_t n_extra = static_cast<int32_t>(c->scratch_list.size());
+  if (shared != c->rider_video.size() || n_extra > ws::AttnArgs::kInlinePages) return false;
+  // key ranges: the audio kernel's over the extra pages, then the video
+  // kernel's (at most rmax per head)
+  const ws::VideoPartition part{H, cl.n_pages, pv.a.seg_cost, cl.n_groups};
+  int rmax = 1;
+  for (int64_t h = 0; h < H; ++h) {
+    const int64_t h0 = h * cl.n_pages;
+    rmax = std::max(rmax, static_cast<int>(ws::video_group_of(part, h0 + cl.n_pages - 1) -
+                                           ws::video_group_of(part, h0) + 1));
+  }
+  int splits = 0, pps = 0;
+  if (n_extra > 0) {
+    splits = choose_audio_splits(c, pa.a.n_qtiles * H, n_extra);
+    splits = std::max(1, std::min(splits, n_extra));
+    pps = (n_extra + splits - 1) / splits;
+    splits = (n_extra + pps - 1) / pps;
+  }
+  if (static_cast<int64_t>(splits + rmax) * H * n_rq > c->part_rows) return false;
+
+  ws::AttnArgs& aa = pa.a;
+  for (int32_t i = 0; i < n_extra; ++i)
+    aa.inline_pages[i] = make_int2(c->scratch_list[static_cast<size_t>(i)].page,
+                                   c->scratch_list[static_cast<size_t>(i)].n_valid);
+  aa.pages = nullptr;
+  aa.n_pages = n_extra;
+  aa.n_splits = std::max(splits, 1);
+  aa.pages_per_split = pps;
+  pa.splits = splits;
+  pa.part_rows = static_cast<int64_t>(splits + rmax) * H * n_rq;
+  pa.merge = true;
+  pa.cb.n_splits = splits;
+  pa.cb.r_pages = cl.n_pages;
+  pa.cb.r_groups = cl.n_groups;
+  pa.cb.seg_cost = pv.a.seg_cost;
+  ws::AttnArgs& av = pv.a;
+  av.rq = static_cast<const uint16_t*>(audio->q);
+  av.rq_tok_stride = audio->q_tok_stride;
+  av.rq_head_stride = audio->q_head_stride;
+  av.n_rq = n_rq;
+  av.rq_row0 = rq_row0;
+  *rider_ranges = rmax;
+  return true;
+}
+
 ws_status step_attention_impl(ws_cache* c, const ws_attn_call* video, const ws_attn_call* audio,
                               void* hip_stream, bool static_workspace) {
   if (!c || !video || !audio) return fail(WS_ERR_INVALID_ARG, "NULL argument");
@@ -717,18 +808,28 @@ ws_status step_attention_impl(ws_cache* c, const ws_attn_call* video, const ws_a
     if (ws_status st = plan_video(); st != WS_OK) return st;
     if (c->arena_wraps != wraps + 1) return fail(WS_ERR_SHAPE, "page-list arena too small for one step");
   }
+  int rider_ranges = 0;
+  const bool riders = plan_riders(c, video, audio, pv, pa, &rider_ranges);
   if (static_workspace)
     if (ws_status st = use_static_workspace(c, pv, pa); st != WS_OK) return st;
-  // video kernel, audio kernel, then one launch merging both
+  if (riders) {  // the video kernel's ranges of the audio rows follow the audio kernel's
+    const int64_t off = static_cast<int64_t>(pa.splits) * c->cfg.num_heads * audio->n_q;
+    pv.a.rpart_o = pa.a.part_o + off * ws::kHeadDim;
+    pv.a.rpart_lse = pa.a.part_lse + off;
+  }
+  // video kernel, audio kernel (over the extra pages only when the audio
+  // rows ride in the video kernel), then one launch merging both
   int sv = -1, sa = -1;
   if (ws_status st = timing_begin(c, pv, stream, &sv); st != WS_OK) return st;
   hipError_t e = launch_plan_kernel(pv, stream);
   if (e != hipSuccess) return hip_fail(e, "unit_attn launch");
   if (ws_status st = timing_mark(c, sv, 1, stream); st != WS_OK) return st;
   if (ws_status st = timing_mark(c, sv, 2, stream); st != WS_OK) return st;
-  if (ws_status st = timing_begin(c, pa, stream, &sa); st != WS_OK) return st;
-  e = launch_plan_kernel(pa, stream);
-  if (e != hipSuccess) return hip_fail(e, "audio_attn launch");
+  if (ws_status st = timing_begin_path(c, riders ? 5 : 1, pa.splits, stream, &sa); st != WS_OK) return st;
+  if (!riders || pa.splits > 0) {
+    e = launch_plan_kernel(pa, stream);
+    if (e != hipSuccess) return hip_fail(e, "audio_attn launch");
+  }
   if (ws_status st = timing_mark(c, sa, 1, stream); st != WS_OK) return st;
   if (pv.merge || pa.merge) {
     ws::CombineArgs none{};
@@ -870,6 +971,7 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   ws::AppendArgs a{};
   a.num_heads = H;
+  a.grid_blocks = kAppendBlocksPerCu * c->num_cus;
   a.kpool = c->kpool;
   a.vpool = c->vpool;
   a.knorm2 = c->knorm2;
@@ -1125,6 +1227,10 @@ ws_status ws_cache_set_option(ws_cache* c, ws_option opt, int32_t value) {
     case WS_OPT_VIDEO_CLASS_CUS:
       if (value < 0 || value > 1) return fail(WS_ERR_INVALID_ARG, "class CU option must be 0 or 1");
       c->opt_class_cus = value;
+      return WS_OK;
+    case WS_OPT_STEP_SEPARATE_AUDIO:
+      if (value < 0 || value > 1) return fail(WS_ERR_INVALID_ARG, "separate-audio option must be 0 or 1");
+      c->opt_separate_audio = value;
       return WS_OK;
     case WS_OPT_VIDEO_RUNNING_MAX:
       if (value < 0 || value > 1) return fail(WS_ERR_INVALID_ARG, "running-max option must be 0 or 1");

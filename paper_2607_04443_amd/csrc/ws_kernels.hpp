@@ -97,8 +97,9 @@ struct AppendArgs {
   static constexpr int kMaxSegs = 8;
   static constexpr int kMaxAppendPages = 192;
   AppendSeg seg[kMaxSegs];
-  int32_t n_blocks;
+  int32_t n_blocks;      // items (pages and query chunks) of the launch
   int32_t num_heads;
+  int32_t grid_blocks;   // blocks of the launch (each loops over the (item, head) tiles)
   uint16_t* kpool;
   uint16_t* vpool;
   float* knorm2;
@@ -157,6 +158,18 @@ struct AttnArgs {
   int64_t out_head_stride;
   float* part_o;         // [split][head][n_q][128], normalised: fp32 (audio), bf16 (video)
   float* part_lse;       // [split][head][n_q], log2 domain (scaled logits)
+  // Video: rider rows, a second query set (prepared Q'') that walks the same
+  // pages in the spare rows of the last query tile: rows rq_row0 .. rq_row0 +
+  // n_rq - 1 of the call's row space (rq_row0 = n_q, a single query class)
+  // are rows 0 .. n_rq - 1 of rq.  Their key ranges always go out as fp32
+  // partials, [range][head][n_rq][128] and [range][head][n_rq].
+  const uint16_t* rq;
+  int64_t rq_tok_stride;
+  int64_t rq_head_stride;
+  int32_t n_rq;          // 0: no rider rows
+  int32_t rq_row0;
+  float* rpart_o;
+  float* rpart_lse;
   uint32_t* flags;
   int2 inline_pages[kInlinePages];
 };
@@ -170,6 +183,12 @@ struct CombineArgs {
   int32_t n_classes;     // video: the call's query classes (AttnArgs::cls)
   int32_t seg_cost;
   AttnClass cls[kMaxClasses];
+  // Audio merge with rider rows: after the n_splits ranges of the audio
+  // kernel come the ranges the video kernel wrote for the rows, as many per
+  // head as the video partition over r_pages pages with r_groups groups
+  // gives (r_groups = 0: none).
+  int32_t r_pages;
+  int32_t r_groups;
   int32_t n_q;
   int32_t num_heads;
   uint16_t* out;

@@ -34,6 +34,7 @@ WS_KIND_COND, WS_KIND_VIDEO, WS_KIND_AUDIO = 0, 1, 2
 WS_APPEND_RAW, WS_APPEND_NORM_ROPE, WS_QUERY_PREPARED = 0, 1, 2
 WS_OPT_VIDEO_KV_SPLITS, WS_OPT_AUDIO_KV_SPLITS, WS_OPT_VIDEO_RUNNING_MAX = 0, 1, 2
 WS_OPT_VIDEO_CLASS_CUS = 3
+WS_OPT_STEP_SEPARATE_AUDIO = 4
 INT32_MIN = -(2 ** 31)
 
 
@@ -533,9 +534,11 @@ class Cache:
 
     def timing_read(self):
         """Per-call launch timing recorded since the last read, oldest first:
-        dicts with path ('video'/'audio'/'append'), n_splits, attn_us, merge_us."""
+        dicts with path ('video', 'audio', 'append', 'qkv_gemm', 'out_gemm', or
+        'audio_riders': a step's audio call with its rows in the video kernel),
+        n_splits, attn_us, merge_us."""
         out = ws_cache_timing_read(self.handle, getattr(self, "_timing_cap", 0))
-        names = {0: "video", 1: "audio", 2: "append", 3: "qkv_gemm", 4: "out_gemm"}
+        names = {0: "video", 1: "audio", 2: "append", 3: "qkv_gemm", 4: "out_gemm", 5: "audio_riders"}
         return [dict(path=names.get(t.path, str(t.path)), n_splits=t.n_splits, attn_us=t.attn_us,
                      merge_us=t.merge_us) for t in out]
 
