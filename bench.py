@@ -69,15 +69,22 @@ def parse():
     ap.add_argument("--long-reps", type=int, default=5)
     ap.add_argument("--no-peak-probes", dest="peak_probes", action="store_false",
                     help="skip the calibration probes (measured MFMA and HBM read ceilings)")
-    ap.add_argument("--pmc-driver", action="store_true",
-                    help="run one step, then the video and audio attention and a 256 MiB device "
-                         "copy three times each, untimed (the program rocprofv3 --pmc runs)")
+    ap.add_argument("--pmc-driver", nargs="?", const="step", choices=("step", "long"),
+                    help="the program rocprofv3 --pmc runs, untimed: 'step' (default) runs three "
+                         "steps, then the video and audio attention three times each as separate "
+                         "calls; 'long' runs the video attention of the long-history workload "
+                         "(30616 keys) three times; both end with three 256 MiB device copies")
     ap.add_argument("--cpu-v01-point", action="store_true",
                     help="time the fp64 oracle on the whole v0.1-scale workload (CPU only) and print "
                          "one JSON line")
-    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="summarise two rocprofv3 --pmc -f csv runs of --pmc-driver (FETCH_SIZE, "
-                         "WRITE_SIZE) as markdown")
+    ap.add_argument("--mfma-summary", metavar="DIR",
+                    help="summarise one rocprofv3 --pmc -f csv run of --pmc-driver with the MFMA and "
+                         "instruction counters (GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES, "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16, ...) for unit_attn_kernel as markdown")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="DIR",
+                    help="summarise rocprofv3 --pmc -f csv runs of --pmc-driver as markdown: "
+                         "FETCH_SIZE and WRITE_SIZE of 'step', optionally followed by FETCH_SIZE "
+                         "and WRITE_SIZE of 'long'")
     return ap.parse_args()
 
 
@@ -157,17 +164,19 @@ def cpu_baseline(budget_s=12.0):
             "single_thread_v01": single}
 
 
-def long_history(args, ws, sets, gamma, eps, stream, dev):
-    """Long-history stress: 32 committed history units (256 + 33 x 920 =
-    30616 keys) and 4 denoising steps issued back-to-back on one stream, each
-    rewriting the current unit's K/V in place (append with RMS-norm + rotary,
-    and the query preparation, in one launch) and running the video
-    attention.  Timed with events around the 4 steps;
-    the median of `long_reps` repetitions.  The history reuses the two
-    resident input sets (values do not change the timing)."""
+LONG_HIST = 32
+
+
+def long_setup(ws, sets, gamma, eps, dev):
+    """The long-history cache: a cond slice and 32 committed history units
+    (256 + 33 x 920 = 30616 keys visible to unit 32), built from the two
+    resident input sets (values do not change the timing).  Returns the
+    cache and a function that issues one denoising step of unit 32: an
+    in-place rewrite of its K/V (append with RMS-norm + rotary, and the query
+    preparation, in one launch) and the video attention."""
     import torch
     from paper_2607_04443_amd import synth
-    hist_l = 32
+    hist_l = LONG_HIST
     cache = ws.Cache(H, 4 + (hist_l + 2) * 16 + 8, max_q_tokens=1024)
     pos = [torch.from_numpy(synth.video_positions(u, GRID)).to(dev) for u in range(hist_l + 1)]
     s0 = sets[0]
@@ -180,14 +189,28 @@ def long_history(args, ws, sets, gamma, eps, stream, dev):
     q_v = torch.empty((LU, H, D), dtype=torch.bfloat16, device=dev)
     mask = ws.mask_spec(hist_l, 0, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
 
+    def one_step(step, attention=True):
+        s = sets[step % 2]
+        cache.step_append(
+            [dict(unit=hist_l, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"],
+                  mode=ws.WS_APPEND_NORM_ROPE, positions=pos[hist_l], gamma=gamma, eps=eps)],
+            [dict(q=s["q"], q_out=q_v, positions=pos[hist_l], gamma=gamma, eps=eps)])
+        if attention:
+            cache.unit_attention(q_v, out, mask, ws.WS_QUERY_PREPARED)
+
+    return cache, one_step
+
+
+def long_history(args, ws, sets, gamma, eps, stream, dev):
+    """Long-history stress (long_setup): 4 denoising steps issued
+    back-to-back on one stream, timed with events around the 4 steps; the
+    median of `long_reps` repetitions."""
+    import torch
+    cache, one_step = long_setup(ws, sets, gamma, eps, dev)
+
     def four_steps():
         for step in range(4):
-            s = sets[step % 2]
-            cache.step_append(
-                [dict(unit=hist_l, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"],
-                      mode=ws.WS_APPEND_NORM_ROPE, positions=pos[hist_l], gamma=gamma, eps=eps)],
-                [dict(q=s["q"], q_out=q_v, positions=pos[hist_l], gamma=gamma, eps=eps)])
-            cache.unit_attention(q_v, out, mask, ws.WS_QUERY_PREPARED)
+            one_step(step)
 
     four_steps()
     torch.cuda.synchronize()
@@ -202,7 +225,7 @@ def long_history(args, ws, sets, gamma, eps, stream, dev):
     cache.close()
     times.sort()
     med = times[len(times) // 2]
-    lk = COND + (hist_l + 1) * LU
+    lk = COND + (LONG_HIST + 1) * LU
     return {"keys": lk, "us_4_steps": med, "us_per_step": med / 4,
             "tflops": 4 * video_flop(LU, lk) / (med * 1e-6) / 1e12}
 
@@ -258,7 +281,9 @@ def catch_up(args, ws, sets, vpos, gamma, eps, stream, dev, n_units=3):
     """Catch-up after a stall: the queries of n_units consecutive 920-token
     units in one ws_unit_attention_groups call, each unit under its own
     8-unit window (256 + 9 x 920 = 8536 keys per unit), against the same work
-    as one ws_unit_attention call per unit.  Queries prepared beforehand;
+    as one ws_unit_attention call per unit, and against the one call with
+    every unit partitioned as if it had all CUs (WS_OPT_VIDEO_CLASS_CUS).
+    Queries prepared beforehand; after a warm-up, the variants in turn,
     medians of `long_reps` repetitions (events around the call(s))."""
     import torch
     first = HIST
@@ -285,29 +310,30 @@ def catch_up(args, ws, sets, vpos, gamma, eps, stream, dev, n_units=3):
             cache.unit_attention(q_all[i * LU:(i + 1) * LU], out[i * LU:(i + 1) * LU], m,
                                  ws.WS_QUERY_PREPARED)
 
-    def timed(fn):
-        for _ in range(3):
-            fn()
-        t = []
-        for _ in range(max(args.long_reps, 1)):
+    def all_cus():
+        cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, 1)
+        one_call()
+        cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, 0)
+
+    # about 20 ms of the same work first (the clocks settle under load), then
+    # the three variants in turn, each call timed on its own
+    for _ in range(40):
+        one_call()
+    t = {one_call: [], separate: [], all_cus: []}
+    for _ in range(max(args.long_reps, 1)):
+        for fn in t:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             fn()
             b.record(stream)
             b.synchronize()
-            t.append(a.elapsed_time(b) * 1e3)
-        t.sort()
-        return t[len(t) // 2]
-
-    t1, t3 = timed(one_call), timed(separate)
-    cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, 1)
-    t1_shared = timed(one_call)
-    cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, 0)
+            t[fn].append(a.elapsed_time(b) * 1e3)
+    t1, t3, t1_all = (sorted(t[fn])[len(t[fn]) // 2] for fn in (one_call, separate, all_cus))
     cache.close()
     lk = COND + (HIST + 1) * LU
     flop = n_units * video_flop(LU, lk)
     return {"units": n_units, "queries": LU * n_units, "keys_per_unit": lk, "flop": flop,
-            "us": t1, "tflops": flop / (t1 * 1e-6) / 1e12, "us_one_call_shared_round": t1_shared,
+            "us": t1, "tflops": flop / (t1 * 1e-6) / 1e12, "us_one_call_all_cus_per_unit": t1_all,
             "us_separate_calls": t3,
             "tflops_separate_calls": flop / (t3 * 1e-6) / 1e12}
 
@@ -382,13 +408,18 @@ def block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev, steps=50, wa
     rows = LU + AUDIO
     f_qkv, f_out = 2.0 * rows * hid * 3 * hid, 2.0 * rows * hid * hid
     t_qkv, t_out = avg("qkv_gemm"), avg("out_gemm")
-    t_app, t_vid, t_aud = avg("append"), avg("video"), avg("audio")
-    t_merge = avg("audio", "merge_us")
+    # the step's audio call: its rows ride in the video kernel, the audio
+    # kernel walks the audio-token pages only (path 'audio_riders'), unless
+    # the step does not qualify (path 'audio')
+    apath = "audio_riders" if any(r["path"] == "audio_riders" for r in rec) else "audio"
+    t_app, t_vid, t_aud = avg("append"), avg("video"), avg(apath)
+    t_merge = avg(apath, "merge_us")
     attn_us = t_app + t_vid + t_aud + t_merge
     return {"us_per_step": us, "rows": rows, "hidden": hid,
             "qkv_gemm_us": t_qkv, "qkv_gemm_tflops": f_qkv / (t_qkv * 1e-6) / 1e12,
             "out_gemm_us": t_out, "out_gemm_tflops": f_out / (t_out * 1e-6) / 1e12,
             "append_us": t_app, "video_kernel_us": t_vid, "audio_kernel_us": t_aud, "merge_us": t_merge,
+            "audio_rows_in_video_kernel": apath == "audio_riders",
             "attention_share": attn_us / (attn_us + t_qkv + t_out)}
 
 
@@ -417,9 +448,10 @@ def recorded_traffic():
     return float(fields["unit_attn_traffic_bytes"])
 
 
-def pmc_summary(fetch_dir, write_dir):
-    """Markdown summary of a FETCH_SIZE and a WRITE_SIZE counter run of
-    --pmc-driver: per-dispatch KiB (median over each kernel's dispatches),
+def pmc_summary(fetch_dir, write_dir, long_fetch=None, long_write=None):
+    """Markdown summary of FETCH_SIZE and WRITE_SIZE counter runs of
+    --pmc-driver (the step driver, optionally also the long-history one):
+    per-dispatch KiB (median over each kernel's dispatches of one grid size),
     scaled by what the same counter reads for the 256 MiB device copy."""
     import csv
     import glob
@@ -435,85 +467,202 @@ def pmc_summary(fetch_dir, write_dir):
                 if r["Counter_Name"] != counter:
                     continue
                 key = (f, r["Dispatch_Id"])
-                name, grid = r["Kernel_Name"], int(r.get("Grid_Size") or 0)
+                name = r["Kernel_Name"]
+                wg = int(r.get("Workgroup_Size") or 1) or 1
+                grid = int(r.get("Grid_Size") or 0) // wg
                 disp.setdefault(key, [name, grid, 0.0])[2] += float(r["Counter_Value"])
         out = {}
         for name, grid, val in disp.values():
             out.setdefault(name, []).append((grid, val))
         return out
 
-    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
-
-    def pick(table, key):
+    def pick(table, key, grid=None):
         rows = [v for n, vals in table.items() if key in n for v in vals]
-        if key == "copyBuffer":  # the 256 MiB copy: the largest grid
-            g = max(r[0] for r in rows)
-            rows = [r for r in rows if r[0] == g]
+        if grid == "max":  # the largest launch (the 256 MiB copy, the step's append)
+            grid = max(r[0] for r in rows)
+        if grid is not None:
+            rows = [r for r in rows if r[0] == grid]
         return statistics.median(v for _, v in rows), len(rows)
 
-    f_copy, _ = pick(fetch, "copyBuffer")
-    w_copy, _ = pick(write, "copyBuffer")
-    f_scale, w_scale = f_copy * 1024 / COPY_BYTES, w_copy * 1024 / COPY_BYTES
-    lines = ["# HBM traffic: unit_attn_kernel and audio_attn_kernel, v0.2 unit with an 8-unit history",
+    def table(fd, wd, kernels):
+        fetch, write = per_kernel(fd, "FETCH_SIZE"), per_kernel(wd, "WRITE_SIZE")
+        f_copy, _ = pick(fetch, "copyBuffer", "max")
+        w_copy, _ = pick(write, "copyBuffer", "max")
+        f_scale, w_scale = f_copy * 1024 / COPY_BYTES, w_copy * 1024 / COPY_BYTES
+        lines = [f"Calibration: the {COPY_BYTES >> 20} MiB device copy (__amd_rocclr_copyBuffer) reads "
+                 f"FETCH_SIZE {f_copy:.0f} KiB and WRITE_SIZE {w_copy:.0f} KiB, i.e. "
+                 f"{f_scale:.3f} and {w_scale:.3f} counted bytes per byte moved; the figures below are "
+                 "divided by these factors.",
+                 "",
+                 "| kernel | workgroups | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes per launch |",
+                 "|---|---|---|---|---|---|"]
+        result = {}
+        for label, key, grid in kernels:
+            try:
+                fv, n = pick(fetch, key, grid)
+                wv, _ = pick(write, key, grid)
+            except (ValueError, statistics.StatisticsError):
+                continue
+            b = fv * 1024 / f_scale + wv * 1024 / w_scale
+            result[label] = b
+            shown = {None: "all", "max": "largest"}.get(grid, grid)
+            lines.append(f"| {label} | {shown} | {n} | {fv:.0f} | {wv:.0f} | "
+                         f"{b / 1e6:.1f} MB |")
+        return lines, result
+
+    def cmds(fd, wd, mode):
+        arg = "" if mode == "step" else " long"
+        return [f"    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc FETCH_SIZE -d <repo>/{fd} "
+                f"-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver{arg}",
+                f"    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc WRITE_SIZE -d <repo>/{wd} "
+                f"-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver{arg}"]
+
+    lines = ["# HBM traffic of the step's kernels, v0.2 unit with an 8-unit history (and the long-history "
+             "video launch)",
              "",
-             "Counters per dispatch (median over the driver's dispatches of each kernel), from two",
-             "runs of the same committed program, one counter each (from the repository root):",
-             "",
-             f"    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc FETCH_SIZE -d <repo>/{fetch_dir} "
-             "-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver",
-             f"    cd /tmp && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -d <repo>/{write_dir} "
-             "-o pmc -f csv -- python3 <repo>/bench.py --pmc-driver",
-             f"    python3 bench.py --pmc-summary {fetch_dir} {write_dir}",
-             "",
-             f"Calibration: the {COPY_BYTES >> 20} MiB device copy (__amd_rocclr_copyBuffer) reads "
-             f"FETCH_SIZE {f_copy:.0f} KiB and WRITE_SIZE {w_copy:.0f} KiB, i.e. "
-             f"{f_scale:.3f} and {w_scale:.3f} counted bytes per byte moved; the figures below are "
-             "divided by these factors.",
-             "",
-             "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes per launch |",
-             "|---|---|---|---|---|"]
-    result = {}
-    for label, key in (("unit_attn_kernel", "unit_attn_kernel"), ("video_combine_kernel", "video_combine"),
-                       ("audio_attn_kernel", "audio_attn_kernel"), ("combine_kernel (audio)", "combine_kernel<"),
-                       ("kv_append_kernel", "kv_append_kernel")):
-        try:
-            fv, n = pick(fetch, key)
-            wv, _ = pick(write, key)
-        except (ValueError, statistics.StatisticsError):
-            continue
-        b = fv * 1024 / f_scale + wv * 1024 / w_scale
-        result[label] = b
-        lines.append(f"| {label} | {n} | {fv:.0f} | {wv:.0f} | {b / 1e6:.1f} MB |")
+             "Counters per dispatch (median over the driver's dispatches of each kernel and grid), "
+             "from runs of committed programs, one counter each (from the repository root):",
+             ""] + cmds(fetch_dir, write_dir, "step")
+    if long_fetch:
+        lines += cmds(long_fetch, long_write, "long")
+    lines += [f"    python3 bench.py --pmc-summary {fetch_dir} {write_dir}"
+              + (f" {long_fetch} {long_write}" if long_fetch else ""),
+              "",
+              "## The v0.2 step (256 + 9 x 920 video keys)",
+              "",
+              "The step driver runs three steps (ws_step_append, then ws_step_attention with the audio "
+              "rows riding in the video kernel and the audio kernel over the 9 audio-token pages, 80 "
+              "workgroups), then the video and the audio attention three times each as separate calls "
+              "(the audio kernel over all 8572 keys, 480 workgroups).  unit_attn_kernel is the median "
+              "over both kinds of launch.",
+              ""]
+    t, result = table(fetch_dir, write_dir, (
+        ("unit_attn_kernel", "unit_attn_kernel", 256),
+        ("step_combine_kernel", "step_combine", None),
+        ("video_combine_kernel", "video_combine", None),
+        ("audio_attn_kernel (all pages)", "audio_attn_kernel", 480),
+        ("audio_attn_kernel (audio pages)", "audio_attn_kernel", 80),
+        ("combine_kernel (audio)", "::combine_kernel(", None),
+        ("kv_append_kernel (the step's)", "kv_append_kernel", "max")))
+    lines += t
     lk_v = COND + (HIST + 1) * LU
     kv_bytes = 2.0 * lk_v * H * D * 2
     lines += ["",
               f"Video K/V visible to one launch: {kv_bytes / 1e6:.1f} MB (each (head, page) tile is "
               "read by the four query-tile workgroups; pages the 256 MB cache already holds are not "
-              "fetched from HBM again).",
-              "",
+              "fetched from HBM again)."]
+    if long_fetch:
+        lk_l = COND + (LONG_HIST + 1) * LU
+        kv_l = 2.0 * lk_l * H * D * 2
+        t, res_l = table(long_fetch, long_write, (("unit_attn_kernel", "unit_attn_kernel", 256),
+                                                  ("video_combine_kernel", "video_combine", None),
+                                                  ("kv_append_kernel (the step's)", "kv_append_kernel", "max")))
+        lines += ["", f"## Long history ({lk_l} video keys)", ""] + t
+        b = res_l.get("unit_attn_kernel")
+        if b:
+            lines += ["", f"Video K/V visible to one launch: {kv_l / 1e6:.1f} MB; unit_attn_kernel moves "
+                          f"{b / kv_l:.2f}x that."]
+    lines += ["",
               f"kernels_sha256: {kernels_sha256()}",
               f"unit_attn_traffic_bytes: {result.get('unit_attn_kernel', float('nan')):.0f}"]
     print("\n".join(lines))
 
 
-def pmc_driver(ws, cache, step, u, q_v, out_v, q_a, out_a, vpos, apos, gamma, eps):
+MFMA_COUNTERS = ("GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CYCLES "
+                 "SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_INSTS_VALU SQ_LDS_BANK_CONFLICT SQ_WAVES")
+
+
+def mfma_summary(d):
+    """MFMA utilisation of unit_attn_kernel (256 workgroups) from one counter
+    run of the step driver: per dispatch, median over the dispatches.
+    GRBM_GUI_ACTIVE comes summed over the 8 XCDs; MfmaUtil is
+    SQ_VALU_MFMA_BUSY_CYCLES / (per-XCD GRBM_GUI_ACTIVE x 1024 SIMDs) and the
+    MFMA FLOP are SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (the counter
+    definitions of rocprofiler-sdk for gfx950)."""
+    import csv
+    import glob
+    import statistics
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    disp = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if "unit_attn_kernel" not in r["Kernel_Name"]:
+                continue
+            if int(r["Grid_Size"]) // max(1, int(r["Workgroup_Size"])) != 256:
+                continue
+            e = disp.setdefault((f, r["Dispatch_Id"]), {"us": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3})
+            e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    if not disp:
+        raise SystemExit("no unit_attn_kernel dispatch in the counters")
+
+    def med(key):
+        return statistics.median(e[key] for e in disp.values() if key in e)
+
+    us = med("us")
+    grbm = med("GRBM_GUI_ACTIVE") / 8
+    busy = med("SQ_VALU_MFMA_BUSY_CYCLES")
+    flop = med("SQ_INSTS_VALU_MFMA_MOPS_BF16") * 512
+    lk_v = COND + (HIST + 1) * LU
+    alg = video_flop(LU, lk_v)
+    rows = [("dispatches", f"{len(disp)}"),
+            ("duration (counter run, median)", f"{us:.1f} us"),
+            ("GRBM_GUI_ACTIVE per XCD", f"{grbm:.0f} cycles ({grbm / us / 1e3:.2f} GHz over the duration)"),
+            ("SQ_VALU_MFMA_BUSY_CYCLES", f"{busy:.0f}"),
+            ("MfmaUtil", f"{100 * busy / (grbm * 1024):.1f} %"),
+            ("MFMA FLOP (MOPS_BF16 x 512)", f"{flop:.4g} ({flop / alg:.3f}x the {alg:.4g} algorithmic)"),
+            ("MFMA TFLOP/s over the duration", f"{flop / (us * 1e-6) / 1e12:.0f}"),
+            ("SQ_INSTS_VALU", f"{med('SQ_INSTS_VALU'):.0f}"),
+            ("SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES", f"{med('SQ_WAIT_INST_ANY') / med('SQ_WAVE_CYCLES'):.3f}"),
+            ("SQ_BUSY_CYCLES", f"{med('SQ_BUSY_CYCLES'):.0f}"),
+            ("SQ_LDS_BANK_CONFLICT", f"{med('SQ_LDS_BANK_CONFLICT'):.0f}"),
+            ("SQ_WAVES", f"{med('SQ_WAVES'):.0f}")]
+    lines = ["# MFMA utilisation: unit_attn_kernel, v0.2 unit with an 8-unit history",
+             "",
+             "One counter run of the step driver (three ws_step_attention steps, then three separate "
+             "video calls), from the repository root:",
+             "",
+             f"    cd /tmp && timeout -s KILL 240 rocprofv3 --pmc {MFMA_COUNTERS} -d <repo>/{d} -o pmc "
+             "-f csv -- python3 <repo>/bench.py --pmc-driver",
+             f"    python3 bench.py --mfma-summary {d}",
+             "",
+             "| quantity | value |", "|---|---|"] + [f"| {a} | {b} |" for a, b in rows] + [
+             "", f"kernels_sha256: {kernels_sha256()}"]
+    print("\n".join(lines))
+
+
+def pmc_driver(mode, ws, cache, step, u, q_v, out_v, q_a, out_a, sets, gamma, eps, dev):
     import torch
-    step(u, False)
-    torch.cuda.synchronize()
-    vmask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
-    amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
-    for _ in range(3):
-        cache.unit_attention(q_v, out_v, vmask, ws.WS_QUERY_PREPARED)
+    if mode == "long":
+        lcache, one_step = long_setup(ws, sets, gamma, eps, dev)
+        one_step(0, attention=False)
         torch.cuda.synchronize()
-    for _ in range(3):
-        cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
-        torch.cuda.synchronize()
-    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=q_v.device)
+        for _ in range(3):
+            one_step(0)
+            torch.cuda.synchronize()
+        lcache.close()
+        what = "3 long-history steps"
+    else:
+        for k in range(3):
+            step(u + k, False)
+            torch.cuda.synchronize()
+        u += 2
+        vmask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
+        amask = ws.mask_spec(u, u - HIST, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO))
+        for _ in range(3):
+            cache.unit_attention(q_v, out_v, vmask, ws.WS_QUERY_PREPARED)
+            torch.cuda.synchronize()
+        for _ in range(3):
+            cache.audio_attention(q_a, out_a, amask, ws.WS_QUERY_PREPARED)
+            torch.cuda.synchronize()
+        what = "3 steps, 3 video, 3 audio"
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
     for _ in range(3):
         dst.copy_(src)
         torch.cuda.synchronize()
-    log("pmc driver: 1 step, 3 video, 3 audio, 3 copies of", COPY_BYTES >> 20, "MiB")
+    log(f"pmc driver: {what}, 3 copies of", COPY_BYTES >> 20, "MiB")
 
 
 def measured_peaks(ws, torch, stream, dev):
@@ -551,7 +700,12 @@ def measured_peaks(ws, torch, stream, dev):
 
 def main():
     args = parse()
+    if args.mfma_summary:
+        mfma_summary(args.mfma_summary)
+        return
     if args.pmc_summary:
+        if len(args.pmc_summary) not in (2, 4):
+            raise SystemExit("--pmc-summary takes 2 or 4 directories")
         pmc_summary(*args.pmc_summary)
         return
     if args.cpu_v01_point:
@@ -648,7 +802,7 @@ def main():
 
     u = HIST
     if args.pmc_driver:
-        pmc_driver(ws, cache, step, u, q_v, out_v, q_a, out_a, vpos, apos, gamma, eps)
+        pmc_driver(args.pmc_driver, ws, cache, step, u, q_v, out_v, q_a, out_a, sets, gamma, eps, dev)
         cache.close()
         return
     for _ in range(args.warmup):

@@ -175,9 +175,9 @@ typedef enum ws_option {
    * bound |q''| * max |k| when it is at most 40 in log2 units, else a lazily
    * raised running maximum), 1 = always the running maximum. */
   WS_OPT_VIDEO_RUNNING_MAX = 2,
-  /* ws_unit_attention_groups: 0 = every query group is partitioned as if
-   * it had all CUs (several rounds of workgroups in one launch), 1 = the
-   * groups share one round of the CUs in proportion to their work. */
+  /* ws_unit_attention_groups: 0 = the query groups share one round of the
+   * CUs in proportion to their work, 1 = every group is partitioned as if it
+   * had all CUs (several rounds of workgroups in one launch). */
   WS_OPT_VIDEO_CLASS_CUS = 3,
   /* ws_step_attention: 0 = the audio rows ride in the video kernel when the
    * step allows it (see there), 1 = always the separate audio kernel. */

@@ -118,7 +118,7 @@ struct ws_cache {
   int32_t opt_video_splits = 0;
   int32_t opt_audio_splits = 0;
   int32_t opt_running_max = 0;
-  int32_t opt_class_cus = 0;  // 0: each query class sized for all CUs, 1: classes share the CUs
+  int32_t opt_class_cus = 0;  // 0: classes share one round of the CUs, 1: each sized for all CUs
   int32_t opt_separate_audio = 0;  // 1: ws_step_attention never lets audio rows ride in the video kernel
   float* knorm2 = nullptr;  // [max_pages][H] squared key-norm maxima
   uint16_t* zeros = nullptr;  // 1 KB of zeros (direct-load source of empty blocks)
@@ -561,12 +561,12 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
     plan->part_rows = static_cast<int64_t>(splits) * H * n_q;
   } else {
     // Per class: query tiles, and groups of workgroups sharing the class's
-    // (head, page) units.  Every class is partitioned as if it had all CUs,
-    // so a call with several classes runs several rounds of workgroups (with
-    // a measured catch-up of three 920-query units over 8536 keys each:
-    // 532 us against 597 us when the classes share one round in proportion
-    // to their work, and 573 us for three separate calls); the option
-    // selects the shared round.
+    // (head, page) units.  The classes share one round of the CUs in
+    // proportion to their work (a catch-up of three 920-query units over
+    // 8536 keys each, measured with the clocks settled: 480 us, against 500
+    // us when every class is partitioned as if it had all CUs and the
+    // launch runs several rounds of workgroups; the option selects the
+    // latter).
     int64_t work = 0;
     for (int k = 0; k < n_cls; ++k) {
       a.cls[k].n_qtiles = (a.cls[k].n_q + ws::kVideoQTile - 1) / ws::kVideoQTile;
@@ -578,7 +578,7 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
     for (int k = 0; k < n_cls; ++k) {
       ws::AttnClass& cl = a.cls[k];
       const int64_t w = static_cast<int64_t>(cl.n_qtiles) * cl.n_pages;
-      const int cus = c->opt_class_cus != 1 || n_cls == 1 || work == 0
+      const int cus = c->opt_class_cus == 1 || n_cls == 1 || work == 0
                           ? c->num_cus
                           : static_cast<int>(std::max<int64_t>(cl.n_qtiles, c->num_cus * w / work));
       cl.n_groups = choose_video_groups(c, H, cl.n_qtiles, cl.n_pages, cus);

@@ -104,23 +104,23 @@ def test_groups_equal_separate_calls_with_one_range_per_head(ws):
         cache.close()
 
 
-@pytest.mark.parametrize("splits,shared", [(0, 0), (3, 0), (0, 1)])
-def test_ragged_groups_against_oracle(ws, splits, shared):
+@pytest.mark.parametrize("splits,all_cus", [(0, 0), (3, 0), (0, 1)])
+def test_ragged_groups_against_oracle(ws, splits, all_cus):
     """Group sizes that end inside query tiles (1, 33, 257, 128) and a group
     whose window hides all but the conditioning slice, with the automatic and
-    a forced key-range split, and with the groups sharing one round of the
-    CUs, against the oracle."""
+    a forced key-range split, and with every group partitioned as if it had
+    all CUs, against the oracle."""
     H, grid = 4, (5, 7)
     cache, oc, rng, keep = _build(ws, H, grid, 10, 6, 53)
     try:
         if splits:
             cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, splits)
-        cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, shared)
+        cache.set_option(ws.WS_OPT_VIDEO_CLASS_CUS, all_cus)
         spec = [(5, -1, 0b011, 1), (3, 2, 0b011, 33), (5, 9, 0b011, 257), (1, -1, 0b011, 128)]
         q, pos = _queries(rng, H, spec, grid)
         got = bf16_f64(_run_groups(ws, cache, q, pos, spec, H))
         ref, _ = oracle.unit_attention_groups(oc, q, spec, positions=pos, gamma=np.ones(128), eps=1e-6)
-        print(assert_gates(got, ref, label=f"ragged groups, splits={splits}, shared={shared}"))
+        print(assert_gates(got, ref, label=f"ragged groups, splits={splits}, all_cus={all_cus}"))
     finally:
         cache.close()
 
