@@ -331,18 +331,19 @@ typedef struct ws_attn_call {
  * Audio rows riding in the video kernel: when the audio call is
  * WS_QUERY_PREPARED, every page the video call sees is visible to the audio
  * call too, and the audio rows fit the spare rows of the video call's last
- * 256-query tile (n_audio <= 256 * ceil(n_video / 256) - n_video), the
- * video kernel also computes the audio rows over
- * the video call's pages (the pages are streamed once for both), and the
- * audio kernel walks only the pages the audio call alone sees (the unit
- * audio tokens); the merge folds both.  WS_OPT_STEP_SEPARATE_AUDIO turns
- * this off.  The video output always equals what ws_unit_attention(video)
- * writes, bit for bit; the audio output equals ws_audio_attention(audio) bit
- * for bit when the rows do not ride, and otherwise differs from it only in
- * the order of fp32 sums.  With timing enabled the call records two ring
- * entries: the video kernel (merge time 0), and the audio kernel with the
- * shared merge (path 1; path 5 when the audio rows ride, with the audio
- * kernel's range count, 0 when it had no pages to walk and was not launched). */
+ * 256-query tile (n_audio <= 256 * ceil(n_video / 256) - n_video), the video
+ * kernel also computes the audio rows over the video call's pages (the pages
+ * are streamed once for both), and the audio kernel walks only the pages the
+ * audio call alone sees (the units' audio tokens); the merge folds both.
+ * WS_OPT_STEP_SEPARATE_AUDIO turns this off.  The video output always equals
+ * what ws_unit_attention(video) writes, bit for bit; the audio output equals
+ * ws_audio_attention(audio) bit for bit when the rows do not ride, and
+ * otherwise agrees with it to the rounding of the bf16 softmax weights (taken
+ * under another shift) and the order of fp32 sums.  With timing
+ * enabled the call records two ring entries: the video kernel (merge time 0),
+ * and the audio kernel with the shared merge (path 1; path 5 when the audio
+ * rows ride, with the audio kernel's range count, 0 when it had no pages to
+ * walk and was not launched). */
 WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, const ws_attn_call* audio,
                                    void* hip_stream);
 
@@ -353,10 +354,11 @@ WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, c
  * object (32 MiB per device, kept until the process ends) instead of the
  * cache's workspaces.  The call itself allocates nothing.
  * Limit: the partials of both calls must fit the 32 MiB: video (ranges per
- * head) x H x n_q rows of 260 bytes, audio (key ranges) x H x n_q rows of
+ * head) x H x n_q rows of 260 bytes, audio (key ranges, plus the video
+ * kernel's ranges of the audio rows when they ride in it) x H x n_q rows of
  * 516 bytes, each region rounded up to 256 bytes; a larger step returns
  * WS_ERR_SHAPE before anything is enqueued.  (The v0.2 unit at 640x368 with
- * an 8-unit window needs about 30 MB.)  Every call on a device shares that
+ * an 8-unit window needs about 29 MB.)  Every call on a device shares that
  * device's workspace: calls that overlap in time on one device (different
  * streams, or different threads) race and must be ordered by the caller.
  * Nothing in it has to start at zero: each call writes every partial row it
