@@ -1496,9 +1496,9 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
 
 // ------------------------------------------------------------------------- //
 // combine (audio key ranges): 16 threads per (head, query) row, 8 d each, 16
-// rows per block.  A thread requests the log-sum-exp and its 8 values of
-// kMergeBatch ranges before using any (one memory round trip per batch),
-// then folds them with a running maximum.  The batch sets the registers a
+// rows per block.  A thread reads the row's log-sum-exps, then requests the
+// 8 values of kMergeBatch ranges before using any (one memory round trip per
+// batch) and folds them against the largest.  The batch sets the registers a
 // thread holds: the audio call's own merge takes 16 ranges at once; inside
 // the merge launch of a step, whose video rows need few registers, 3 (more
 // would cap the occupancy of the video rows' blocks).
@@ -1517,9 +1517,20 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   }
   const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
-  float mx = kNegInf, wsum = 0.f;
+  // The largest log-sum-exp first: every range is then weighted the same way
+  // whatever the batch, so the step's merge launch and the audio call's own
+  // give the same bits.
+  float mx = kNegInf;
+  for (int sp0 = 0; sp0 < n_splits; sp0 += 16) {
+    float lb[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) lb[i] = sp0 + i < n_splits ? a.part_lse[(sp0 + i) * split_stride + row] : kNegInf;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, lb[i]);
+  }
+  float wsum = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int sp0 = 0; sp0 < n_splits; sp0 += kMergeBatch) {
+  for (int sp0 = 0; sp0 < n_splits && mx != kNegInf; sp0 += kMergeBatch) {
     float lb[kMergeBatch];
     f32x4 o0[kMergeBatch], o1[kMergeBatch];
 #pragma unroll
@@ -1531,17 +1542,9 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
       o0[i] = ok ? *reinterpret_cast<const f32x4*>(po) : (f32x4){0.f, 0.f, 0.f, 0.f};
       o1[i] = ok ? *reinterpret_cast<const f32x4*>(po + 4) : (f32x4){0.f, 0.f, 0.f, 0.f};
     }
-    float bm = mx;
-#pragma unroll
-    for (int i = 0; i < kMergeBatch; ++i) bm = fmaxf(bm, lb[i]);
-    if (bm == kNegInf) continue;
-    const float sc = fast_exp2(mx - bm);  // 0 while nothing was folded yet
-    wsum *= sc;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] *= sc;
 #pragma unroll
     for (int i = 0; i < kMergeBatch; ++i) {
-      const float w = lb[i] == kNegInf ? 0.f : fast_exp2(lb[i] - bm);
+      const float w = lb[i] == kNegInf ? 0.f : fast_exp2(lb[i] - mx);
       wsum += w;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -1549,7 +1552,6 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
         acc[4 + k] += w * o1[i][k];
       }
     }
-    mx = bm;
   }
   const float inv = mx != kNegInf ? 1.0f / wsum : 0.f;
   u32x4 w;
@@ -1637,13 +1639,14 @@ __global__ __launch_bounds__(256) void video_combine_kernel(const CombineArgs a)
 }
 
 // The merges of one step's video and audio calls in one launch: blocks below
-// n_video merge video rows, the rest audio rows.
+// n_audio merge audio rows (they start first: their rows fold more ranges),
+// the rest video rows.
 __global__ __launch_bounds__(256) void step_combine_kernel(const CombineArgs v, const CombineArgs au,
-                                                           int n_video) {
-  if (static_cast<int>(blockIdx.x) < n_video)
-    video_combine_block(v, combine_class_table(), blockIdx.x);
+                                                           int n_audio) {
+  if (static_cast<int>(blockIdx.x) < n_audio)
+    combine_block<3>(au, blockIdx.x);
   else
-    combine_block<4>(au, blockIdx.x - n_video);
+    video_combine_block(v, combine_class_table(), blockIdx.x - n_audio);
 }
 
 }  // namespace
@@ -1695,7 +1698,7 @@ hipError_t launch_step_combine(const CombineArgs& v, const CombineArgs& au, hipS
   const int n_video = v.n_groups > 0 ? (v.num_heads * v.n_q + 15) / 16 : 0;
   const int n_audio = au.num_heads > 0 ? (au.num_heads * au.n_q + 15) / 16 : 0;
   if (n_video + n_audio == 0) return hipSuccess;
-  hipLaunchKernelGGL(step_combine_kernel, dim3(n_video + n_audio), dim3(256), 0, stream, v, au, n_video);
+  hipLaunchKernelGGL(step_combine_kernel, dim3(n_video + n_audio), dim3(256), 0, stream, v, au, n_audio);
   return hipGetLastError();
 }
 

@@ -58,6 +58,10 @@ using ws_internal::hip_fail;
 using ws::kMaxVideoSplits;
 // Blocks per CU of an append launch; each loops over the launch's tiles.
 constexpr int kAppendBlocksPerCu = 4;
+// Pages per key range of the audio kernel when the step's audio rows ride in
+// the video kernel and it walks only the audio-token pages (one page per
+// wave: measured 1.5 us faster per step than two).
+constexpr int kRiderPagesPerRange = 4;
 constexpr int kMaxAudioSplits = 512;
 using ws::kMaxAudioQ;
 
@@ -748,7 +752,10 @@ bool plan_riders(ws_cache* c, const ws_attn_call* video, const ws_attn_call* aud
   }
   int splits = 0, pps = 0;
   if (n_extra > 0) {
-    splits = choose_audio_splits(c, pa.a.n_qtiles * H, n_extra);
+    // few pages (latency-bound): as many ranges as give each wave of the
+    // audio kernel at most kRiderPagesPerRange / 4 pages
+    splits = c->opt_audio_splits > 0 ? c->opt_audio_splits
+                                     : (n_extra + kRiderPagesPerRange - 1) / kRiderPagesPerRange;
     splits = std::max(1, std::min(splits, n_extra));
     pps = (n_extra + splits - 1) / splits;
     splits = (n_extra + pps - 1) / pps;
