@@ -1184,6 +1184,8 @@ __device__ __forceinline__ const_class_table class_table() {
   return (const_class_table)(seg + offsetof(AttnArgs, cls));
 }
 
+__device__ __forceinline__ void rider_pages_wave(const AttnArgs& a, int head, int range0, int k, int n);
+
 __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnArgs a) {
   // Work decode.  Each query class (the rows of one unit's queries, with the
   // pages its mask leaves visible) owns a block of workgroups: n_groups
@@ -1216,6 +1218,23 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
   }
   const VideoPartition part{a.num_heads, n_pages, a.seg_cost, tab[ci].n_groups};
   const int64_t lo = video_group_lo(part, group), hi = video_group_lo(part, group + 1);
+  // The rider rows' own pages: in the last query tile's workgroup of the
+  // group that holds a head's last page, the waves without rows of their
+  // own (the last rx_waves of the 8) attend them for that head before they
+  // join the page loop (where such waves only stage pages), as key ranges
+  // after the head's ranges of the shared pages.
+  if (a.rx_pages > 0 && local % n_qtiles == n_qtiles - 1 && lo < hi) {
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int k = wave - (kVideoWaves - a.rx_waves);
+    if (k >= 0) {
+      for (int64_t head = lo / n_pages; head <= (hi - 1) / n_pages; ++head) {
+        const int64_t h0 = head * n_pages;
+        if (video_group_of(part, h0 + n_pages - 1) != group) continue;
+        rider_pages_wave(a, static_cast<int>(head), static_cast<int>(group - video_group_of(part, h0) + 1), k,
+                         a.rx_waves);
+      }
+    }
+  }
   bool first = true;
   for (int64_t x = lo; x < hi; first = false) {
     const int64_t head = x / n_pages, h0 = head * n_pages;
@@ -1276,6 +1295,156 @@ __device__ __forceinline__ void audio_load_v(u32x4 (&v)[8][2], const uint16_t* v
     const int step = ok ? v_tile_index(0, 16) : 0;  // next 16 d
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) v[dt][c] = *reinterpret_cast<const u32x4*>(src + step * dt);
+  }
+}
+
+// The page loop of the audio path, one wave: pages p_begin, p_begin + step,
+// ... (< p_end) of the list, whose first page's operands kreg and vreg hold
+// on entry.  Accumulates O^T (o), the running maximum and the row sum of the
+// wave's 16 query columns (m_run and l_run as set up by the caller: the
+// fixed shift, or -inf for a running maximum).
+//
+// Each page's K registers are reloaded (for the wave's next page) as soon as
+// its S products are issued, and its V^T registers as soon as the P*V
+// products are, so both loads of a page are in flight while the wave waits on
+// the one before it.
+__device__ __forceinline__ void audio_page_loop(const_page_list pages, int p_begin, int p_end, int step,
+                                                const uint16_t* kpool, const uint16_t* vpool, int64_t page_stride,
+                                                const uint16_t* zeros, const bf16x8 (&qreg)[4], bool fixed_shift,
+                                                u32x4 (&kreg)[4][4], u32x4 (&vreg)[8][2], int g, int i16, int lane,
+                                                f32x4 (&o)[8], float& m_run, float& l_run) {
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  for (int pi = p_begin; pi < p_end; pi += step) {
+    const int n_valid = pages[pi].y;
+    int2 nxt = make_int2(0, 0);  // past the last page: zeros
+    if (pi + step < p_end) nxt = make_int2(pages[pi + step].x, pages[pi + step].y);
+    // S^T of the page's four key tiles
+    f32x4 sacc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      sacc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[t][s]), qreg[s], sacc[t], 0, 0, 0);
+    }
+    audio_load_k(kreg, kpool + nxt.x * page_stride, zeros, nxt.y, g, i16, lane);
+    if (n_valid < kPageTokens) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (audio_key(t, 4 * g + r) >= n_valid) sacc[t][r] = kNegInf;
+    }
+    float alpha = 1.f;
+    if (!fixed_shift) {
+      float mx = kNegInf;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) mx = fmaxf(mx, fmaxf(fmaxf(sacc[t][0], sacc[t][1]), fmaxf(sacc[t][2], sacc[t][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
+      m_run = m_new;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+    }
+    const float m_use = m_run == kNegInf ? 0.f : m_run;
+    // P in bf16 (word c of chunk c: keys 32 c + 8 g + 0..7); the row sum is
+    // taken over the same bf16 values the MFMAs consume
+    u32x4 pw[2];
+    float psum = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4& sc = sacc[2 * c + h];
+        const uint32_t w0 = pack_bf16(fast_exp2(sc[0] - m_use), fast_exp2(sc[1] - m_use));
+        const uint32_t w1 = pack_bf16(fast_exp2(sc[2] - m_use), fast_exp2(sc[3] - m_use));
+        pw[c][2 * h] = w0;
+        pw[c][2 * h + 1] = w1;
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones, psum, false);
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vreg[dt][c]), as_bf16x8(pw[c]), o[dt], 0, 0, 0);
+    audio_load_v(vreg, vpool + nxt.x * page_stride, zeros, nxt.y, g, i16, lane);
+  }
+}
+
+// The rider rows over their own pages (entries rx_page0 .. rx_page0 + rx_pages
+// of the page list) for one head, inside the video kernel: the audio path's
+// page loop on all 8 waves (wave w takes pages w, w + 8, ...), 16 rider rows
+// at a time, merged across the waves through the (then idle) LDS stages and
+// written as key range `range` of the rows' fp32 partials.
+// The rider rows over their own pages (entries rx_page0 .. rx_page0 + rx_pages
+// of the page list) for one head, by one wave of the video kernel that has no
+// rows of its own: the audio path's page loop over pages k, k + n, ... of
+// them (wave k of n such waves), 16 rider rows at a time, each written as a
+// key range of its own (range0 + k) of the rows' fp32 partials.  No LDS and
+// no barrier: the wave does this before its first page barrier, while the
+// waves with rows run their first segment's prologue.
+__device__ __forceinline__ void rider_pages_wave(const AttnArgs& a, int head, int range0, int k, int n) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, i16 = lane & 15;
+  const_page_list pages = page_list(a);
+  const int64_t page_stride = static_cast<int64_t>(a.num_heads) * kPageHeadElems;
+  const uint16_t* kpool = a.kpool + head * kPageHeadElems;
+  const uint16_t* vpool = a.vpool + head * kPageHeadElems;
+  const int p_begin = a.rx_page0 + k, p_end = a.rx_page0 + a.rx_pages;
+  const int64_t row0 = (static_cast<int64_t>(range0 + k) * a.num_heads + head) * a.n_rq;
+  for (int q0 = 0; q0 < a.n_rq; q0 += kAudioQTile) {
+    u32x4 kreg[4][4], vreg[8][2];
+    {
+      int2 pg = make_int2(0, 0);
+      if (p_begin < p_end) pg = make_int2(pages[p_begin].x, pages[p_begin].y);
+      audio_load_k(kreg, kpool + pg.x * page_stride, a.zeros, pg.y, g, i16, lane);
+      audio_load_v(vreg, vpool + pg.x * page_stride, a.zeros, pg.y, g, i16, lane);
+    }
+    const int q = q0 + i16;
+    const bool q_ok = q < a.n_rq;
+    bf16x8 qreg[4];
+    const uint16_t* qp = a.rq + q * a.rq_tok_stride + head * a.rq_head_stride + 8 * g;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      qreg[s] = as_bf16x8(q_ok ? *reinterpret_cast<const u32x4*>(qp + 32 * s) : (u32x4){0u, 0u, 0u, 0u});
+    // softmax shift as in the audio kernel, over the wave's pages
+    float kn2 = 0.f;
+    for (int pi = p_begin + n * lane; pi < p_end; pi += 64 * n)
+      kn2 = fmaxf(kn2, a.knorm2[static_cast<int64_t>(pages[pi].x) * a.num_heads + head]);
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) kn2 = fmaxf(kn2, __shfl_xor(kn2, off));
+    float qn2 = 0.f;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const u32x4 w = __builtin_bit_cast(u32x4, qreg[s]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) qn2 += bf16_lo(w[j]) * bf16_lo(w[j]) + bf16_hi(w[j]) * bf16_hi(w[j]);
+    }
+    qn2 += __shfl_xor(qn2, 16);
+    qn2 += __shfl_xor(qn2, 32);
+    const float bound = sqrtf(qn2 * kn2);
+    const bool fixed_shift = a.fixed_shift != 0 && __all(bound <= kShiftBoundMax);
+    float m_run = fixed_shift ? bound : kNegInf, l_run = 0.f;
+    f32x4 o[8];
+    audio_page_loop(pages, p_begin, p_end, n, kpool, vpool, page_stride, a.zeros, qreg, fixed_shift, kreg, vreg,
+                    g, i16, lane, o, m_run, l_run);
+    // lane holds O^T[16 dt + 4 g + r][q] of the wave's pages
+    float l_w = l_run + __shfl_xor(l_run, 16);
+    l_w += __shfl_xor(l_w, 32);
+    if (q_ok) {
+      const float inv = l_w > 0.f ? 1.0f / l_w : 0.f;
+      float* po = a.rpart_o + (row0 + q) * kHeadDim;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+        *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * g) = o[dt] * inv;
+      if (g == 0) a.rpart_lse[row0 + q] = l_w > 0.f ? m_run + __log2f(l_w) : kNegInf;
+    }
   }
 }
 
@@ -1382,73 +1551,8 @@ __global__ __launch_bounds__(256, 2) void audio_attn_kernel(const AttnArgs a) {
   float m_run = fixed_shift ? bound : kNegInf, l_run = 0.f;
 
   f32x4 o[8];
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-
-  // Each page's K operands are reloaded (for the wave's next page) as soon
-  // as its S products are issued, and its V^T operands as soon as the P*V
-  // products are, so both loads of a page are in flight while the wave waits
-  // on the one before it.
-  for (int pi = p_begin; pi < p_end; pi += 4) {
-    const int n_valid = pages[pi].y;
-    int2 nxt = make_int2(0, 0);  // past the last page: zeros
-    if (pi + 4 < p_end) nxt = make_int2(pages[pi + 4].x, pages[pi + 4].y);
-    // S^T of the page's four key tiles
-    f32x4 sacc[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      sacc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[t][s]), qreg[s], sacc[t], 0, 0, 0);
-    }
-    audio_load_k(kreg, kpool + nxt.x * page_stride, a.zeros, nxt.y, g, i16, lane);
-    if (n_valid < kPageTokens) {
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (audio_key(t, 4 * g + r) >= n_valid) sacc[t][r] = kNegInf;
-    }
-    float alpha = 1.f;
-    if (!fixed_shift) {
-      float mx = kNegInf;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) mx = fmaxf(mx, fmaxf(fmaxf(sacc[t][0], sacc[t][1]), fmaxf(sacc[t][2], sacc[t][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
-      m_run = m_new;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
-    }
-    const float m_use = m_run == kNegInf ? 0.f : m_run;
-    // P in bf16 (word c of chunk c: keys 32 c + 8 g + 0..7); the row sum is
-    // taken over the same bf16 values the MFMAs consume
-    u32x4 pw[2];
-    float psum = 0.f;
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const f32x4& sc = sacc[2 * c + h];
-        const uint32_t w0 = pack_bf16(fast_exp2(sc[0] - m_use), fast_exp2(sc[1] - m_use));
-        const uint32_t w1 = pack_bf16(fast_exp2(sc[2] - m_use), fast_exp2(sc[3] - m_use));
-        pw[c][2 * h] = w0;
-        pw[c][2 * h + 1] = w1;
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones, psum, false);
-      }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vreg[dt][c]), as_bf16x8(pw[c]), o[dt], 0, 0, 0);
-    audio_load_v(vreg, vpool + nxt.x * page_stride, a.zeros, nxt.y, g, i16, lane);
-  }
+  audio_page_loop(pages, p_begin, p_end, 4, kpool, vpool, page_stride, a.zeros, qreg, fixed_shift, kreg, vreg,
+                  g, i16, lane, o, m_run, l_run);
 
   // merge the four waves: lane holds O^T[16 dt + 4 g + r][q] of its keys
   float l_w = l_run + __shfl_xor(l_run, 16);
@@ -1513,7 +1617,8 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   if (a.r_groups > 0) {  // the ranges the video kernel wrote for rider rows
     const VideoPartition part{a.num_heads, a.r_pages, a.seg_cost, a.r_groups};
     const int64_t h0 = static_cast<int64_t>(head) * a.r_pages;
-    n_splits += static_cast<int>(video_group_of(part, h0 + a.r_pages - 1) - video_group_of(part, h0) + 1);
+    n_splits += static_cast<int>(video_group_of(part, h0 + a.r_pages - 1) - video_group_of(part, h0) + 1) +
+                a.r_extra;  // and those of the rows' own pages
   }
   const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;

@@ -58,6 +58,9 @@ using ws_internal::hip_fail;
 using ws::kMaxVideoSplits;
 // Blocks per CU of an append launch; each loops over the launch's tiles.
 constexpr int kAppendBlocksPerCu = 4;
+// Fewest waves without rows in the video call's last query tile (with the
+// audio rows) for the video kernel to attend the audio rows' own pages.
+constexpr int kRiderMinIdleWaves = 2;
 // Pages per key range of the audio kernel when the step's audio rows ride in
 // the video kernel and it walks only the audio-token pages (one page per
 // wave: measured 1.5 us faster per step than two).
@@ -750,8 +753,18 @@ bool plan_riders(ws_cache* c, const ws_attn_call* video, const ws_attn_call* aud
     rmax = std::max(rmax, static_cast<int>(ws::video_group_of(part, h0 + cl.n_pages - 1) -
                                            ws::video_group_of(part, h0) + 1));
   }
+  // The rows' own pages go to the video kernel when its last query tile
+  // leaves at least kRiderMinIdleWaves waves without rows (they attend the
+  // pages while the others start their first segment) and the page list
+  // stays inline; otherwise to the audio kernel.
+  const int last_rows = rq_row0 + n_rq - (cl.n_qtiles - 1) * ws::kVideoQTile;
+  const int idle_waves = ws::kVideoWaves - (last_rows + 31) / 32;
+  const bool in_video = n_extra > 0 && c->opt_audio_splits == 0 && pv.a.pages == nullptr &&
+                        idle_waves >= kRiderMinIdleWaves &&
+                        pv.a.n_pages + n_extra <= ws::AttnArgs::kInlinePages;
+  const int rx_waves = in_video ? std::min(idle_waves, n_extra) : 0;
   int splits = 0, pps = 0;
-  if (n_extra > 0) {
+  if (n_extra > 0 && !in_video) {
     // few pages (latency-bound): as many ranges as give each wave of the
     // audio kernel at most kRiderPagesPerRange / 4 pages
     splits = c->opt_audio_splits > 0 ? c->opt_audio_splits
@@ -760,7 +773,8 @@ bool plan_riders(ws_cache* c, const ws_attn_call* video, const ws_attn_call* aud
     pps = (n_extra + splits - 1) / splits;
     splits = (n_extra + pps - 1) / pps;
   }
-  if (static_cast<int64_t>(splits + rmax) * H * n_rq > c->part_rows) return false;
+  const int ranges = splits + rmax + rx_waves;
+  if (static_cast<int64_t>(ranges) * H * n_rq > c->part_rows) return false;
 
   ws::AttnArgs& aa = pa.a;
   for (int32_t i = 0; i < n_extra; ++i)
@@ -771,13 +785,22 @@ bool plan_riders(ws_cache* c, const ws_attn_call* video, const ws_attn_call* aud
   aa.n_splits = std::max(splits, 1);
   aa.pages_per_split = pps;
   pa.splits = splits;
-  pa.part_rows = static_cast<int64_t>(splits + rmax) * H * n_rq;
+  pa.part_rows = static_cast<int64_t>(ranges) * H * n_rq;
   pa.merge = true;
   pa.cb.n_splits = splits;
   pa.cb.r_pages = cl.n_pages;
   pa.cb.r_groups = cl.n_groups;
   pa.cb.seg_cost = pv.a.seg_cost;
+  pa.cb.r_extra = rx_waves;
   ws::AttnArgs& av = pv.a;
+  if (in_video) {
+    av.rx_page0 = pv.a.n_pages;
+    av.rx_pages = n_extra;
+    av.rx_waves = rx_waves;
+    for (int32_t i = 0; i < n_extra; ++i)
+      av.inline_pages[av.rx_page0 + i] = make_int2(c->scratch_list[static_cast<size_t>(i)].page,
+                                                   c->scratch_list[static_cast<size_t>(i)].n_valid);
+  }
   av.rq = static_cast<const uint16_t*>(audio->q);
   av.rq_tok_stride = audio->q_tok_stride;
   av.rq_head_stride = audio->q_head_stride;

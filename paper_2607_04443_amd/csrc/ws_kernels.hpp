@@ -170,6 +170,14 @@ struct AttnArgs {
   int32_t rq_row0;
   float* rpart_o;
   float* rpart_lse;
+  // The rider rows' own pages (visible to them only), entries rx_page0 ..
+  // rx_page0 + rx_pages - 1 of the inline page list (rx_pages = 0: none, or
+  // attended elsewhere): attended by the last rx_waves waves (which have no
+  // rows) of the last query tile's workgroup of the group holding each
+  // head's last page, one key range per wave after the head's ranges.
+  int32_t rx_page0;
+  int32_t rx_pages;
+  int32_t rx_waves;
   uint32_t* flags;
   int2 inline_pages[kInlinePages];
 };
@@ -189,6 +197,7 @@ struct CombineArgs {
   // gives (r_groups = 0: none).
   int32_t r_pages;
   int32_t r_groups;
+  int32_t r_extra;       // more ranges per head: the rows' own pages, from the video kernel's idle waves
   int32_t n_q;
   int32_t num_heads;
   uint16_t* out;

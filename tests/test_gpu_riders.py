@@ -126,33 +126,43 @@ class Step:
         self.cache.close()
 
 
-@pytest.mark.parametrize("n_v,n_a,audio_tokens,splits,akinds,norm_rope", [
-    (920, 4, 4, 0, ALL, False),     # the v0.2 unit: riders in rows 920..923 of the fourth tile
-    (100, 33, 40, 0, ALL, False),   # 33 riders over two waves of the only tile, one shared
-    (920, 4, 4, 3, ALL, False),     # three forced key ranges per head
-    (700, 64, 4, 0, ALL, False),    # 64 riders (the audio maximum), up to the tile's end
-    (920, 4, 4, 0, VIDEO, False),   # no audio-only pages: no audio kernel at all
-    (910, 9, 4, 0, ALL, True),      # NORM_ROPE video rows and prepared riders in one wave
+# Where the audio-only pages are attended: by the video kernel after its
+# segments ("video": the last query tile has at most 6 active waves), by the
+# audio kernel ("kernel": a fuller last tile, or forced by an audio split
+# count), or nowhere ("none": no such pages).
+@pytest.mark.parametrize("n_v,n_a,audio_tokens,splits,akinds,norm_rope,asplits,where", [
+    (920, 4, 4, 0, ALL, False, 0, "video"),     # the v0.2 unit: riders in rows 920..923
+    (920, 4, 4, 0, ALL, False, 2, "kernel"),    # the same, audio pages in the audio kernel
+    (100, 33, 40, 0, ALL, False, 0, "video"),   # 33 riders over two waves, one shared; 40-token pages
+    (920, 4, 4, 3, ALL, False, 0, "video"),     # three forced key ranges per head
+    (920, 12, 40, 0, ALL, False, 0, "video"),   # 12 riders over 4 pages of 40 tokens
+    (700, 64, 4, 0, ALL, False, 0, "kernel"),   # 64 riders (the audio maximum), to the tile's end
+    (920, 4, 4, 0, VIDEO, False, 0, "none"),    # no audio-only pages: no audio kernel at all
+    (910, 9, 4, 0, ALL, True, 0, "video"),      # NORM_ROPE video rows and prepared riders in one wave
 ])
-def test_riders_match_oracle_and_separate_kernel(ws, n_v, n_a, audio_tokens, splits, akinds, norm_rope):
+def test_riders_match_oracle_and_separate_kernel(ws, n_v, n_a, audio_tokens, splits, akinds, norm_rope,
+                                                 asplits, where):
     H = 8
     S = Step(ws, H, (23, 40), 256, audio_tokens, 4, 61)
     try:
         if splits:
             S.cache.set_option(ws.WS_OPT_VIDEO_KV_SPLITS, splits)
+        if asplits:
+            S.cache.set_option(ws.WS_OPT_AUDIO_KV_SPLITS, asplits)
         u = S.unit
         vmask, amask = (u, u - 3, VIDEO), (u, u - 3, akinds)
         qv, qa = S.queries(n_v), S.queries(n_a)
         if norm_rope:
             qv = synth.normal_bf16(S.rng, (n_v, H, 128))
         print(f"riders: n_v={n_v} n_a={n_a} audio_tokens={audio_tokens} splits={splits} "
-              f"norm_rope={norm_rope}", flush=True)
+              f"norm_rope={norm_rope} asplits={asplits} where={where}", flush=True)
         fv, fa, rec = S.step(qv, qa, vmask, amask, norm_rope=norm_rope)
         assert [r["path"] for r in rec] == ["video", "audio_riders"], rec
-        if akinds == VIDEO:
-            assert rec[1]["n_splits"] == 0
+        # the audio kernel's range count: 0 when it was not launched
+        if where == "kernel":
+            assert rec[1]["n_splits"] >= 1, rec
         else:
-            assert rec[1]["n_splits"] >= 1
+            assert rec[1]["n_splits"] == 0, rec
         sv, sa, rec2 = S.step(qv, qa, vmask, amask, separate=True, norm_rope=norm_rope)
         assert [r["path"] for r in rec2] == ["video", "audio"], rec2
         np.testing.assert_array_equal(fv, sv)
