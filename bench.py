@@ -413,6 +413,8 @@ def block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev, steps=50, wa
     # the step does not qualify (path 'audio')
     apath = "audio_riders" if any(r["path"] == "audio_riders" for r in rec) else "audio"
     t_app, t_vid, t_aud = avg("append"), avg("video"), avg(apath)
+    if all(r["n_splits"] == 0 for r in rec if r["path"] == apath):
+        t_aud = 0.0  # no audio kernel launched: the rows' own pages were attended in the video kernel
     t_merge = avg(apath, "merge_us")
     attn_us = t_app + t_vid + t_aud + t_merge
     return {"us_per_step": us, "rows": rows, "hidden": hid,

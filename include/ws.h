@@ -333,8 +333,10 @@ typedef struct ws_attn_call {
  * call too, and the audio rows fit the spare rows of the video call's last
  * 256-query tile (n_audio <= 256 * ceil(n_video / 256) - n_video), the video
  * kernel also computes the audio rows over the video call's pages (the pages
- * are streamed once for both), and the audio kernel walks only the pages the
- * audio call alone sees (the units' audio tokens); the merge folds both.
+ * are streamed once for both); the pages the audio call alone sees (the
+ * units' audio tokens) are walked by the video kernel's waves that have no
+ * rows (when its last query tile leaves at least two) or else by the audio
+ * kernel; the merge folds all the ranges.
  * WS_OPT_STEP_SEPARATE_AUDIO turns this off.  The video output always equals
  * what ws_unit_attention(video) writes, bit for bit; the audio output equals
  * ws_audio_attention(audio) bit for bit when the rows do not ride, and
@@ -342,8 +344,8 @@ typedef struct ws_attn_call {
  * under another shift) and the order of fp32 sums.  With timing
  * enabled the call records two ring entries: the video kernel (merge time 0),
  * and the audio kernel with the shared merge (path 1; path 5 when the audio
- * rows ride, with the audio kernel's range count, 0 when it had no pages to
- * walk and was not launched). */
+ * rows ride, with the audio kernel's range count, 0 when it was not
+ * launched). */
 WS_API ws_status ws_step_attention(ws_cache* cache, const ws_attn_call* video, const ws_attn_call* audio,
                                    void* hip_stream);
 

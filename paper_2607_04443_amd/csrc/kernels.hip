@@ -1624,9 +1624,10 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;
   // The largest log-sum-exp first: every range is then weighted the same way
   // whatever the batch, so the step's merge launch and the audio call's own
-  // give the same bits.
+  // give the same bits.  (With all ranges in one batch it comes from that
+  // batch's loads.)
   float mx = kNegInf;
-  for (int sp0 = 0; sp0 < n_splits; sp0 += 16) {
+  for (int sp0 = 0; n_splits > kMergeBatch && sp0 < n_splits; sp0 += 16) {
     float lb[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) lb[i] = sp0 + i < n_splits ? a.part_lse[(sp0 + i) * split_stride + row] : kNegInf;
@@ -1635,7 +1636,7 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   }
   float wsum = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int sp0 = 0; sp0 < n_splits && mx != kNegInf; sp0 += kMergeBatch) {
+  for (int sp0 = 0; sp0 < n_splits; sp0 += kMergeBatch) {
     float lb[kMergeBatch];
     f32x4 o0[kMergeBatch], o1[kMergeBatch];
 #pragma unroll
@@ -1647,6 +1648,11 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
       o0[i] = ok ? *reinterpret_cast<const f32x4*>(po) : (f32x4){0.f, 0.f, 0.f, 0.f};
       o1[i] = ok ? *reinterpret_cast<const f32x4*>(po + 4) : (f32x4){0.f, 0.f, 0.f, 0.f};
     }
+    if (n_splits <= kMergeBatch) {
+#pragma unroll
+      for (int i = 0; i < kMergeBatch; ++i) mx = fmaxf(mx, lb[i]);
+    }
+    if (mx == kNegInf) break;
 #pragma unroll
     for (int i = 0; i < kMergeBatch; ++i) {
       const float w = lb[i] == kNegInf ? 0.f : fast_exp2(lb[i] - mx);
