@@ -2,7 +2,8 @@
 queries of a step see the video queries' pages plus the units' audio tokens
 (Sec. 3: both latent streams of a unit attend over the one cache), so the
 video kernel computes the audio rows over the shared pages in the spare rows
-of its last query tile and the audio kernel walks only the audio pages.
+of its last query tile, and the audio-token pages are walked by that tile's
+waves without rows (or by the audio kernel).
 Checked against the oracle, against the separate audio kernel
 (WS_OPT_STEP_SEPARATE_AUDIO) and, for the video rows, bit for bit against
 ws_unit_attention; steps that do not qualify take the separate kernel."""
@@ -126,10 +127,10 @@ class Step:
         self.cache.close()
 
 
-# Where the audio-only pages are attended: by the video kernel after its
-# segments ("video": the last query tile has at most 6 active waves), by the
-# audio kernel ("kernel": a fuller last tile, or forced by an audio split
-# count), or nowhere ("none": no such pages).
+# Where the audio-only pages are attended: by the video kernel's waves without
+# rows ("video": the last query tile leaves at least two), by the audio kernel
+# ("kernel": a fuller last tile, or forced by an audio split count), or
+# nowhere ("none": no such pages).
 @pytest.mark.parametrize("n_v,n_a,audio_tokens,splits,akinds,norm_rope,asplits,where", [
     (920, 4, 4, 0, ALL, False, 0, "video"),     # the v0.2 unit: riders in rows 920..923
     (920, 4, 4, 0, ALL, False, 2, "kernel"),    # the same, audio pages in the audio kernel
