@@ -17,6 +17,20 @@ from paper_2607_04443_amd import synth
 CONTRACT_MAX, CONTRACT_MEAN = 2e-2, 2e-3
 STRICT_FROB, STRICT_REL, STRICT_RMS = 1e-2, 2.0 ** -7, 0.08
 
+# Independent of any kernel output: a first-order bound on |GPU - exact| per
+# output element, from the roundings the GPU path makes (bf16 unit roundoff
+# u = 2^-9) and the oracle's own fp64 data.  For query row q, key k, dim d,
+# with p the exact softmax weights, O the exact output and s the logit scale:
+#   output and key-range partials rounded to bf16     2u * A_qd,  A = sum_k p|v_kd|
+#   P rounded to bf16 before P*V (and its row sum)     u  * sum_k p (|v_kd| + |O_qd|)
+#   Q'' and K' rounded to bf16: a logit errs by at most
+#     D_qk = 2u * s * sum_i |q'_i k'_i|, which moves O by sum_k p D_qk (|v_kd| + |O_qd|)
+#   fp32 sums of n_k terms (row sum, P*V)              2 n_k 2^-24 * A_qd
+# (to first order; 5% margin for the second-order terms).  Rigorous but
+# loose: it assumes every rounding error aligned.  The Frobenius gate above
+# follows the same model's rms (about 3e-3 at 8.5k keys, gate 1e-2).
+ROUND_U = 2.0 ** -9
+
 
 def to_dev(bits):
     import torch
@@ -96,8 +110,50 @@ class Loaded:
                                        heads=heads)
         return out
 
+    def bound(self, q_bits, q_pos, q_unit, kinds, heads=None, min_unit=-(2 ** 31), mode=None):
+        """rounding_bound for the same call as oracle()."""
+        mode = oracle.MODE_NORM_ROPE if mode is None else mode
+        return rounding_bound(self.ocache, q_bits, q_unit, mode=mode, positions=q_pos,
+                              gamma=self.wl.gamma_q.astype(np.float64), eps=self.wl.eps,
+                              min_visible_unit=min_unit, kind_mask=sum(1 << k for k in kinds), heads=heads)
+
     def close(self):
         self.cache.close()
+
+
+def rounding_bound(ocache, q_bits, q_unit, *, mode=oracle.MODE_NORM_ROPE, positions=None, gamma=None,
+                   eps=1e-6, scale=None, min_visible_unit=-(2 ** 31), kind_mask=0b011, heads=None):
+    """The elementwise bound above for oracle.unit_attention's output with the
+    same arguments: [n_q, len(heads), D] float64."""
+    q_bits = np.asarray(q_bits, dtype=np.uint16)
+    n_q, H, D = q_bits.shape
+    heads = list(range(H)) if heads is None else list(heads)
+    scale = 1.0 / np.sqrt(D) if scale is None else scale
+    gamma = np.ones(D) if gamma is None else gamma
+    u = ROUND_U
+    out = np.zeros((n_q, len(heads), D))
+    for hi, h in enumerate(heads):
+        q = oracle.query_prologue(q_bits[:, h, :], mode, positions, gamma, eps, ocache.band_pairs, ocache.theta)
+        k, v = ocache.keys_values(h, q_unit, min_visible_unit, kind_mask)
+        n_k = k.shape[0]
+        if n_k == 0:
+            continue
+        # float32 is ample for a bound (its own error is ~1e-7 relative)
+        q32, k32, v32 = (x.astype(np.float32) for x in (q, k, v))
+        logit = np.float32(scale) * (q32 @ k32.T)
+        logit -= logit.max(axis=1, keepdims=True)
+        p = np.exp(logit, out=logit)
+        p /= p.sum(axis=1, keepdims=True)
+        av = np.abs(v32)
+        o = np.abs(p @ v32)
+        a = p @ av
+        w = np.abs(q32) @ np.abs(k32).T
+        w *= np.float32(2 * u * scale)
+        w += np.float32(u)
+        w *= p
+        b = w @ av + o * w.sum(axis=1, keepdims=True)
+        out[:, hi, :] = 1.05 * ((2 * u + 2 * n_k * 2.0 ** -24) * a + b) + 1e-7
+    return out
 
 
 def errors(got, ref):
@@ -106,9 +162,16 @@ def errors(got, ref):
                 frob=float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)))
 
 
-def assert_gates(got, ref, strict=True, label="", scale=1.0):
+def assert_gates(got, ref, strict=True, label="", scale=1.0, bound=None):
+    """The contract gates; with strict, the Frobenius gate and the fitted
+    elementwise one; with a bound (rounding_bound), |got - ref| <= bound
+    everywhere as well."""
     assert np.isfinite(got).all(), f"{label}: non-finite output"
     e = errors(got, ref)
+    if bound is not None:
+        r = np.abs(got - ref) / bound
+        e["bound_ratio"] = float(r.max())
+        assert e["bound_ratio"] <= 1.0, f"{label}: rounding bound exceeded: {e}"
     rms = float(np.sqrt(np.mean(ref * ref)))
     bound = STRICT_REL * np.abs(ref) + STRICT_RMS * rms
     ratio = np.abs(got - ref) / np.maximum(bound, 1e-30)

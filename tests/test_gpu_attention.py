@@ -28,13 +28,18 @@ def _video(L, step=0, heads=None, **kw):
     return got, ref
 
 
+def _video_bound(L, step=0, heads=None, **kw):
+    st = L.wl.steps[step]
+    return L.bound(st.q_video, st.q_video_pos, L.wl.current_unit, VIDEO_KINDS, heads=heads, **kw)
+
+
 @pytest.mark.parametrize("name,heads", [("v01", None), ("v02_single", None), ("v02_hist8", None)])
 def test_video_parity(ws, name, heads):
     wl = synth.make_workload(name)
     L = Loaded(ws, wl)
     try:
         got, ref = _video(L, heads=heads)
-        e = assert_gates(got, ref, label=name)
+        e = assert_gates(got, ref, label=name, bound=_video_bound(L, heads=heads))
         print(name, e)
     finally:
         L.close()
@@ -87,10 +92,11 @@ def test_video_parity_gamma_variants(ws, variant):
             # gamma_q = 4 widens the logits 4x and with them the bf16 logit error; where
             # two keys compete the output error is ~ p1 p2 d(s1 - s2) |v1 - v2|, so only
             # the scale-free Frobenius gate and 4x-widened contract gates apply
-            print(variant, assert_gates(got, ref, label=variant, scale=4.0, strict=False))
+            print(variant, assert_gates(got, ref, label=variant, scale=4.0, strict=False,
+                                        bound=_video_bound(L)))
             assert np.linalg.norm(got - ref) <= 1e-2 * np.linalg.norm(ref)
         else:
-            print(variant, assert_gates(got, ref, label=variant))
+            print(variant, assert_gates(got, ref, label=variant, bound=_video_bound(L)))
     finally:
         L.close()
 
@@ -103,7 +109,8 @@ def test_audio_parity(ws, name):
         st = wl.steps[0]
         got = L.run("audio", st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
         ref = L.oracle(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
-        print(name, assert_gates(got, ref, label=name))
+        bound = L.bound(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+        print(name, assert_gates(got, ref, label=name, bound=bound))
     finally:
         L.close()
 
@@ -696,8 +703,10 @@ def test_bench_step_at_full_size(ws):
         np.testing.assert_array_equal(outs[0][0], outs[1][0])
         np.testing.assert_array_equal(outs[0][1], outs[1][1])
         refv = L.oracle(st.q_video, st.q_video_pos, wl.current_unit, VIDEO_KINDS)
-        print("video", assert_gates(bf16_f64(outs[0][0]), refv, label="bench step video"))
+        bv = L.bound(st.q_video, st.q_video_pos, wl.current_unit, VIDEO_KINDS)
+        print("video", assert_gates(bf16_f64(outs[0][0]), refv, label="bench step video", bound=bv))
         refa = L.oracle(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
-        print("audio", assert_gates(bf16_f64(outs[0][1]), refa, label="bench step audio"))
+        ba = L.bound(st.q_audio, st.q_audio_pos, wl.current_unit, ALL_KINDS)
+        print("audio", assert_gates(bf16_f64(outs[0][1]), refa, label="bench step audio", bound=ba))
     finally:
         L.close()

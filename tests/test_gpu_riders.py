@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
-from helpers import assert_gates, bf16_f64, dev_f32, dev_i32, from_dev, to_dev
+from helpers import assert_gates, bf16_f64, dev_f32, dev_i32, from_dev, rounding_bound, to_dev
 from paper_2607_04443_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -123,6 +123,12 @@ class Step:
         return oracle.unit_attention(self.oc, q, u, mode=oracle.MODE_RAW, scale=LN2, min_visible_unit=mn,
                                      kind_mask=_km(kinds))[0]
 
+    def bound(self, q, mask):
+        """rounding_bound of the prepared rows' attention (oracle's RAW reading)."""
+        u, mn, kinds = mask
+        return rounding_bound(self.oc, q, u, mode=oracle.MODE_RAW, scale=LN2, min_visible_unit=mn,
+                              kind_mask=_km(kinds))
+
     def close(self):
         self.cache.close()
 
@@ -169,8 +175,9 @@ def test_riders_match_oracle_and_separate_kernel(ws, n_v, n_a, audio_tokens, spl
         np.testing.assert_array_equal(fv, sv)
         np.testing.assert_array_equal(fv, S.separate_video(qv, vmask, norm_rope))
         refa = S.oracle(qa, amask)
-        print("riders audio", assert_gates(bf16_f64(fa), refa, label="audio rows in the video kernel"))
-        print("separate audio", assert_gates(bf16_f64(sa), refa, label="separate audio kernel"))
+        ba = S.bound(qa, amask)
+        print("riders audio", assert_gates(bf16_f64(fa), refa, label="audio rows in the video kernel", bound=ba))
+        print("separate audio", assert_gates(bf16_f64(sa), refa, label="separate audio kernel", bound=ba))
         print("video", assert_gates(bf16_f64(fv), S.oracle(qv, vmask, norm_rope), label="video rows"))
         # a repeat is bit-identical (every partial row the merge reads is rewritten)
         fv2, fa2, _ = S.step(qv, qa, vmask, amask, norm_rope=norm_rope)

@@ -281,3 +281,58 @@ def test_block_step_projections_are_linear():
                                rtol=0, atol=1e-12)
     np.testing.assert_allclose(o[nv:], np.broadcast_to(vcond.sum(0) / (3 + nv + na), (na, H, D)),
                                rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("gamma_q", [1.0, 4.0])
+def test_rounding_bound_covers_the_bf16_rounding_model(gamma_q):
+    """helpers.rounding_bound (the GPU parity tests' independent elementwise
+    gate) covers an emulation of the GPU path's roundings written here from
+    the model, on a cache of a RAW slice and three NORM_ROPE units: Q'' and
+    K' rounded to bf16, softmax weights rounded to bf16 against each key
+    range's maximum (the shift cancels in the weights' relative rounding),
+    two key ranges written as bf16 partials and merged by log-sum-exp, the
+    output rounded to bf16."""
+    from helpers import rounding_bound
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 71))
+    grid = (6, 8)
+    c = oracle.OracleCache(num_heads=H)
+    ck, cv = synth.normal_bf16(rng, (40, H, D)), synth.normal_bf16(rng, (40, H, D))
+    c.append(0, oracle.KIND_COND, ck, cv, oracle.MODE_RAW)
+    ones = np.ones(D)
+    for u in range(3):
+        k, v = synth.normal_bf16(rng, (48, H, D)), synth.normal_bf16(rng, (48, H, D))
+        c.append(u, oracle.KIND_VIDEO, k, v, oracle.MODE_NORM_ROPE, synth.video_positions(u, grid), ones, 1e-6)
+    q = synth.normal_bf16(rng, (24, H, D))
+    qpos = synth.video_positions(2, grid)[:24]
+    gq = np.full(D, gamma_q)
+    kw = dict(positions=qpos, gamma=gq, eps=1e-6, kind_mask=0b011)
+    exact, _ = oracle.unit_attention(c, q, 2, **kw)
+    bound = rounding_bound(c, q, 2, **kw)
+    scale = 1.0 / np.sqrt(D)
+    log2e = 1.0 / np.log(2.0)
+
+    def rnd(x):
+        return oracle.bf16_decode(oracle.bf16_round(x))
+
+    worst = 0.0
+    for h in range(H):
+        qh = oracle.query_prologue(q[:, h, :], oracle.MODE_NORM_ROPE, qpos, gq, 1e-6)
+        k, v = c.keys_values(h, 2, -(2 ** 31), 0b011)
+        s = rnd(qh * scale * log2e) @ rnd(k).T  # log2 domain
+        half = k.shape[0] // 2
+        parts = []
+        for lo, hi in ((0, half), (half, k.shape[0])):
+            m = s[:, lo:hi].max(axis=1, keepdims=True)
+            p = rnd(np.exp2(s[:, lo:hi] - m))
+            l = p.sum(axis=1, keepdims=True)
+            parts.append((rnd(p @ v[lo:hi] / l), m[:, 0] + np.log2(l[:, 0])))
+        mx = np.maximum(parts[0][1], parts[1][1])
+        w = [np.exp2(lse - mx)[:, None] for _, lse in parts]
+        emu = rnd((w[0] * parts[0][0] + w[1] * parts[1][0]) / (w[0] + w[1]))
+        err = np.abs(emu - exact[:, h, :])
+        assert (err <= bound[:, h, :]).all(), float((err / bound[:, h, :]).max())
+        worst = max(worst, float((err / bound[:, h, :]).max()))
+    print(f"gamma_q={gamma_q}: worst error / bound = {worst:.3f}")
+    assert 0.0 < worst < 1.0
+    # and the bound is far below the outputs' spread: it can still tell a wrong row
+    assert bound.max() < 0.25 * np.abs(exact).max()
