@@ -31,6 +31,9 @@ per-component fields) and the library's launch timing (ws_cache_timing_*):
 `roofline` is for the video attention kernel (the dominant one), its FLOP
 per launch over its average launch time from HIP events recorded on the
 calls' stream around the kernel itself.
+`video_configs` times the video kernel alone on the v0.1, v0.2 single-unit
+and v0.2 8-unit-history configurations (median of the library's per-launch
+kernel times).
 `us_per_unit_separate_audio` is the contract step with the audio call in
 its own kernel over all of its pages (WS_OPT_STEP_SEPARATE_AUDIO).
 `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
@@ -423,6 +426,66 @@ def block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev, steps=50, wa
             "append_us": t_app, "video_kernel_us": t_vid, "audio_kernel_us": t_aud, "merge_us": t_merge,
             "audio_rows_in_video_kernel": apath == "audio_riders",
             "attention_share": attn_us / (attn_us + t_qkv + t_out)}
+
+
+def video_configs(ws, torch, dev, launches=60):
+    """The video kernel alone on the seeded configurations v0.1 (12 heads, 252
+    queries over 820 keys), v0.2 single unit (40 heads, 920 over 1176) and
+    v0.2 with an 8-unit history (920 over 8536): the cache and queries of each
+    (prepared by one ws_step_append), then `launches` ws_unit_attention calls;
+    the median of the library's per-launch kernel times (HIP events on the
+    call's stream around the kernel) and its TFLOP/s."""
+    import numpy as np
+    from paper_2607_04443_amd import synth
+    out = {}
+    for name in ("v01", "v02_single", "v02_hist8"):
+        wl = synth.make_workload(name, steps=1)
+        cfg = wl.config
+        keep = []
+
+        def dev_bits(bits):
+            t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+            keep.append(t)
+            return t
+
+        def dev_arr(a, dt):
+            t = torch.from_numpy(np.ascontiguousarray(a, dtype=dt)).to(dev)
+            keep.append(t)
+            return t
+
+        cache = ws.Cache(cfg.heads, 8 + (cfg.hist + 2) * (cfg.unit_tokens // 64 + 3) + cfg.cond // 64,
+                         max_q_tokens=1024)
+        gk, gq = dev_arr(wl.gamma_k, np.float32), dev_arr(wl.gamma_q, np.float32)
+        st = wl.steps[0]
+        for seg in wl.cached + st.segments:
+            k, v = dev_bits(seg.k), dev_bits(seg.v)
+            if seg.mode == synth.MODE_RAW:
+                cache.append(seg.unit, seg.kind, k, v, ws.WS_APPEND_RAW)
+            else:
+                cache.append(seg.unit, seg.kind, k, v, ws.WS_APPEND_NORM_ROPE,
+                             dev_arr(seg.positions, np.int32), gk, wl.eps)
+        q = dev_bits(st.q_video)
+        qp = torch.empty_like(q)
+        cache.step_append([], [dict(q=q, q_out=qp, positions=dev_arr(st.q_video_pos, np.int32), gamma=gq,
+                                    eps=wl.eps)])
+        o = torch.empty_like(q)
+        mask = ws.mask_spec(wl.current_unit, -(2 ** 31), (ws.WS_KIND_COND, ws.WS_KIND_VIDEO))
+        for _ in range(20):
+            cache.unit_attention(qp, o, mask, ws.WS_QUERY_PREPARED)
+        torch.cuda.synchronize()
+        cache.timing_enable(launches)
+        for _ in range(launches):
+            cache.unit_attention(qp, o, mask, ws.WS_QUERY_PREPARED)
+        torch.cuda.synchronize()
+        t = sorted(r["attn_us"] for r in cache.timing_read())
+        cache.timing_enable(0)
+        cache.close()
+        lq, lk = cfg.unit_tokens, cfg.cond + (cfg.hist + 1) * cfg.unit_tokens
+        flop = 4.0 * cfg.heads * lq * lk * D
+        med = t[len(t) // 2]
+        out[name] = {"heads": cfg.heads, "queries": lq, "keys": lk, "flop": flop, "kernel_us_median": med,
+                     "tflops": flop / (med * 1e-6) / 1e12}
+    return out
 
 
 COPY_BYTES = 256 << 20
@@ -875,6 +938,7 @@ def main():
     long_hist = long_history(args, ws, sets, gamma, eps, stream, dev) if args.long_reps > 0 else None
     catch = catch_up(args, ws, sets, vpos, gamma, eps, stream, dev) if args.long_reps > 0 else None
     block = block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev) if args.long_reps > 0 else None
+    vconf = video_configs(ws, torch, dev) if args.long_reps > 0 else None
     peaks = measured_peaks(ws, torch, stream, dev) if args.peak_probes else None
 
     t_vkern, t_vmerge = kernel_us("video", "attn_us"), kernel_us("video", "merge_us")
@@ -911,6 +975,7 @@ def main():
                             "cold_cond256": cold_256},
         "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
         "long_history": long_hist,
+        "video_configs": vconf,
         "catch_up": catch,
         "block_step": block,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,
