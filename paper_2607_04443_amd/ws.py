@@ -13,6 +13,11 @@ from __future__ import annotations
 import ctypes
 import os
 
+# torch first: libws.so then binds to the HIP runtime torch has loaded, so
+# both share one runtime (loaded ahead of torch, libws.so pulls in the system
+# runtime, which found no device next to torch's ROCm build).
+import torch  # noqa: F401
+
 from . import _build
 
 if not os.path.exists(_build.LIB_PATH):
