@@ -733,8 +733,10 @@ def pmc_driver(mode, ws, cache, step, u, q_v, out_v, q_a, out_a, sets, gamma, ep
 def measured_peaks(ws, torch, stream, dev):
     """The ceilings this GPU sustains, from the library's calibration probes:
     a bf16 MFMA loop (2048 workgroups of 4 waves, register operands, about
-    10 ms) and one streaming read of a 2 GiB buffer; medians of 7 timed runs
-    after 3 untimed ones."""
+    10 ms) on small-integer operands and on random ones (attention's
+    operands switch as many bits as the latter, and the clock the chip holds
+    under a long MFMA load falls with them), and one streaming read of a
+    2 GiB buffer; medians of 7 timed runs after 3 untimed ones."""
     sink = torch.zeros(2, dtype=torch.float32, device=dev)
     buf = torch.zeros(1 << 31, dtype=torch.uint8, device=dev)
     h = stream.cuda_stream
@@ -757,9 +759,11 @@ def measured_peaks(ws, torch, stream, dev):
         flop[0] = ws.ws_probe_mfma(2048, 20000, sink.data_ptr(), h)
 
     t_m = timed(mfma)
+    t_mr = timed(lambda: ws.ws_probe_mfma_random(2048, 20000, sink.data_ptr(), h))
     t_r = timed(lambda: ws.ws_probe_read(buf.data_ptr(), buf.numel(), 4096, sink.data_ptr() + 4, h))
     del buf
     return {"mfma_bf16_tflops": flop[0] / t_m / 1e12, "mfma_frac_of_published": flop[0] / t_m / 1e12 / PEAK_BF16_TFLOPS,
+            "mfma_bf16_random_operands_tflops": flop[0] / t_mr / 1e12,
             "hbm_read_gbps": (1 << 31) / t_r / 1e9, "hbm_frac_of_published": (1 << 31) / t_r / 1e9 / PEAK_HBM_GBS}
 
 
@@ -985,6 +989,7 @@ def main():
     }
     if peaks is not None:
         peaks["video_kernel_frac"] = achieved / peaks["mfma_bf16_tflops"]
+        peaks["video_kernel_frac_of_random"] = achieved / peaks["mfma_bf16_random_operands_tflops"]
         if cold is not None:
             peaks["audio_cold_frac"] = cold["gbps"] / peaks["hbm_read_gbps"]
         result["measured_peaks"] = peaks

@@ -489,8 +489,14 @@ WS_API ws_status ws_cache_timing_read(ws_cache* cache, ws_call_timing* out, int3
  *
  * ws_probe_mfma: `workgroups` (1..65536) workgroups of 4 waves; each wave
  * issues iters (1..2^24) rounds of 4 independent 32x32x16 bf16 MFMAs on
- * register operands.  *flop (host) receives the launch's FLOP count.  sink is
- * a device float[1], written only in a case the arithmetic never reaches.
+ * register operands (small integers, the same for the 4 chains: few bits
+ * switch).  *flop (host) receives the launch's FLOP count.  sink is a device
+ * float[1], written only in a case the arithmetic never reaches.
+ *
+ * ws_probe_mfma_random: the same launch with hashed operands, random sign
+ * and mantissa bits and magnitudes in [0.5, 2), different for each chain (the
+ * switching activity of attention's operands, which lowers the clock the
+ * chip holds under a long MFMA load).
  *
  * ws_probe_read: reads the `bytes` bytes at device address buf once
  * (16-byte aligned, bytes a positive multiple of 16) with `workgroups`
@@ -498,6 +504,8 @@ WS_API ws_status ws_cache_timing_read(ws_cache* cache, ws_call_timing* out, int3
  * written only in a case that does not occur for ordinary data. */
 WS_API ws_status ws_probe_mfma(int32_t workgroups, int32_t iters, float* sink, double* flop,
                                void* hip_stream);
+WS_API ws_status ws_probe_mfma_random(int32_t workgroups, int32_t iters, float* sink, double* flop,
+                                      void* hip_stream);
 WS_API ws_status ws_probe_read(const void* buf, int64_t bytes, int32_t workgroups, uint32_t* sink,
                                void* hip_stream);
 

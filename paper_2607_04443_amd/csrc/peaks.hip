@@ -18,22 +18,41 @@ using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 constexpr int kProbeThreads = 256;
 constexpr int kMfmaChains = 4;  // independent accumulators per wave
 
+// A bf16 value of magnitude in [0.5, 2) with hashed sign and mantissa bits
+// (the switching activity of attention operands, not of small integers).
+__device__ __forceinline__ __bf16 hashed_bf16(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  const uint16_t bits = static_cast<uint16_t>((x & 0x807fu) | ((x & 0x100u) ? 0x3f80u : 0x3f00u));
+  return __builtin_bit_cast(__bf16, bits);
+}
+
 // Each wave runs iters rounds of kMfmaChains independent 32x32x16 bf16 MFMAs
-// on register operands.  The result is stored only if it equals a value the
-// arithmetic cannot produce (kept so the loop is not removed).
+// on register operands.  kRandom = false: small-integer operands shared by
+// the chains (few bits switch: the clock the chip holds at its lowest
+// switching activity); true: hashed operands of their own per chain, so that
+// consecutive MFMAs see different random bits.  The result is stored only if
+// it equals a value the arithmetic cannot produce (kept so the loop is not
+// removed).
+template <bool kRandom>
 __global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, float* sink) {
-  bf16x8 a, b;
-  for (int i = 0; i < 8; ++i) {
-    a[i] = (__bf16)(float)((threadIdx.x + i) & 7);
-    b[i] = (__bf16)(float)((threadIdx.x * 3 + i) & 7);
-  }
+  bf16x8 a[kMfmaChains], b[kMfmaChains];
+  const uint32_t t = blockIdx.x * kProbeThreads + threadIdx.x;
+  for (int c = 0; c < kMfmaChains; ++c)
+    for (int i = 0; i < 8; ++i) {
+      a[c][i] = kRandom ? hashed_bf16(t * 64u + c * 16u + i) : (__bf16)(float)((threadIdx.x + i) & 7);
+      b[c][i] = kRandom ? hashed_bf16(t * 64u + c * 16u + 8u + i) : (__bf16)(float)((threadIdx.x * 3 + i) & 7);
+    }
   f32x16 acc[kMfmaChains];
   for (int c = 0; c < kMfmaChains; ++c)
     for (int r = 0; r < 16; ++r) acc[c][r] = 0.0f;
   for (int it = 0; it < iters; ++it) {
 #pragma unroll
     for (int c = 0; c < kMfmaChains; ++c)
-      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[c], b[c], acc[c], 0, 0, 0);
   }
   float s = 0.0f;
   for (int c = 0; c < kMfmaChains; ++c)
@@ -59,8 +78,11 @@ __global__ __launch_bounds__(kProbeThreads) void read_probe_kernel(const u32x4* 
 
 }  // namespace
 
-hipError_t launch_mfma_probe(int workgroups, int iters, float* sink, hipStream_t stream) {
-  hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters, sink);
+hipError_t launch_mfma_probe(int workgroups, int iters, bool random_operands, float* sink, hipStream_t stream) {
+  if (random_operands)
+    hipLaunchKernelGGL(mfma_probe_kernel<true>, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters, sink);
+  else
+    hipLaunchKernelGGL(mfma_probe_kernel<false>, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters, sink);
   return hipGetLastError();
 }
 

@@ -1313,14 +1313,26 @@ ws_status ws_cache_timing_read(ws_cache* c, ws_call_timing* out, int32_t max, in
   return WS_OK;
 }
 
-ws_status ws_probe_mfma(int32_t workgroups, int32_t iters, float* sink, double* flop,
-                        void* hip_stream) {
+namespace {
+ws_status probe_mfma(int32_t workgroups, int32_t iters, bool random_operands, float* sink, double* flop,
+                     void* hip_stream) {
   if (!sink || !flop) return fail(WS_ERR_INVALID_ARG, "NULL argument");
   if (workgroups < 1 || workgroups > 65536 || iters < 1 || iters > (1 << 24))
     return fail(WS_ERR_INVALID_ARG, "workgroups must be in [1, 65536] and iters in [1, 2^24]");
   *flop = ws::mfma_probe_flop(workgroups, iters);
-  WS_HIP(ws::launch_mfma_probe(workgroups, iters, sink, static_cast<hipStream_t>(hip_stream)));
+  WS_HIP(ws::launch_mfma_probe(workgroups, iters, random_operands, sink, static_cast<hipStream_t>(hip_stream)));
   return WS_OK;
+}
+}  // namespace
+
+ws_status ws_probe_mfma(int32_t workgroups, int32_t iters, float* sink, double* flop,
+                        void* hip_stream) {
+  return probe_mfma(workgroups, iters, false, sink, flop, hip_stream);
+}
+
+ws_status ws_probe_mfma_random(int32_t workgroups, int32_t iters, float* sink, double* flop,
+                               void* hip_stream) {
+  return probe_mfma(workgroups, iters, true, sink, flop, hip_stream);
 }
 
 ws_status ws_probe_read(const void* buf, int64_t bytes, int32_t workgroups, uint32_t* sink,

@@ -218,7 +218,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 // in one launch; either may be absent (zero-initialised).
 hipError_t launch_step_combine(const CombineArgs& video, const CombineArgs& audio, hipStream_t stream);
 // Calibration probes (peaks.hip).
-hipError_t launch_mfma_probe(int workgroups, int iters, float* sink, hipStream_t stream);
+hipError_t launch_mfma_probe(int workgroups, int iters, bool random_operands, float* sink, hipStream_t stream);
 hipError_t launch_read_probe(const void* buf, int64_t n16, int workgroups, uint32_t* sink,
                              hipStream_t stream);
 double mfma_probe_flop(int workgroups, int iters);

@@ -154,6 +154,7 @@ _SIGS = {
     "ws_cache_timing_enable": [_vp, _i32],
     "ws_cache_timing_read": [_vp, _P(ws_call_timing), _i32, _P(_i32)],
     "ws_probe_mfma": [_i32, _i32, _vp, _P(ctypes.c_double), _vp],
+    "ws_probe_mfma_random": [_i32, _i32, _vp, _P(ctypes.c_double), _vp],
     "ws_probe_read": [_vp, _i64, _i32, _vp, _vp],
 }
 for _name, _args in _SIGS.items():
@@ -321,6 +322,14 @@ def ws_probe_mfma(workgroups, iters, sink, stream):
     sink: device address of a float; stream: HIP stream handle."""
     flop = ctypes.c_double()
     _check(_lib.ws_probe_mfma(workgroups, iters, sink, ctypes.byref(flop), stream), "ws_probe_mfma")
+    return flop.value
+
+
+def ws_probe_mfma_random(workgroups, iters, sink, stream):
+    """The same loop on hashed random operands; returns its FLOP count."""
+    flop = ctypes.c_double()
+    _check(_lib.ws_probe_mfma_random(workgroups, iters, sink, ctypes.byref(flop), stream),
+           "ws_probe_mfma_random")
     return flop.value
 
 

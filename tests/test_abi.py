@@ -51,14 +51,16 @@ def test_probe_arguments_rejected_before_any_device_call():
     lib = ctypes.CDLL(b.LIB_PATH)
     lib.ws_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                   ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    lib.ws_probe_mfma_random.argtypes = lib.ws_probe_mfma.argtypes
     lib.ws_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
                                   ctypes.c_void_p]
     lib.ws_last_error.restype = ctypes.c_char_p
     flop = ctypes.c_double()
     fake = ctypes.c_void_p(4096)
-    for wg, it in [(0, 1), (65537, 1), (1, 0), (1, (1 << 24) + 1)]:
-        assert lib.ws_probe_mfma(wg, it, fake, ctypes.byref(flop), None) == 1, (wg, it)
-    assert lib.ws_probe_mfma(1, 1, None, ctypes.byref(flop), None) == 1
+    for probe in (lib.ws_probe_mfma, lib.ws_probe_mfma_random):
+        for wg, it in [(0, 1), (65537, 1), (1, 0), (1, (1 << 24) + 1)]:
+            assert probe(wg, it, fake, ctypes.byref(flop), None) == 1, (wg, it)
+        assert probe(1, 1, None, ctypes.byref(flop), None) == 1
     assert lib.ws_probe_read(fake, 0, 1, fake, None) == 1
     assert lib.ws_probe_read(fake, 24, 1, fake, None) == 1          # not a multiple of 16
     assert lib.ws_probe_read(ctypes.c_void_p(4104), 32, 1, fake, None) == 1  # misaligned

@@ -288,6 +288,7 @@ def test_calibration_probes(ws):
     h = torch.cuda.current_stream().cuda_stream
     flop = ws.ws_probe_mfma(8, 16, sink.data_ptr(), h)
     assert flop == 8 * 4 * 16 * 4 * 2.0 * 32 * 32 * 16
+    assert ws.ws_probe_mfma_random(8, 16, sink.data_ptr(), h) == flop
     ws.ws_probe_read(buf.data_ptr(), buf.numel(), 64, sink.data_ptr() + 4, h)
     torch.cuda.synchronize()
     assert (sink.cpu() == 7.0).all()
