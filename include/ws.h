@@ -420,7 +420,12 @@ typedef struct ws_block_step_args {
 /* One sub-block step on hip_stream, in the order above.  The append follows
  * the rules of ws_kv_append (a first step of a unit takes pages, later steps
  * rewrite them; committed units are rejected); arguments, pages and the
- * rewrite rule are checked before anything is enqueued.  With timing enabled
+ * rewrite rule are checked before anything is enqueued.  The first step
+ * with a given row count (n_video + n_audio) asks hipBLASLt for up to 16
+ * algorithms per projection, times each on this step's operands on
+ * hip_stream (waiting for the stream; a few ms) and keeps the fastest; later
+ * steps with that row count reuse it (run the first one outside any stream
+ * capture).  With timing enabled
  * the two projections record ring entries of their own (path 3: QKV
  * projection, path 4: output projection), besides the append and attention
  * entries.  args: host struct, read before the call returns. */

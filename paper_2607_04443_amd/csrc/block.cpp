@@ -20,6 +20,8 @@ namespace {
 
 constexpr int kMaxPlans = 8;           // projection shapes kept per block (row counts)
 constexpr size_t kGemmWorkspace = size_t(64) << 20;
+constexpr int kTuneCandidates = 16;    // heuristic algorithms timed per new projection shape
+constexpr int kTuneRuns = 5;           // timed launches per candidate (after one untimed)
 
 struct GemmPlan {
   int64_t rows = -1;                  // M (tokens)
@@ -91,10 +93,50 @@ void free_block(ws_block* b) {
   if (b->attn) (void)hipFree(b->attn);
 }
 
+// Times each heuristic candidate on the operands it will run on (kTuneRuns
+// launches after an untimed one, HIP events on the stream) and returns the
+// index of the fastest; candidates that fail to launch or need more
+// workspace than the block holds are skipped.  Waits for the stream.
+int fastest_candidate(ws_block* b, const GemmPlan& p, const hipblasLtMatmulHeuristicResult_t* res, int found,
+                      const uint16_t* x, const uint16_t* w, uint16_t* y, hipStream_t stream) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess) return 0;
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return 0;
+  }
+  const float alpha = 1.0f, beta = 0.0f;
+  int best = 0;
+  float best_ms = -1.0f;
+  for (int i = 0; i < found; ++i) {
+    if (res[i].state != HIPBLAS_STATUS_SUCCESS || res[i].workspaceSize > kGemmWorkspace) continue;
+    auto run = [&]() {
+      return hipblasLtMatmul(b->lt, b->desc, &alpha, w, p.a, x, p.b, &beta, y, p.c, y, p.c, &res[i].algo,
+                             b->workspace, res[i].workspaceSize, stream);
+    };
+    if (run() != HIPBLAS_STATUS_SUCCESS) continue;
+    bool ok = hipEventRecord(e0, stream) == hipSuccess;
+    for (int r = 0; ok && r < kTuneRuns; ++r) ok = run() == HIPBLAS_STATUS_SUCCESS;
+    ok = ok && hipEventRecord(e1, stream) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
+    float ms = 0.0f;
+    if (!ok || hipEventElapsedTime(&ms, e0, e1) != hipSuccess) continue;
+    if (best_ms < 0.0f || ms < best_ms) {
+      best_ms = ms;
+      best = i;
+    }
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return best;
+}
+
 // Row-major Y[M][N] = X[M][K] W[K][N] in hipBLASLt's column-major terms:
 // Y^T (N x M, ld N) = W^T (N x K, ld N) X^T (K x M, ld K), no transposes.
-// The layouts and the heuristic's algorithm are kept per (projection, M).
-ws_status gemm_plan(ws_block* b, int which, int64_t m, const GemmPlan** out) {
+// The layouts and the algorithm are kept per (projection, M): a new M asks
+// the heuristic for up to kTuneCandidates algorithms and keeps the one that
+// runs fastest on this step's operands (x, w -> y).
+ws_status gemm_plan(ws_block* b, int which, int64_t m, const uint16_t* x, const uint16_t* w, uint16_t* y,
+                    hipStream_t stream, const GemmPlan** out) {
   const int64_t k = b->hidden, n = which == 0 ? 3 * int64_t(b->hidden) : b->hidden;
   for (const GemmPlan& p : b->plans[which])
     if (p.rows == m) {
@@ -107,14 +149,16 @@ ws_status gemm_plan(ws_block* b, int which, int64_t m, const GemmPlan** out) {
   WS_LT(hipblasLtMatrixLayoutCreate(&p.a, HIP_R_16BF, n, k, n));
   WS_LT(hipblasLtMatrixLayoutCreate(&p.b, HIP_R_16BF, k, m, k));
   WS_LT(hipblasLtMatrixLayoutCreate(&p.c, HIP_R_16BF, n, m, n));
-  hipblasLtMatmulHeuristicResult_t res[1];
+  hipblasLtMatmulHeuristicResult_t res[kTuneCandidates];
   int found = 0;
-  WS_LT(hipblasLtMatmulAlgoGetHeuristic(b->lt, b->desc, p.a, p.b, p.c, p.c, b->pref, 1, res, &found));
+  WS_LT(hipblasLtMatmulAlgoGetHeuristic(b->lt, b->desc, p.a, p.b, p.c, p.c, b->pref, kTuneCandidates, res,
+                                        &found));
   if (found < 1) return ws_internal::fail(WS_ERR_UNSUPPORTED, "hipBLASLt found no algorithm for %lld x %lld x %lld",
                                           static_cast<long long>(m), static_cast<long long>(n),
                                           static_cast<long long>(k));
-  p.algo = res[0].algo;
-  p.workspace = res[0].workspaceSize;
+  const int best = found > 1 ? fastest_candidate(b, p, res, found, x, w, y, stream) : 0;
+  p.algo = res[best].algo;
+  p.workspace = res[best].workspaceSize;
   p.rows = m;
   *out = &p;
   return WS_OK;
@@ -221,11 +265,19 @@ ws_status ws_block_step(ws_block* b, const ws_block_step_args* s, void* hip_stre
           st != WS_OK)
         return st;
   }
-  // both projections' layouts and algorithms are resolved before anything is enqueued
-  const GemmPlan *p_qkv = nullptr, *p_out = nullptr;
-  if (ws_status st = gemm_plan(b, 0, n, &p_qkv); st != WS_OK) return st;
-  if (ws_status st = gemm_plan(b, 1, n, &p_out); st != WS_OK) return st;
+  // both projections' layouts and algorithms are resolved before the step
+  // is enqueued (a new row count times the candidates on the step's own
+  // operands: the output projection's input is the attention buffer as it
+  // stands, its output y, which the step then overwrites)
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  uint16_t* attn = s->attn_out ? static_cast<uint16_t*>(s->attn_out) : b->attn;
+  const GemmPlan *p_qkv = nullptr, *p_out = nullptr;
+  if (ws_status st = gemm_plan(b, 0, n, static_cast<const uint16_t*>(s->x), b->w_qkv, b->qkv, stream, &p_qkv);
+      st != WS_OK)
+    return st;
+  if (ws_status st = gemm_plan(b, 1, n, attn, b->w_out, static_cast<uint16_t*>(s->y), stream, &p_out);
+      st != WS_OK)
+    return st;
   ws_cache* c = b->cache;
   const int64_t hid = b->hidden, row3 = 3 * hid;
   // Every argument of the two library calls is checked by them before they
@@ -273,7 +325,6 @@ ws_status ws_block_step(ws_block* b, const ws_block_step_args* s, void* hip_stre
   add(0, s->n_video, WS_KIND_VIDEO, s->video_positions);
   if (s->n_audio > 0) add(s->n_video, s->n_audio, WS_KIND_AUDIO, s->audio_positions);
   if (ws_status st = ws_step_append(c, n_kv, kv, n_qs, qs, hip_stream); st != WS_OK) return st;
-  uint16_t* attn = s->attn_out ? static_cast<uint16_t*>(s->attn_out) : b->attn;
   auto call = [&](int32_t row0, int32_t rows, const ws_mask_spec& m) {
     ws_attn_call a{};
     a.q = b->qprep + row0 * hid;
