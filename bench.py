@@ -84,6 +84,10 @@ def parse():
                     help="summarise one rocprofv3 --pmc -f csv run of --pmc-driver with the MFMA and "
                          "instruction counters (GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES, "
                          "SQ_INSTS_VALU_MFMA_MOPS_BF16, ...) for unit_attn_kernel as markdown")
+    ap.add_argument("--trace-summary", metavar="CSV",
+                    help="summarise the kernel_trace.csv of one rocprofv3 --kernel-trace -f csv run of "
+                         "the default bench as markdown: durations per kernel and grid, and the "
+                         "contract steps' append, video and merge medians")
     ap.add_argument("--pmc-summary", nargs="+", metavar="DIR",
                     help="summarise rocprofv3 --pmc -f csv runs of --pmc-driver as markdown: "
                          "FETCH_SIZE and WRITE_SIZE of 'step', optionally followed by FETCH_SIZE "
@@ -637,6 +641,57 @@ MFMA_COUNTERS = ("GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MO
                  "SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_INSTS_VALU SQ_LDS_BANK_CONFLICT SQ_WAVES")
 
 
+def trace_summary(path, warmup=100, steps=200):
+    """Kernel durations of a --kernel-trace run of the default bench, grouped
+    by kernel and grid, and the medians of the contract steps (the first
+    `steps` (append, video, merge) triples after `warmup`, in launch
+    order)."""
+    import csv
+    import statistics
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Start_Timestamp"]))
+    groups, order, seq = {}, [], []
+    for r in rows:
+        name = r["Kernel_Name"]
+        short = name.replace("(anonymous namespace)", "anon").split("(")[0].split("::")[-1].strip()
+        if short.startswith("void "):
+            short = short[5:]
+        if "rocclr" in name:
+            short = name.split("(")[0][:40]
+        if "at::native" in name:
+            short = name[:40] + "..."
+        if name.startswith("Cijk_"):  # hipBLASLt's generated GEMM kernels
+            tile = [t for t in name.split("_") if t.startswith("MT")]
+            short = f"hipBLASLt GEMM (macro tile {tile[0][2:] if tile else '?'})"
+        wg = int(r["Grid_Size_X"]) // int(r["Workgroup_Size_X"])
+        wgy = int(r["Grid_Size_Y"]) // int(r["Workgroup_Size_Y"])
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        label = ""
+        if short == "unit_attn_kernel" and wg == 256:
+            label = "long history (30616 keys)" if d > 400 else "v0.2 unit, 8536 keys"
+        key = (short, wg, wgy, label)
+        if key not in groups:
+            order.append(key)
+        groups.setdefault(key, []).append(d)
+        seq.append((short, wg, d))
+    print("| kernel | workgroups | workload | calls | avg us | median us | min us | max us |")
+    print("|---|---|---|---|---|---|---|---|")
+    for key in sorted(order, key=lambda k: -sum(groups[k])):
+        v = groups[key]
+        wgs = f"{key[1]}" + (f", {key[2]}" if key[2] > 1 else "")
+        print(f"| {key[0]} | {wgs} | {key[3]} | {len(v)} | {statistics.mean(v):.2f} | "
+              f"{statistics.median(v):.2f} | {min(v):.2f} | {max(v):.2f} |")
+    triples = []
+    for i in range(len(seq) - 2):
+        if (seq[i][0] == "kv_append_kernel" and seq[i + 1][0] == "unit_attn_kernel" and seq[i + 1][1] == 256
+                and seq[i + 2][0] == "step_combine_kernel"):
+            triples.append((seq[i][2], seq[i + 1][2], seq[i + 2][2]))
+    contract = triples[warmup:warmup + steps]
+    if contract:
+        med = [statistics.median(t[j] for t in contract) for j in range(3)]
+        print(f"\nContract steps ({len(contract)} after {warmup} warm-up, medians): append {med[0]:.2f} us, "
+              f"video {med[1]:.2f} us, merge {med[2]:.2f} us: {sum(med):.1f} us of kernel time per step.")
+
+
 def mfma_summary(d):
     """MFMA utilisation of unit_attn_kernel (256 workgroups) from one counter
     run of the step driver: per dispatch, median over the dispatches.
@@ -771,6 +826,9 @@ def main():
     args = parse()
     if args.mfma_summary:
         mfma_summary(args.mfma_summary)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary)
         return
     if args.pmc_summary:
         if len(args.pmc_summary) not in (2, 4):
