@@ -666,8 +666,9 @@ def trace_summary(path, warmup=100, steps=200):
         wgy = int(r["Grid_Size_Y"]) // int(r["Workgroup_Size_Y"])
         d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
         label = ""
-        if short == "unit_attn_kernel" and wg == 256:
-            label = "long history (30616 keys)" if d > 400 else "v0.2 unit, 8536 keys"
+        if short == "unit_attn_kernel" and wg == 256:  # by duration: 1176, 8536 or 30616 keys
+            label = ("long history (30616 keys)" if d > 400 else "v0.2 unit, 8536 keys" if d > 100
+                     else "v0.2 single unit, 1176 keys")
         key = (short, wg, wgy, label)
         if key not in groups:
             order.append(key)
