@@ -910,32 +910,6 @@ __device__ __forceinline__ void video_flush(const VideoCtx& c, VideoState& st, c
   }
 }
 
-// The partition's lookups in 32-bit arithmetic when every intermediate
-// value fits (the check is uniform and cheap; 64-bit division is a long
-// instruction sequence): with len = heads * (pages + seg_cost), every
-// product below is at most (len + 1) * (groups + 1).  Same integers as
-// video_group_of / video_group_lo.
-__device__ __forceinline__ bool part_fits32(const VideoPartition& p) {
-  const int64_t len = p.heads * (p.pages + p.seg_cost);
-  return (len + 1) * (p.groups + 1) < (int64_t(1) << 32);
-}
-__device__ __forceinline__ int64_t group_of(const VideoPartition& p, int64_t x) {
-  if (!part_fits32(p)) return video_group_of(p, x);
-  const uint32_t pages = static_cast<uint32_t>(p.pages), cost = static_cast<uint32_t>(p.seg_cost);
-  const uint32_t stride = pages + cost, len = static_cast<uint32_t>(p.heads) * stride;
-  const uint32_t ux = static_cast<uint32_t>(x), h = ux / pages;
-  const uint32_t place = h * stride + cost + (ux - h * pages);
-  return static_cast<int64_t>(((place + 1) * static_cast<uint32_t>(p.groups) + len - 1) / len) - 1;
-}
-__device__ __forceinline__ int64_t group_lo(const VideoPartition& p, int64_t g) {
-  if (!part_fits32(p)) return video_group_lo(p, g);
-  const uint32_t pages = static_cast<uint32_t>(p.pages), cost = static_cast<uint32_t>(p.seg_cost);
-  const uint32_t stride = pages + cost, len = static_cast<uint32_t>(p.heads) * stride;
-  const uint32_t v0 = static_cast<uint32_t>(g) * len / static_cast<uint32_t>(p.groups);
-  const uint32_t h = v0 / stride, o = v0 - h * stride;
-  return static_cast<int64_t>(h * pages + (o > cost ? o - cost : 0u));
-}
-
 // One segment of a video workgroup's work: the query tile of rows
 // [q_lo, min(q_lo + 256, q_hi)) of head `head` against entries
 // [p_begin, p_end) of the call's page list, which is key range `seg` of the
@@ -1243,7 +1217,7 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
     return;
   }
   const VideoPartition part{a.num_heads, n_pages, a.seg_cost, tab[ci].n_groups};
-  const int64_t lo = group_lo(part, group), hi = group_lo(part, group + 1);
+  const int64_t lo = video_group_lo(part, group), hi = video_group_lo(part, group + 1);
   // The rider rows' own pages: in the last query tile's workgroup of the
   // group that holds a head's last page, the waves without rows of their
   // own (the last rx_waves of the 8) attend them for that head before they
@@ -1255,8 +1229,8 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
     if (k >= 0) {
       for (int64_t head = lo / n_pages; head <= (hi - 1) / n_pages; ++head) {
         const int64_t h0 = head * n_pages;
-        if (group_of(part, h0 + n_pages - 1) != group) continue;
-        rider_pages_wave(a, static_cast<int>(head), static_cast<int>(group - group_of(part, h0) + 1), k,
+        if (video_group_of(part, h0 + n_pages - 1) != group) continue;
+        rider_pages_wave(a, static_cast<int>(head), static_cast<int>(group - video_group_of(part, h0) + 1), k,
                          a.rx_waves);
       }
     }
@@ -1265,8 +1239,8 @@ __global__ __launch_bounds__(kVideoWaves * 64) void unit_attn_kernel(const AttnA
   for (int64_t x = lo; x < hi; first = false) {
     const int64_t head = x / n_pages, h0 = head * n_pages;
     const int64_t x_end = min(hi, h0 + n_pages);
-    const int64_t g_first = group_of(part, h0);
-    const int64_t g_last = group_of(part, h0 + n_pages - 1);
+    const int64_t g_first = video_group_of(part, h0);
+    const int64_t g_last = video_group_of(part, h0 + n_pages - 1);
     const VideoSeg sg{static_cast<int>(head), page0 + static_cast<int>(x - h0), page0 + static_cast<int>(x_end - h0),
                       static_cast<int>(group - g_first), static_cast<int>(g_last - g_first + 1), q_lo, q_hi};
     video_segment(a, sg, first);
@@ -1643,7 +1617,7 @@ __device__ __forceinline__ void combine_block(const CombineArgs& a, int bid) {
   if (a.r_groups > 0) {  // the ranges the video kernel wrote for rider rows
     const VideoPartition part{a.num_heads, a.r_pages, a.seg_cost, a.r_groups};
     const int64_t h0 = static_cast<int64_t>(head) * a.r_pages;
-    n_splits += static_cast<int>(group_of(part, h0 + a.r_pages - 1) - group_of(part, h0) + 1) +
+    n_splits += static_cast<int>(video_group_of(part, h0 + a.r_pages - 1) - video_group_of(part, h0) + 1) +
                 a.r_extra;  // and those of the rows' own pages
   }
   const int d0 = 8 * lane;
@@ -1724,7 +1698,7 @@ __device__ __forceinline__ void video_combine_block(const CombineArgs& a, const_
   if (n_pages == 0) return;
   const VideoPartition part{a.num_heads, n_pages, a.seg_cost, cls_groups};
   const int64_t h0 = static_cast<int64_t>(head) * n_pages;
-  const int n_ranges = static_cast<int>(group_of(part, h0 + n_pages - 1) - group_of(part, h0) + 1);
+  const int n_ranges = static_cast<int>(video_group_of(part, h0 + n_pages - 1) - video_group_of(part, h0) + 1);
   if (n_ranges < 2) return;
   const int d0 = 8 * lane;
   const int64_t split_stride = static_cast<int64_t>(a.num_heads) * a.n_q;

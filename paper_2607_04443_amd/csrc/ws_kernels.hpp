@@ -50,17 +50,42 @@ __host__ __device__ inline int64_t video_place(const VideoPartition& p, int64_t 
   const int64_t h = x / p.pages;
   return h * (p.pages + p.seg_cost) + p.seg_cost + (x - h * p.pages);
 }
-// The group that holds unit x.
-__host__ __device__ inline int64_t video_group_of(const VideoPartition& p, int64_t x) {
+// The group that holds unit x, and the first unit of group g's share
+// (g = groups gives the end), in 64-bit arithmetic.
+__host__ __device__ inline int64_t video_group_of_wide(const VideoPartition& p, int64_t x) {
   const int64_t len = p.heads * (p.pages + p.seg_cost);
   return ((video_place(p, x) + 1) * p.groups + len - 1) / len - 1;
 }
-// The first unit of group g's share (g = groups gives the end).
-__host__ __device__ inline int64_t video_group_lo(const VideoPartition& p, int64_t g) {
+__host__ __device__ inline int64_t video_group_lo_wide(const VideoPartition& p, int64_t g) {
   const int64_t len = p.heads * (p.pages + p.seg_cost);
   const int64_t v0 = g * len / p.groups;
   const int64_t h = v0 / (p.pages + p.seg_cost), o = v0 - h * (p.pages + p.seg_cost);
   return h * p.pages + (o > p.seg_cost ? o - p.seg_cost : 0);
+}
+// Whether the same lookups fit 32-bit arithmetic: with len = heads * (pages
+// + seg_cost), every intermediate value is at most (len + 1) * (groups + 1).
+// The 32-bit form gives the same integers; on the GPU it avoids the long
+// instruction sequence of a 64-bit division.
+__host__ __device__ inline bool video_fits32(const VideoPartition& p) {
+  const int64_t len = p.heads * (p.pages + p.seg_cost);
+  return (len + 1) * (p.groups + 1) < (int64_t(1) << 32);
+}
+// The lookups the host and the kernels use.
+__host__ __device__ inline int64_t video_group_of(const VideoPartition& p, int64_t x) {
+  if (!video_fits32(p)) return video_group_of_wide(p, x);
+  const uint32_t pages = static_cast<uint32_t>(p.pages), cost = static_cast<uint32_t>(p.seg_cost);
+  const uint32_t stride = pages + cost, len = static_cast<uint32_t>(p.heads) * stride;
+  const uint32_t ux = static_cast<uint32_t>(x), h = ux / pages;
+  const uint32_t place = h * stride + cost + (ux - h * pages);
+  return static_cast<int64_t>(((place + 1) * static_cast<uint32_t>(p.groups) + len - 1) / len) - 1;
+}
+__host__ __device__ inline int64_t video_group_lo(const VideoPartition& p, int64_t g) {
+  if (!video_fits32(p)) return video_group_lo_wide(p, g);
+  const uint32_t pages = static_cast<uint32_t>(p.pages), cost = static_cast<uint32_t>(p.seg_cost);
+  const uint32_t stride = pages + cost, len = static_cast<uint32_t>(p.heads) * stride;
+  const uint32_t v0 = static_cast<uint32_t>(g) * len / static_cast<uint32_t>(p.groups);
+  const uint32_t h = v0 / stride, o = v0 - h * stride;
+  return static_cast<int64_t>(h * pages + (o > cost ? o - cost : 0u));
 }
 
 struct RopeTables {
