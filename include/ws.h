@@ -391,7 +391,9 @@ typedef struct ws_block ws_block; /* opaque; owned by the library */
  *   kept alive and unchanged while the block is used;
  *   max_rows: most tokens (n_video + n_audio) a step takes, 1..max_q_tokens.
  * Allocates the GEMM workspace (64 MiB) and the step's Q/K/V, prepared-query
- * and attention buffers (max_rows rows); ws_block_step allocates nothing.
+ * and attention buffers (max_rows rows); ws_block_step allocates no device
+ * memory (its first step with a new row count creates, and destroys, two
+ * HIP events to time the GEMM candidates).
  * The cache must outlive the block.  Synchronous. */
 WS_API ws_status ws_block_create(ws_cache* cache, const void* w_qkv, const void* w_out, int32_t max_rows,
                                  ws_block** out);
