@@ -79,6 +79,31 @@ def test_catch_up_three_units_and_an_empty_group(ws):
         cache.close()
 
 
+def test_catch_up_at_full_width(ws):
+    """The catch-up the bench times: three 920-row units (7, 8 and 9, each
+    over its own 8-unit window: 8536 keys) in one call with all 40 heads,
+    where the three query classes share one round of the CUs and every head
+    is split into key ranges.  Heads 0, 13, 26 and 39 of every row against
+    the oracle, with the a-priori rounding bound."""
+    from helpers import rounding_bound
+    H, grid = 40, (23, 40)
+    heads = [0, 13, 26, 39]
+    cache, oc, rng, keep = _build(ws, H, grid, 256, 10, 52)
+    try:
+        spec = [(7, -1, 0b011, 920), (8, 0, 0b011, 920), (9, 1, 0b011, 920)]
+        q, pos = _queries(rng, H, spec, grid)
+        got = bf16_f64(_run_groups(ws, cache, q, pos, spec, H))[:, heads, :]
+        ref, _ = oracle.unit_attention_groups(oc, q, spec, positions=pos, gamma=np.ones(128), eps=1e-6,
+                                              heads=heads)
+        for i, (u, mn, km, n) in enumerate(spec):
+            rows = slice(920 * i, 920 * (i + 1))
+            bound = rounding_bound(oc, q[rows], u, positions=pos[rows], gamma=np.ones(128), eps=1e-6,
+                                   min_visible_unit=mn, kind_mask=km, heads=heads)
+            print(f"unit {u}", assert_gates(got[rows], ref[rows], label=f"catch-up unit {u}", bound=bound))
+    finally:
+        cache.close()
+
+
 def test_groups_equal_separate_calls_with_one_range_per_head(ws):
     """With one key range per head (forced), every group's rows are computed
     exactly as a ws_unit_attention call of that group alone: bit for bit."""
