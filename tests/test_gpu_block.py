@@ -121,3 +121,63 @@ def test_block_step_rejects_before_enqueue(ws):
     finally:
         block.close()
         cache.close()
+
+
+def test_block_step_at_bench_size(ws):
+    """The sub-block the bench times: 40 heads (hidden 5120), a 924-row step
+    (920 video + 4 audio tokens) over a 256-token slice and 8 history units,
+    with the projections' algorithms picked by timing at this row count.
+    Attention output and projected output, all heads, against the oracle."""
+    import torch
+    H_, grid, cond, audio, hist = 40, (23, 40), 256, 4, 8
+    hid = H_ * 128
+    lu = grid[0] * grid[1]
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 63))
+    cache = ws.Cache(H_, 4 + (hist + 2) * 16 + 8, max_q_tokens=1024)
+    oc = oracle.OracleCache(num_heads=H_)
+    g = np.ones(128, np.float32)
+    gd = dev_f32(g)
+    keep = [gd]
+    block = None
+    try:
+        ck, cv = synth.normal_bf16(rng, (cond, H_, 128)), synth.normal_bf16(rng, (cond, H_, 128))
+        keep += [to_dev(ck), to_dev(cv)]
+        cache.append(0, ws.WS_KIND_COND, keep[-2], keep[-1], ws.WS_APPEND_RAW)
+        oc.append(0, oracle.KIND_COND, ck, cv, oracle.MODE_RAW)
+        for u in range(hist):
+            for kind, n, pos in ((ws.WS_KIND_VIDEO, lu, synth.video_positions(u, grid)),
+                                 (ws.WS_KIND_AUDIO, audio, synth.audio_positions(u, audio))):
+                k, v = synth.normal_bf16(rng, (n, H_, 128)), synth.normal_bf16(rng, (n, H_, 128))
+                dk, dv, dp = to_dev(k), to_dev(v), dev_i32(pos)
+                keep += [dk, dv, dp]
+                cache.append(u, kind, dk, dv, ws.WS_APPEND_NORM_ROPE, dp, gd, 1e-6)
+                oc.append(u, kind, k, v, oracle.MODE_NORM_ROPE, pos, g, 1e-6)
+            cache.commit(u)
+            oc.commit(u)
+        # N(0, 1) / 64 (about 1 / sqrt(hidden); a power of two keeps the draw's bf16 rounding)
+        w_qkv = synth.bf16_bits(rng.standard_normal((hid, 3 * hid), dtype=np.float32) * np.float32(2 ** -6))
+        w_out = synth.bf16_bits(rng.standard_normal((hid, hid), dtype=np.float32) * np.float32(2 ** -6))
+        dwq, dwo = to_dev(w_qkv), to_dev(w_out)
+        keep += [dwq, dwo]
+        block = ws.Block(cache, dwq, dwo, max_rows=lu + audio)
+        x = synth.normal_bf16(rng, (lu + audio, hid))
+        vpos, apos = synth.video_positions(hist, grid), synth.audio_positions(hist, audio)
+        dx, dvp, dap = to_dev(x), dev_i32(vpos), dev_i32(apos)
+        y = torch.full_like(dx, float("nan"))
+        o = torch.full_like(dx, float("nan"))
+        keep += [dx, dvp, dap, y, o]
+        block.step(dx, lu, hist, dvp, dap, gd, gd, y,
+                   ws.mask_spec(hist, -(2 ** 31), (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
+                   ws.mask_spec(hist, -(2 ** 31), (ws.WS_KIND_COND, ws.WS_KIND_VIDEO, ws.WS_KIND_AUDIO)),
+                   attn_out=o)
+        torch.cuda.synchronize()
+        ry, ro = oracle.block_step(oc, x, lu, w_qkv, w_out, hist, video_positions=vpos, audio_positions=apos,
+                                   gamma_q=np.ones(128), gamma_k=np.ones(128), eps=1e-6,
+                                   video_mask=(-(2 ** 31), 0b011), audio_mask=(-(2 ** 31), 0b111))
+        got_o = bf16_f64(from_dev(o)).reshape(-1, H_, 128)
+        print("attention", assert_gates(got_o, ro, label="bench-size block attention"))
+        print("output", assert_gates(bf16_f64(from_dev(y)), ry, label="bench-size block output"))
+    finally:
+        if block is not None:
+            block.close()
+        cache.close()
