@@ -77,3 +77,33 @@ def test_noalloc_step_matches_step_attention(ws):
         assert np.isfinite(synth.bf16_to_f32(from_dev(ov))).all()
     finally:
         L.close()
+
+
+def test_noalloc_step_with_riding_audio_rows(ws):
+    """The bench's step shape with prepared queries, where the audio rows ride
+    in the video kernel and their key ranges (the shared pages' and the
+    audio-token pages') also live in the static workspace: bit for bit equal
+    to ws_step_attention, on a full step and then a smaller one."""
+    import torch
+    from test_gpu_riders import Step
+    S = Step(ws, 40, (23, 40), 256, 4, 8, 71)
+    try:
+        u = S.unit
+        qv, qa = S.queries(920), S.queries(4)
+        for n_v, n_a, mn in ((920, 4, -(2 ** 31)), (300, 2, u - 2)):
+            dqv, dqa = to_dev(qv[:n_v]), to_dev(qa[:n_a])
+            S.keep += [dqv, dqa]
+            outs = []
+            for fn in (S.cache.step_attention, S.cache.step_attention_noalloc):
+                ov, oa = torch.full_like(dqv, float("nan")), torch.full_like(dqa, float("nan"))
+                fn(dict(q=dqv, out=ov, mask=ws.mask_spec(u, mn, VIDEO_KINDS), mode=ws.WS_QUERY_PREPARED),
+                   dict(q=dqa, out=oa, mask=ws.mask_spec(u, mn, ALL_KINDS), mode=ws.WS_QUERY_PREPARED))
+                torch.cuda.synchronize()
+                outs.append((from_dev(ov), from_dev(oa)))
+            (rv, ra), (nv, na) = outs
+            print(f"noalloc with riders: {n_v} + {n_a} rows", flush=True)
+            assert np.isfinite(synth.bf16_to_f32(nv)).all() and np.isfinite(synth.bf16_to_f32(na)).all()
+            np.testing.assert_array_equal(nv, rv)
+            np.testing.assert_array_equal(na, ra)
+    finally:
+        S.close()
