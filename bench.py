@@ -686,6 +686,15 @@ def trace_summary(path, warmup=100, steps=200):
         if (seq[i][0] == "kv_append_kernel" and seq[i + 1][0] == "unit_attn_kernel" and seq[i + 1][1] == 256
                 and seq[i + 2][0] == "step_combine_kernel"):
             triples.append((seq[i][2], seq[i + 1][2], seq[i + 2][2]))
+    # the breakdown pass: separate calls after each step's append, each
+    # unit_attn_kernel followed by its own video_combine_kernel (the launches
+    # roofline.achieved averages)
+    separate = [seq[i][2] for i in range(1, len(seq) - 1)
+                if seq[i][0] == "unit_attn_kernel" and seq[i][1] == 256 and 100 < seq[i][2] < 400
+                and seq[i - 1][0] == "kv_append_kernel" and seq[i + 1][0] == "video_combine_kernel"]
+    if separate:
+        print(f"\nBreakdown pass (separate video calls): {len(separate)} unit_attn_kernel launches, average "
+              f"{statistics.mean(separate):.2f} us, median {statistics.median(separate):.2f} us.")
     contract = triples[warmup:warmup + steps]
     if contract:
         med = [statistics.median(t[j] for t in contract) for j in range(3)]

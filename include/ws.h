@@ -461,12 +461,16 @@ WS_API ws_status ws_cache_set_option(ws_cache* cache, ws_option opt, int32_t val
 
 /* Launch timing of the attention entry points (for benchmarks and
  * profilers).  While enabled, every ws_unit_attention / ws_audio_attention
- * call records three HIP events on its own stream: before its attention
- * kernel, between that kernel and the split-KV merge kernel, and after the
- * merge; every append call (ws_kv_append, ws_kv_append_many, ws_step_append)
- * records events before its first and after its last launch (merge time 0).
- * The cache keeps the events of the last `capacity` calls in a ring (older
- * calls are overwritten); recording adds no synchronization. */
+ * call records three HIP events on its own stream: the start and the end of
+ * its attention kernel, taken by the kernel's dispatch itself
+ * (hipExtLaunchKernelGGL: the kernel's execution, as a profiler's kernel
+ * trace reports it), and one recorded after the split-KV merge kernel;
+ * every append call (ws_kv_append, ws_kv_append_many, ws_step_append) takes
+ * the start of its first launch and the end of its last (merge time 0).
+ * The projections of ws_block_step are timed with events recorded before
+ * and after them.  The cache keeps the events of the last `capacity` calls
+ * in a ring (older calls are overwritten); recording adds no
+ * synchronization. */
 typedef struct ws_call_timing {
   int32_t path;      /* 0 = video attention, 1 = audio attention, 2 = append,
                         3 = QKV projection, 4 = output projection (ws_block_step),

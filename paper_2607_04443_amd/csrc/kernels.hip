@@ -14,6 +14,8 @@
 // The attention is the performer's per-step attention over its K/V cache
 // (Wan-Streamer v0.2, Sec. 3); block-causal visibility (Fig. 1 caption) is
 // resolved on the host into the list of visible pages.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 #include <cstddef>
 #include <mutex>
@@ -1791,22 +1793,34 @@ hipError_t static_scratch(void** ptr) {
   return hipSuccess;
 }
 
-hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
+// With start or stop events, a launch goes through hipExtLaunchKernelGGL,
+// whose events take the dispatch's own start and end timestamps (the
+// kernel's execution, without the queue's event processing around it).
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   const int tiles = a.n_blocks * a.num_heads;
   const int grid = std::min(tiles, std::max(1, a.grid_blocks));
-  hipLaunchKernelGGL(kv_append_kernel, dim3(grid), dim3(256), 0, stream, a);
+  if (start || stop)
+    hipExtLaunchKernelGGL(kv_append_kernel, dim3(grid), dim3(256), 0, stream, start, stop, 0, a);
+  else
+    hipLaunchKernelGGL(kv_append_kernel, dim3(grid), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_wg);
-  hipLaunchKernelGGL(unit_attn_kernel, grid, dim3(kVideoWaves * 64), 0, stream, a);
+hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+  const dim3 grid(a.n_wg), block(kVideoWaves * 64);
+  if (start || stop)
+    hipExtLaunchKernelGGL(unit_attn_kernel, grid, block, 0, stream, start, stop, 0, a);
+  else
+    hipLaunchKernelGGL(unit_attn_kernel, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(a.num_heads * a.n_qtiles * a.n_splits);
-  hipLaunchKernelGGL(audio_attn_kernel, grid, dim3(256), 0, stream, a);
+hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+  const dim3 grid(a.num_heads * a.n_qtiles * a.n_splits);
+  if (start || stop)
+    hipExtLaunchKernelGGL(audio_attn_kernel, grid, dim3(256), 0, stream, start, stop, 0, a);
+  else
+    hipLaunchKernelGGL(audio_attn_kernel, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

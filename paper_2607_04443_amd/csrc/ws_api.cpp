@@ -140,13 +140,16 @@ struct ws_cache {
 
 namespace ws_internal {
 
-// Timing ring slot of the next call (or -1), with its first event recorded.
-ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot) {
+// Timing ring slot of the next call (or -1), with its first event recorded
+// unless the kernel launch stamps it (stamped: the library's own kernels
+// take events 0 and 1 as their dispatch's start and end).
+ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot,
+                            bool stamped) {
   TimingRing& tr = c->timing;
   *slot = tr.cap > 0 ? tr.next : -1;
   if (*slot >= 0) {
     tr.meta[*slot] = ws_call_timing{path, splits, 0.f, 0.f};
-    WS_HIP(hipEventRecord(tr.ev[3 * *slot], stream));
+    if (!stamped) WS_HIP(hipEventRecord(tr.ev[3 * *slot], stream));
     tr.next = (tr.next + 1) % tr.cap;
     tr.count = std::min(tr.count + 1, tr.cap);
   }
@@ -157,6 +160,9 @@ ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream) {
   if (slot >= 0) WS_HIP(hipEventRecord(c->timing.ev[3 * slot + k], stream));
   return WS_OK;
 }
+
+// Event k of a timing slot, or nullptr when the call is not timed.
+hipEvent_t timing_event(ws_cache* c, int slot, int k) { return slot >= 0 ? c->timing.ev[3 * slot + k] : nullptr; }
 
 int32_t cache_heads(const ws_cache* c) { return c->cfg.num_heads; }
 int32_t cache_max_q(const ws_cache* c) { return c->cfg.max_q_tokens; }
@@ -184,6 +190,7 @@ ws_status precheck_append(const ws_cache* c, int32_t unit, ws_kind kind, int32_t
 
 using ws_internal::timing_begin_path;
 using ws_internal::timing_mark;
+using ws_internal::timing_event;
 
 namespace {
 
@@ -636,13 +643,17 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
   return WS_OK;
 }
 
-hipError_t launch_plan_kernel(const AttnPlan& p, hipStream_t stream) {
-  return p.audio ? ws::launch_audio_attention(p.a, stream) : ws::launch_unit_attention(p.a, stream);
+hipError_t launch_plan_kernel(const AttnPlan& p, hipStream_t stream, hipEvent_t start = nullptr,
+                              hipEvent_t stop = nullptr) {
+  return p.audio ? ws::launch_audio_attention(p.a, stream, start, stop)
+                 : ws::launch_unit_attention(p.a, stream, start, stop);
 }
 
 
+// A timed attention call: events 0 and 1 are the kernel's own dispatch
+// timestamps (see launch_plan_kernel), event 2 follows the merge.
 ws_status timing_begin(ws_cache* c, const AttnPlan& p, hipStream_t stream, int* slot) {
-  return timing_begin_path(c, p.audio ? 1 : 0, p.splits, stream, slot);
+  return timing_begin_path(c, p.audio ? 1 : 0, p.splits, stream, slot, true);
 }
 
 
@@ -658,9 +669,8 @@ ws_status attention_impl(bool audio, const void* q, int64_t q_tok_stride, int64_
     return st;
   int slot = -1;
   if (ws_status st = timing_begin(c, p, stream, &slot); st != WS_OK) return st;
-  hipError_t e = launch_plan_kernel(p, stream);
+  hipError_t e = launch_plan_kernel(p, stream, timing_event(c, slot, 0), timing_event(c, slot, 1));
   if (e != hipSuccess) return hip_fail(e, audio ? "audio_attn launch" : "unit_attn launch");
-  if (ws_status st = timing_mark(c, slot, 1, stream); st != WS_OK) return st;
   if (p.merge) {
     e = ws::launch_combine(p.cb, stream);
     if (e != hipSuccess) return hip_fail(e, "combine launch");
@@ -851,16 +861,18 @@ ws_status step_attention_impl(ws_cache* c, const ws_attn_call* video, const ws_a
   // rows ride in the video kernel), then one launch merging both
   int sv = -1, sa = -1;
   if (ws_status st = timing_begin(c, pv, stream, &sv); st != WS_OK) return st;
-  hipError_t e = launch_plan_kernel(pv, stream);
+  hipError_t e = launch_plan_kernel(pv, stream, timing_event(c, sv, 0), timing_event(c, sv, 1));
   if (e != hipSuccess) return hip_fail(e, "unit_attn launch");
-  if (ws_status st = timing_mark(c, sv, 1, stream); st != WS_OK) return st;
   if (ws_status st = timing_mark(c, sv, 2, stream); st != WS_OK) return st;
-  if (ws_status st = timing_begin_path(c, riders ? 5 : 1, pa.splits, stream, &sa); st != WS_OK) return st;
-  if (!riders || pa.splits > 0) {
-    e = launch_plan_kernel(pa, stream);
+  const bool audio_kernel = !riders || pa.splits > 0;
+  if (ws_status st = timing_begin_path(c, riders ? 5 : 1, pa.splits, stream, &sa, audio_kernel); st != WS_OK)
+    return st;
+  if (audio_kernel) {
+    e = launch_plan_kernel(pa, stream, timing_event(c, sa, 0), timing_event(c, sa, 1));
     if (e != hipSuccess) return hip_fail(e, "audio_attn launch");
+  } else if (ws_status st = timing_mark(c, sa, 1, stream); st != WS_OK) {
+    return st;
   }
-  if (ws_status st = timing_mark(c, sa, 1, stream); st != WS_OK) return st;
   if (pv.merge || pa.merge) {
     ws::CombineArgs none{};
     e = ws::launch_step_combine(pv.merge ? pv.cb : none, pa.merge ? pa.cb : none, stream);
@@ -1009,13 +1021,20 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
   a.flags = c->flags_dev;
   int n_segs = 0;
   int tslot = -1;
-  if (ws_status st = timing_begin_path(c, 2, n + n_q, stream, &tslot); st != WS_OK) {
+  if (ws_status st = timing_begin_path(c, 2, n + n_q, stream, &tslot, true); st != WS_OK) {
     roll_back();
     return st;
   }
-  auto flush = [&]() -> hipError_t {
+  // the first launch stamps event 0 with its start, the final one event 1
+  // with its end; one recorded by hand below when no launch takes it
+  bool started = false, stopped = false;
+  auto flush = [&](bool final_launch) -> hipError_t {
     if (a.n_blocks == 0) return hipSuccess;
-    const hipError_t e = ws::launch_kv_append(a, stream);
+    hipEvent_t ev0 = started ? nullptr : timing_event(c, tslot, 0);
+    hipEvent_t ev1 = final_launch ? timing_event(c, tslot, 1) : nullptr;
+    const hipError_t e = ws::launch_kv_append(a, stream, ev0, ev1);
+    started = started || ev0 != nullptr;
+    stopped = stopped || ev1 != nullptr;
     a.n_blocks = 0;
     n_segs = 0;
     return e;
@@ -1026,7 +1045,7 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
     int slot = -1;
     for (size_t p = 0; p < pl.size(); ++p) {
       if (a.n_blocks == ws::AppendArgs::kMaxAppendPages) {
-        if (hipError_t e = flush(); e != hipSuccess) {
+        if (hipError_t e = flush(false); e != hipSuccess) {
           roll_back();
           return hip_fail(e, "kv_append launch");
         }
@@ -1034,7 +1053,7 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
       }
       if (slot < 0) {
         if (n_segs == ws::AppendArgs::kMaxSegs) {
-          if (hipError_t e = flush(); e != hipSuccess) {
+          if (hipError_t e = flush(false); e != hipSuccess) {
             roll_back();
             return hip_fail(e, "kv_append launch");
           }
@@ -1065,7 +1084,7 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
     int slot = -1;
     for (int ch = 0; ch < chunks; ++ch) {
       if (a.n_blocks == ws::AppendArgs::kMaxAppendPages) {
-        if (hipError_t e = flush(); e != hipSuccess) {
+        if (hipError_t e = flush(false); e != hipSuccess) {
           roll_back();
           return hip_fail(e, "kv_append launch");
         }
@@ -1073,7 +1092,7 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
       }
       if (slot < 0) {
         if (n_segs == ws::AppendArgs::kMaxSegs) {
-          if (hipError_t e = flush(); e != hipSuccess) {
+          if (hipError_t e = flush(false); e != hipSuccess) {
             roll_back();
             return hip_fail(e, "kv_append launch");
           }
@@ -1100,11 +1119,14 @@ ws_status ws_step_append(ws_cache* c, int32_t n, const ws_append_item* items, in
       ++a.n_blocks;
     }
   }
-  if (hipError_t e = flush(); e != hipSuccess) {
+  if (hipError_t e = flush(true); e != hipSuccess) {
     roll_back();
     return hip_fail(e, "kv_append launch");
   }
-  if (ws_status st = timing_mark(c, tslot, 1, stream); st != WS_OK) return st;
+  if (!started)
+    if (ws_status st = timing_mark(c, tslot, 0, stream); st != WS_OK) return st;
+  if (!stopped)
+    if (ws_status st = timing_mark(c, tslot, 1, stream); st != WS_OK) return st;
   return timing_mark(c, tslot, 2, stream);
 }
 

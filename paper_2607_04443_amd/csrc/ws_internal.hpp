@@ -26,8 +26,11 @@ ws_status precheck_append(const ws_cache* c, int32_t unit, ws_kind kind, int32_t
 int32_t free_pages(const ws_cache* c);
 
 // Launch timing ring (ws_cache_timing_*): a slot for one call of `path`,
-// its first event recorded; timing_mark records event k (1, 2) of the slot.
-ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot);
+// its first event recorded (unless `stamped`: the call's kernel launch takes
+// events 0 and 1 as its dispatch's start and end); timing_mark records event
+// k (0, 1, 2) of the slot.
+ws_status timing_begin_path(ws_cache* c, int32_t path, int32_t splits, hipStream_t stream, int* slot,
+                            bool stamped = false);
 ws_status timing_mark(ws_cache* c, int slot, int k, hipStream_t stream);
 
 }  // namespace ws_internal

@@ -230,14 +230,17 @@ struct CombineArgs {
   int64_t out_head_stride;
 };
 
-hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream, hipEvent_t start = nullptr,
+                            hipEvent_t stop = nullptr);
 // Video path: 256-query tiles on 8 waves, 32x32x16 bf16 MFMA, LDS-staged
 // pages; n_groups x n_qtiles workgroups, each with an even share of the
 // (head, page) units.
-hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_unit_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start = nullptr,
+                                 hipEvent_t stop = nullptr);
 // Audio path: 4 independent waves per (head, 16-query tile, key range),
 // pages loaded straight into registers, 16x16x32 bf16 MFMA.
-hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_audio_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start = nullptr,
+                                  hipEvent_t stop = nullptr);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 // The merges of a video call (n_groups > 0) and an audio call (num_heads > 0)
 // in one launch; either may be absent (zero-initialised).
