@@ -24,7 +24,9 @@ All inputs are synthetic N(0,1) bf16 resident in HBM; H = 40 heads of 128.
 
 Prints one JSON line.  `value` is attention TFLOP/s over the whole step
 (video + audio FLOP / step time), from `steps` steps timed with nothing
-recorded in between.  A second pass of `steps` steps issues the two
+recorded in between, after `settle` untimed steps (the clocks' ramp from
+idle, reported block by block in settle_us_per_step) and `warmup` untimed
+steps: a performer runs the step back to back for as long as it streams.  A second pass of `steps` steps issues the two
 attentions as separate calls (ws_unit_attention, ws_audio_attention, each
 with its own merge) and records events around each component (the
 per-component fields) and the library's launch timing (ws_cache_timing_*):
@@ -61,10 +63,14 @@ def video_flop(lq, lk):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # The GPU takes about 20 ms of this load (some 100 steps) to settle: with
-    # 5 warm-up steps the first 50 timed steps average about 10% slower.
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    # From idle the GPU's clocks take some 30 ms of this load to settle: the
+    # first 25 steps run about 15% slower than step 150 on (settle_us_per_step
+    # in the output shows the ramp). The settle steps run before the warm-up.
+    ap.add_argument("--settle", type=int, default=200,
+                    help="untimed steps before the warm-up steps, in blocks of 25 whose average step "
+                         "times are reported as settle_us_per_step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--video-splits", type=int, default=0)
     ap.add_argument("--audio-splits", type=int, default=0)
@@ -641,11 +647,11 @@ MFMA_COUNTERS = ("GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MO
                  "SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_INSTS_VALU SQ_LDS_BANK_CONFLICT SQ_WAVES")
 
 
-def trace_summary(path, warmup=100, steps=200):
+def trace_summary(path, steps=200):
     """Kernel durations of a --kernel-trace run of the default bench, grouped
-    by kernel and grid, and the medians of the contract steps (the first
-    `steps` (append, video, merge) triples after `warmup`, in launch
-    order)."""
+    by kernel and grid, and the medians of the contract steps: the last
+    `steps` of the first unbroken run of (append, video, merge) launch
+    triples (settle, warm-up and contract steps, in launch order)."""
     import csv
     import statistics
     rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Start_Timestamp"]))
@@ -681,11 +687,14 @@ def trace_summary(path, warmup=100, steps=200):
         wgs = f"{key[1]}" + (f", {key[2]}" if key[2] > 1 else "")
         print(f"| {key[0]} | {wgs} | {key[3]} | {len(v)} | {statistics.mean(v):.2f} | "
               f"{statistics.median(v):.2f} | {min(v):.2f} | {max(v):.2f} |")
-    triples = []
+    triples, last = [], None
     for i in range(len(seq) - 2):
         if (seq[i][0] == "kv_append_kernel" and seq[i + 1][0] == "unit_attn_kernel" and seq[i + 1][1] == 256
                 and seq[i + 2][0] == "step_combine_kernel"):
+            if last is not None and i != last + 3:
+                break
             triples.append((seq[i][2], seq[i + 1][2], seq[i + 2][2]))
+            last = i
     # the breakdown pass: separate calls after each step's append, each
     # unit_attn_kernel followed by its own video_combine_kernel (the launches
     # roofline.achieved averages)
@@ -695,10 +704,11 @@ def trace_summary(path, warmup=100, steps=200):
     if separate:
         print(f"\nBreakdown pass (separate video calls): {len(separate)} unit_attn_kernel launches, average "
               f"{statistics.mean(separate):.2f} us, median {statistics.median(separate):.2f} us.")
-    contract = triples[warmup:warmup + steps]
+    contract = triples[-steps:]
     if contract:
         med = [statistics.median(t[j] for t in contract) for j in range(3)]
-        print(f"\nContract steps ({len(contract)} after {warmup} warm-up, medians): append {med[0]:.2f} us, "
+        print(f"\nContract steps ({len(contract)} after {len(triples) - len(contract)} settle and warm-up "
+              f"steps, medians): append {med[0]:.2f} us, "
               f"video {med[1]:.2f} us, merge {med[2]:.2f} us: {sum(med):.1f} us of kernel time per step.")
 
 
@@ -869,7 +879,7 @@ def main():
         return torch.from_numpy(synth.normal_bf16(rng, shape).view(np.int16)).view(
             torch.bfloat16).to(dev)
 
-    n_steps_total = args.warmup + args.steps
+    n_steps_total = args.settle + args.warmup + args.steps
     max_pages = 4 + (HIST + 2) * 16 + 8
     cache = ws.Cache(H, max_pages, max_q_tokens=1024)
     if args.video_splits:
@@ -942,6 +952,16 @@ def main():
         pmc_driver(args.pmc_driver, ws, cache, step, u, q_v, out_v, q_a, out_a, sets, gamma, eps, dev)
         cache.close()
         return
+    settle_us = []
+    torch.cuda.synchronize()
+    for b in range(0, args.settle, 25):
+        n = min(25, args.settle - b)
+        t0 = time.perf_counter()
+        for _ in range(n):
+            step(u, False)
+            u += 1
+        torch.cuda.synchronize()
+        settle_us.append(round((time.perf_counter() - t0) * 1e6 / n, 1))
     for _ in range(args.warmup):
         step(u, False)
         u += 1
@@ -1023,6 +1043,8 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_steps": args.settle,
+        "settle_us_per_step": settle_us,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
