@@ -811,7 +811,9 @@ def measured_peaks(ws, torch, stream, dev):
     10 ms) on small-integer operands and on random ones (attention's
     operands switch as many bits as the latter, and the clock the chip holds
     under a long MFMA load falls with them), and one streaming read of a
-    2 GiB buffer; medians of 7 timed runs after 3 untimed ones."""
+    2 GiB buffer (512 workgroups, each a contiguous chunk, nontemporal
+    loads: loads that allocate in the caches sustain less); medians of 7
+    timed runs after 3 untimed ones."""
     sink = torch.zeros(2, dtype=torch.float32, device=dev)
     buf = torch.zeros(1 << 31, dtype=torch.uint8, device=dev)
     h = stream.cuda_stream
@@ -835,7 +837,7 @@ def measured_peaks(ws, torch, stream, dev):
 
     t_m = timed(mfma)
     t_mr = timed(lambda: ws.ws_probe_mfma_random(2048, 20000, sink.data_ptr(), h))
-    t_r = timed(lambda: ws.ws_probe_read(buf.data_ptr(), buf.numel(), 4096, sink.data_ptr() + 4, h))
+    t_r = timed(lambda: ws.ws_probe_read(buf.data_ptr(), buf.numel(), 512, sink.data_ptr() + 4, h))
     del buf
     return {"mfma_bf16_tflops": flop[0] / t_m / 1e12, "mfma_frac_of_published": flop[0] / t_m / 1e12 / PEAK_BF16_TFLOPS,
             "mfma_bf16_random_operands_tflops": flop[0] / t_mr / 1e12,

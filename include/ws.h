@@ -511,8 +511,10 @@ WS_API ws_status ws_cache_timing_read(ws_cache* cache, ws_call_timing* out, int3
  *
  * ws_probe_read: reads the `bytes` bytes at device address buf once
  * (16-byte aligned, bytes a positive multiple of 16) with `workgroups`
- * (1..65536) workgroups of 256 threads; sink is a device uint32[1], likewise
- * written only in a case that does not occur for ordinary data. */
+ * (1..65536) workgroups of 256 threads, each reading one contiguous chunk
+ * with nontemporal loads (the form that sustains the highest read rate);
+ * sink is a device uint32[1], likewise written only in a case that does not
+ * occur for ordinary data. */
 WS_API ws_status ws_probe_mfma(int32_t workgroups, int32_t iters, float* sink, double* flop,
                                void* hip_stream);
 WS_API ws_status ws_probe_mfma_random(int32_t workgroups, int32_t iters, float* sink, double* flop,

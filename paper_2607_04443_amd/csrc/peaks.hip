@@ -60,18 +60,27 @@ __global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, fl
   if (s == -1.0f) sink[0] = s;
 }
 
-// Streams n16 16-byte words once (grid-stride, four independent loads in
-// flight per thread) and folds them with XOR.
+// Streams n16 16-byte words once and folds them with XOR.  Each workgroup
+// reads one contiguous chunk, eight independent 16-byte loads in flight per
+// thread, with the nontemporal hint: loads that allocate in the caches
+// sustain 5.5-6.2 TB/s on a 2 GiB buffer, nontemporal ones about 7 TB/s
+// (the highest read rate found for this part).
+constexpr int kReadUnroll = 8;
 __global__ __launch_bounds__(kProbeThreads) void read_probe_kernel(const u32x4* __restrict__ p,
                                                                    int64_t n16, uint32_t* sink) {
-  const int64_t stride = int64_t(gridDim.x) * kProbeThreads;
-  int64_t i = int64_t(blockIdx.x) * kProbeThreads + threadIdx.x;
+  const int64_t chunk = (n16 + gridDim.x - 1) / gridDim.x;
+  const int64_t begin = int64_t(blockIdx.x) * chunk;
+  const int64_t end = begin + chunk < n16 ? begin + chunk : n16;
+  int64_t i = begin + threadIdx.x;
   u32x4 x = {0u, 0u, 0u, 0u};
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const u32x4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
-    x ^= a ^ b ^ c ^ d;
+  for (; i + (kReadUnroll - 1) * kProbeThreads < end; i += kReadUnroll * kProbeThreads) {
+    u32x4 w[kReadUnroll];
+#pragma unroll
+    for (int k = 0; k < kReadUnroll; ++k) w[k] = __builtin_nontemporal_load(p + i + k * kProbeThreads);
+#pragma unroll
+    for (int k = 0; k < kReadUnroll; ++k) x ^= w[k];
   }
-  for (; i < n16; i += stride) x ^= p[i];
+  for (; i < end; i += kProbeThreads) x ^= __builtin_nontemporal_load(p + i);
   const uint32_t v = x.x ^ x.y ^ x.z ^ x.w;
   if (v == 0x9e3779b9u) sink[0] = v;
 }
