@@ -428,19 +428,28 @@ constexpr int kVideoSegCostPages = 6;
 int choose_video_groups(const ws_cache* c, int n_heads, int n_qtiles, int n_pages, int n_cus) {
   if (n_pages == 0) return n_heads;
   if (c->opt_video_splits > 0) return n_heads * c->opt_video_splits;
+  // Cost of G groups in pages of one query tile: rounds of the CUs times
+  // (a share's pages plus a fixed cost per segment it holds: prologue, or
+  // switch to the next head), plus the merge launch when a head is split
+  // over groups.  Shares line up with heads when G is a multiple or a
+  // divisor of H (VideoPartition), so that every group holds max(G, H) / G
+  // whole segments; otherwise the G shares cut G + H - 1 segments.
   constexpr double kSegCostPages = 9.5;
-  constexpr int64_t kMinGroupPages = 4;
-  const int64_t units = static_cast<int64_t>(n_heads) * n_pages;
+  constexpr double kMergeCostPages = 4.0;
+  const int64_t H = n_heads;
+  const int64_t units = H * n_pages;
   const int64_t one_round = std::max<int64_t>(1, n_cus / n_qtiles);
   // at most kMaxVideoSplits ranges per head: ceil(G / H) + 1 <= kMaxVideoSplits
-  const int64_t g_max = std::min<int64_t>({static_cast<int64_t>(n_heads) * (kMaxVideoSplits - 1),
-                                           std::max<int64_t>(1, units / kMinGroupPages), 4 * one_round});
-  int64_t best = std::min<int64_t>(n_heads, g_max);
+  const int64_t g_max = std::min<int64_t>({H * (kMaxVideoSplits - 1), units, 4 * one_round});
+  int64_t best = std::min<int64_t>(H, g_max);
   double best_cost = -1.0;
   for (int64_t g = 1; g <= g_max; ++g) {
     const double rounds = static_cast<double>((g + one_round - 1) / one_round);
-    const double segs = static_cast<double>(g + std::min<int64_t>(g, n_heads) - 1) / g;
-    const double cost = rounds * (static_cast<double>(units) / g + kSegCostPages * segs);
+    const bool aligned = g % H == 0 || H % g == 0;
+    const double segs = static_cast<double>(aligned ? std::max(g, H) : g + H - 1) / g;
+    const bool split = g > H || !aligned;
+    const double cost =
+        rounds * (static_cast<double>(units) / g + kSegCostPages * segs) + (split ? kMergeCostPages : 0.0);
     if (best_cost < 0 || cost < best_cost - 1e-9) {
       best = g;
       best_cost = cost;
