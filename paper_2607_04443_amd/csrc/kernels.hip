@@ -725,26 +725,30 @@ __device__ __forceinline__ void video_page(const VideoCtx& c, VideoState& st, in
   wait_dma_all_but_last_page();
 }
 
-// Fixed-shift pages, software-pipelined across pages so that every group of
-// eight MFMAs carries eight exponentials (the softmax VALU then runs in the
-// shadow of the matrix pipe throughout, instead of piling up in two phases).
-// Iteration p (page p from LDS stage kCur, V^T of page p-1 from the stage
-// before it), 32 MFMA steps with operand reads three steps ahead through a
-// ring of four registers; the last three steps read the first operands of
-// page p + 1 (complete since the previous barrier), so the ring runs on
-// across the page barrier:
-//   steps  0- 7  S tile 0 of p                 exp: tile 1 of p-1, keys 0-15
-//   steps  8-11  P*V of p-1, key chunk 2       exp: tile 1 of p-1, keys 16-31
-//   steps 12-15  S tile 1 of p, k-steps 0-3      (same)
-//   steps 16-19  P*V of p-1, key chunk 3       exp: tile 0 of p, keys 0-15
-//   steps 20-23  S tile 1 of p, k-steps 4-7      (same)
-//   steps 24-27  P*V of p, key chunk 0         exp: tile 0 of p, keys 16-31
-//   steps 28-31  P*V of p, key chunk 1
-// ("keys 0-15" of a tile are its accumulator registers 0-7 in both lane
-// halves, i.e. key chunk 0 or 2 of the page.)  The first page of a range
-// (kFirst) has no page p-1: steps 0-7 S tile 0, 8-15 S tile 1 with the
-// exponentials of tile 0 keys 0-15, 16-23 P*V chunks 0-1 with those of keys
-// 16-31.  Tile 1 of the last page is finished by video_flush.
+// Fixed-shift pages, software-pipelined across pages so that the softmax
+// VALU work is spread over the MFMA steps (it then runs in the shadow of the
+// matrix pipe instead of piling up in a few of them).  Iteration p (page p
+// from LDS stage kCur, V^T of page p-1 from the stage before it), 32 MFMA
+// steps with operand reads three steps ahead through a ring of four
+// registers; the last three steps read the first operands of page p + 1
+// (complete since the previous barrier), so the ring runs on across the page
+// barrier.  Exponentials per step in brackets ("register r" is accumulator
+// register r of a tile, in both lane halves; registers 0-7 are the tile's
+// first 16 keys):
+//   steps  0- 3  S tile 0 of p        [2: tile 1 of p-1, registers 0-3, 8-11]
+//   steps  4- 7  S tile 0 of p        [1: tile 1 of p-1, registers 4-7]
+//   steps  8-11  P*V of p-1, chunk 2  [1: tile 1 of p-1, registers 12-15]
+//   steps 12-15  P*V of p-1, chunk 3  [1: tile 0 of p, registers 0-3]
+//   steps 16-23  S tile 1 of p        [1: tile 0 of p, registers 4-11]
+//   steps 24-27  P*V of p, chunk 0    [1: tile 0 of p, registers 12-15]
+//   steps 28-31  P*V of p, chunk 1
+// Every P word is complete before the P*V step that reads it, and the
+// previous page's tile 1 is fully exponentiated (step 11) before this
+// page's tile 1 is accumulated (step 16), so their registers need not be
+// live together.  The first page of a range (kFirst) has no page p-1: steps
+// 0-7 S tile 0, 8-15 S tile 1 with the exponentials of tile 0 keys 0-15,
+// 16-23 P*V chunks 0-1 with those of keys 16-31.  Tile 1 of the last page is
+// finished by video_flush.
 constexpr int kRingAhead = 3;  // operand reads issued this many MFMA steps ahead
 struct PipeState {
   f32x16 s1;      // S tile 1 of the previous page (exp2 argument)
@@ -798,9 +802,8 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
     if (kFirst) return o < 16 ? kread(o) : vread(sv, (o - 16) & 3, (o - 16) >> 2);
     if (o < 8) return kread(o);
     if (o < 12) return vread(svp, o - 8, 2);
-    if (o < 16) return kread(8 + o - 12);
-    if (o < 20) return vread(svp, o - 16, 3);
-    if (o < 24) return kread(12 + o - 20);
+    if (o < 16) return vread(svp, o - 12, 3);
+    if (o < 24) return kread(8 + o - 16);
     return vread(sv, (o - 24) & 3, (o - 24) >> 2);
   };
   constexpr int kAhead = kRingAhead;
@@ -853,36 +856,40 @@ __device__ __forceinline__ void video_iter(const VideoCtx& c, VideoState& st, Pi
         st.o[o - 20] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p1), st.o[o - 20], 0, 0, 0);
       }
     } else {
-      if (o < 8) {
-        // all of the previous page's tile 1 is exponentiated here, so that
-        // its registers are free before this page's tile 1 is accumulated
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
-        const float ea = fast_exp2(ps.s1[o]), eb = fast_exp2(ps.s1[8 + o]);
-        if ((o & 1) == 0) {
-          e2_lo = ea;
-          e3_lo = eb;
+      // exponentials of the previous page's tile 1: registers 0-7 (key chunk
+      // 2) one per step in steps 0-7, registers 8-11 a second one in steps
+      // 0-3 and 12-15 one per step in 8-11, all done before the P*V of
+      // chunks 2 and 3 reads them; those of this page's tile 0 one per step
+      // in steps 12-27 (registers 0-7 before chunk 0 is read at step 24)
+      auto prev_exp = [&](int r, u32x4& dst) {
+        const float e = fast_exp2(ps.s1[r]);
+        if ((r & 1) == 0) {
+          if (r < 8) e2_lo = e; else e3_lo = e;
         } else {
-          const uint32_t wa = pack_bf16(e2_lo, ea), wb = pack_bf16(e3_lo, eb);
-          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wa), ones, l, false);
-          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wb), ones, l, false);
-          pp2[o >> 1] = wa;
-          pp3[o >> 1] = wb;
+          const uint32_t w = pack_bf16(r < 8 ? e2_lo : e3_lo, e);
+          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, l, false);
+          dst[(r & 7) >> 1] = w;
         }
+      };
+      if (o < 8) {
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o], o == 0 ? s_init : s0, 0, 0, 0);
+        prev_exp(o, pp2);
+        if (o < 4) prev_exp(8 + o, pp3);
       } else if (o < 12) {
         st.o[o - 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp2), st.o[o - 8], 0, 0, 0);
+        prev_exp(12 + o - 8, pp3);
       } else if (o < 16) {
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 12], o == 12 ? s_init : s1, 0, 0, 0);
-      } else if (o < 20) {
-        st.o[o - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp3), st.o[o - 16], 0, 0, 0);
-        if (o == 16 && tail) mask_tail(s0, 0);
-        exp_one(s0, o - 16, p0, (o - 16) >> 1);
+        st.o[o - 12] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pp3), st.o[o - 12], 0, 0, 0);
+        if (o == 12 && tail) mask_tail(s0, 0);
+        exp_one(s0, o - 12, p0, (o - 12) >> 1);
       } else if (o < 24) {
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[4 + o - 20], s1, 0, 0, 0);
-        exp_one(s0, o - 16, p0, (o - 16) >> 1);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, c.qreg[o - 16], o == 16 ? s_init : s1, 0, 0, 0);
+        const int r = 4 + o - 16;
+        exp_one(s0, r, r < 8 ? p0 : p1, (r & 7) >> 1);
       } else if (o < 28) {
         st.o[o - 24] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p0), st.o[o - 24], 0, 0, 0);
-        exp_one(s0, 8 + 2 * (o - 24), p1, o - 24);
-        exp_one(s0, 9 + 2 * (o - 24), p1, o - 24);
+        const int r = 12 + o - 24;
+        exp_one(s0, r, p1, (r & 7) >> 1);
       } else {
         st.o[o - 28] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(p1), st.o[o - 28], 0, 0, 0);
       }
