@@ -610,8 +610,9 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
       total_groups += cl.n_groups;
       // ranges per head: exactly the forced split count, else at most
       // ceil(groups / H) + 1 (a share of at most one head's pages meets at
-      // most two heads); a single range writes bf16 directly
-      if (cl.n_pages > 0 && cl.n_groups != H) {
+      // most two heads); a single range writes bf16 directly, and no head
+      // is split when the group count divides H
+      if (cl.n_pages > 0 && (cl.n_groups > H || H % cl.n_groups != 0)) {
         merge = true;
         max_ranges = std::max<int64_t>(max_ranges, c->opt_video_splits > 0
                                                        ? c->opt_video_splits
