@@ -36,6 +36,8 @@ calls' stream around the kernel itself.
 `video_configs` times the video kernel alone on the v0.1, v0.2 single-unit
 and v0.2 8-unit-history configurations (median of the library's per-launch
 kernel times).
+`v01_step` is the step at the v0.1 stream shape (192x336, 12 heads,
+252-token units, 820 keys), timed the same way.
 `us_per_unit_separate_audio` is the contract step with the audio call in
 its own kernel over all of its pages (WS_OPT_STEP_SEPARATE_AUDIO).
 `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
@@ -436,6 +438,86 @@ def block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev, steps=50, wa
             "append_us": t_app, "video_kernel_us": t_vid, "audio_kernel_us": t_aud, "merge_us": t_merge,
             "audio_rows_in_video_kernel": apath == "audio_riders",
             "attention_share": attn_us / (attn_us + t_qkv + t_out)}
+
+
+def v01_step(ws, torch, dev, steps=200, settle=200):
+    """The v0.1-scale streaming step (192x336: 12 heads, 252-token units, a
+    64-token conditioning slice, a 2-unit history window), timed like the
+    contract step: the slice rewrite, the unit's K/V append and its query
+    preparation in one ws_step_append launch, then ws_unit_attention on the
+    prepared queries (252 queries over 64 + 3 x 252 = 820 keys), commit and
+    eviction; `settle` untimed steps, then `steps` timed ones."""
+    import numpy as np
+    from paper_2607_04443_amd import synth
+    h, grid, cond, hist = 12, (12, 21), 64, 2
+    lu = grid[0] * grid[1]
+    rng = np.random.Generator(np.random.PCG64(synth.SEED_BASE + 5))
+
+    def dev_bf16(shape):
+        return torch.from_numpy(synth.normal_bf16(rng, shape).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    sets = [dict(ck=dev_bf16((cond, h, D)), cv=dev_bf16((cond, h, D)), k=dev_bf16((lu, h, D)),
+                 v=dev_bf16((lu, h, D)), q=dev_bf16((lu, h, D))) for _ in range(2)]
+    n_units = hist + settle + steps + 50 + 2
+    vpos = [torch.from_numpy(synth.video_positions(u, grid)).to(dev) for u in range(n_units)]
+    gamma = torch.ones(D, dtype=torch.float32, device=dev)
+    cache = ws.Cache(h, 2 + (hist + 2) * ((lu + 63) // 64) + 4, max_q_tokens=1024)
+    s0 = sets[0]
+    cache.append(0, ws.WS_KIND_COND, s0["ck"], s0["cv"], ws.WS_APPEND_RAW)
+    for u in range(hist):
+        s = sets[u % 2]
+        cache.append(u, ws.WS_KIND_VIDEO, s["k"], s["v"], ws.WS_APPEND_NORM_ROPE, vpos[u], gamma, 1e-6)
+        cache.commit(u)
+    q_p = torch.empty((lu, h, D), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((lu, h, D), dtype=torch.bfloat16, device=dev)
+
+    stream = torch.cuda.current_stream()
+
+    def step(u):
+        s = sets[u % 2]
+        cache.step_append([
+            dict(unit=0, kind=ws.WS_KIND_COND, k=s["ck"], v=s["cv"], mode=ws.WS_APPEND_RAW),
+            dict(unit=u, kind=ws.WS_KIND_VIDEO, k=s["k"], v=s["v"], mode=ws.WS_APPEND_NORM_ROPE,
+                 positions=vpos[u], gamma=gamma, eps=1e-6)],
+            [dict(q=s["q"], q_out=q_p, positions=vpos[u], gamma=gamma, eps=1e-6)], stream=stream)
+        cache.unit_attention(q_p, out, ws.mask_spec(u, u - hist, (ws.WS_KIND_COND, ws.WS_KIND_VIDEO)),
+                             ws.WS_QUERY_PREPARED, stream=stream)
+        cache.commit(u)
+        cache.evict_before(u - hist + 1)
+
+    u = hist
+    for _ in range(settle):
+        step(u)
+        u += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(u)
+        u += 1
+    enqueued = time.perf_counter() - t0
+    torch.cuda.synchronize()
+    us = (time.perf_counter() - t0) * 1e6 / steps
+    # the GPU's share: a further pass with the library's launch timing on
+    # (append launch, attention kernel, and the time from its end to the
+    # merge's end)
+    cache.timing_enable(3 * 50)
+    for _ in range(50):
+        step(u)
+        u += 1
+    torch.cuda.synchronize()
+    rec = cache.timing_read()
+    cache.close()
+
+    def mean(path, key):
+        v = [r[key] for r in rec if r["path"] == path]
+        return sum(v) / len(v) if v else 0.0
+
+    lk = cond + (hist + 1) * lu
+    flop = 4.0 * h * lu * lk * D
+    return {"heads": h, "queries": lu, "keys": lk, "flop": flop, "us_per_unit": us,
+            "tflops": flop / (us * 1e-6) / 1e12, "host_enqueue_us_per_step": enqueued * 1e6 / steps,
+            "append_us": mean("append", "attn_us"), "video_kernel_us": mean("video", "attn_us"),
+            "video_merge_us": mean("video", "merge_us")}
 
 
 def video_configs(ws, torch, dev, launches=60):
@@ -1033,6 +1115,7 @@ def main():
     catch = catch_up(args, ws, sets, vpos, gamma, eps, stream, dev) if args.long_reps > 0 else None
     block = block_step(args, ws, sets, vpos, apos, gamma, eps, stream, dev) if args.long_reps > 0 else None
     vconf = video_configs(ws, torch, dev) if args.long_reps > 0 else None
+    v01 = v01_step(ws, torch, dev) if args.long_reps > 0 else None
     peaks = measured_peaks(ws, torch, stream, dev) if args.peak_probes else None
 
     t_vkern, t_vmerge = kernel_us("video", "attn_us"), kernel_us("video", "merge_us")
@@ -1072,6 +1155,8 @@ def main():
         "kv_append": {"us": t_append, "gbps": append_bytes / (t_append * 1e-6) / 1e9},
         "long_history": long_hist,
         "video_configs": vconf,
+        # the step at the v0.1 stream shape (192x336), timed like the contract
+        "v01_step": v01,
         "catch_up": catch,
         "block_step": block,
         "roofline": {"bound": "mfma", "kernel": "unit_attn_kernel", "achieved": achieved,
