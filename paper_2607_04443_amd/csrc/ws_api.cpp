@@ -413,13 +413,10 @@ ws_status create_impl(const ws_cache_config* cfg, ws_cache** out) {
 }
 
 // Number of workgroup groups of the video kernel (a group is one workgroup
-// per query tile; together the groups share the (head, page) units evenly).
-// One round of groups fits the CUs when groups * n_qtiles <= CUs.  A group
-// whose share crosses a head boundary pays one more query prologue, pipeline
-// fill and partial write-back, worth about kSegCostPages pages (measured on
-// MI355X: ~15 us against ~1.6 us per page), and every head split into more
-// than one range is merged by the combine kernel.  A forced split count s
-// gives H * s groups: every head in s equal key ranges.
+// per query tile; together the groups share the (head, page) units evenly;
+// one round of groups fits the CUs when groups * n_qtiles <= CUs): the cost
+// model of ws::video_group_count.  A forced split count s gives H * s
+// groups: every head in s equal key ranges.
 // Partition cost of starting a head's segment inside a workgroup's share, in
 // pages: the segment switch (epilogue stores, query load, key-norm bound,
 // pipeline refill) takes about as long as six pages of the main loop.
@@ -428,34 +425,7 @@ constexpr int kVideoSegCostPages = 6;
 int choose_video_groups(const ws_cache* c, int n_heads, int n_qtiles, int n_pages, int n_cus) {
   if (n_pages == 0) return n_heads;
   if (c->opt_video_splits > 0) return n_heads * c->opt_video_splits;
-  // Cost of G groups in pages of one query tile: rounds of the CUs times
-  // (a share's pages plus a fixed cost per segment it holds: prologue, or
-  // switch to the next head), plus the merge launch when a head is split
-  // over groups.  Shares line up with heads when G is a multiple or a
-  // divisor of H (VideoPartition), so that every group holds max(G, H) / G
-  // whole segments; otherwise the G shares cut G + H - 1 segments.
-  constexpr double kSegCostPages = 9.5;
-  constexpr double kMergeCostPages = 4.0;
-  const int64_t H = n_heads;
-  const int64_t units = H * n_pages;
-  const int64_t one_round = std::max<int64_t>(1, n_cus / n_qtiles);
-  // at most kMaxVideoSplits ranges per head: ceil(G / H) + 1 <= kMaxVideoSplits
-  const int64_t g_max = std::min<int64_t>({H * (kMaxVideoSplits - 1), units, 4 * one_round});
-  int64_t best = std::min<int64_t>(H, g_max);
-  double best_cost = -1.0;
-  for (int64_t g = 1; g <= g_max; ++g) {
-    const double rounds = static_cast<double>((g + one_round - 1) / one_round);
-    const bool aligned = g % H == 0 || H % g == 0;
-    const double segs = static_cast<double>(aligned ? std::max(g, H) : g + H - 1) / g;
-    const bool split = g > H || !aligned;
-    const double cost =
-        rounds * (static_cast<double>(units) / g + kSegCostPages * segs) + (split ? kMergeCostPages : 0.0);
-    if (best_cost < 0 || cost < best_cost - 1e-9) {
-      best = g;
-      best_cost = cost;
-    }
-  }
-  return static_cast<int>(best);
+  return static_cast<int>(ws::video_group_count(n_heads, n_qtiles, n_pages, n_cus));
 }
 
 int choose_audio_splits(const ws_cache* c, int n_items, int n_pages) {
@@ -612,7 +582,7 @@ ws_status plan_attention(bool audio, const void* q, int64_t q_tok_stride, int64_
       // ceil(groups / H) + 1 (a share of at most one head's pages meets at
       // most two heads); a single range writes bf16 directly, and no head
       // is split when the group count divides H
-      if (cl.n_pages > 0 && (cl.n_groups > H || H % cl.n_groups != 0)) {
+      if (cl.n_pages > 0 && ws::video_heads_split(H, cl.n_groups)) {
         merge = true;
         max_ranges = std::max<int64_t>(max_ranges, c->opt_video_splits > 0
                                                        ? c->opt_video_splits

@@ -260,6 +260,43 @@ hipError_t static_scratch(void** ptr);
 
 constexpr int kVideoQTile = 256;
 constexpr int kMaxVideoSplits = 8;  // key-range splits of the video kernel
+
+// Whether a partition into `groups` shares splits some head over more than
+// one share (then a merge of the key ranges is needed): no head is split
+// when the group count divides the head count.
+inline bool video_heads_split(int64_t heads, int64_t groups) { return groups > heads || heads % groups != 0; }
+
+// Group count of the video kernel for one query class (host): the G that
+// minimises rounds of the CUs x (a share's pages plus a fixed cost per
+// segment it holds: query prologue, or switch to the next head), plus the
+// merge launch when a head is split.  Shares line up with heads when G is a
+// multiple or a divisor of H, so that every group holds max(G, H) / G whole
+// segments; otherwise the G shares cut G + H - 1 segments.  At most
+// kMaxVideoSplits ranges per head (ceil(G / H) + 1 of them).
+inline int64_t video_group_count(int64_t heads, int64_t qtiles, int64_t pages, int64_t cus) {
+  if (pages == 0) return heads;
+  constexpr double kSegCostPages = 9.5;   // about 15 us against about 1.6 us per page
+  constexpr double kMergeCostPages = 4.0;  // the merge launch and its traffic
+  const int64_t units = heads * pages;
+  const int64_t one_round = cus / qtiles > 1 ? cus / qtiles : 1;
+  int64_t g_max = heads * (kMaxVideoSplits - 1);
+  if (units < g_max) g_max = units;
+  if (4 * one_round < g_max) g_max = 4 * one_round;
+  int64_t best = heads < g_max ? heads : g_max;
+  double best_cost = -1.0;
+  for (int64_t g = 1; g <= g_max; ++g) {
+    const double rounds = static_cast<double>((g + one_round - 1) / one_round);
+    const bool aligned = g % heads == 0 || heads % g == 0;
+    const double segs = static_cast<double>(aligned ? (g > heads ? g : heads) : g + heads - 1) / g;
+    const double cost = rounds * (static_cast<double>(units) / g + kSegCostPages * segs) +
+                        (video_heads_split(heads, g) ? kMergeCostPages : 0.0);
+    if (best_cost < 0 || cost < best_cost - 1e-9) {
+      best = g;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
 constexpr int kVideoWaves = kVideoQTile / 32;
 constexpr int kAudioQTile = 16;
 constexpr int kMaxAudioQ = 64;  // audio queries per call

@@ -84,3 +84,69 @@ def test_partition_lookups_tile_the_units(tmp_path):
     out = subprocess.run([str(exe)], capture_output=True, text=True)
     assert out.returncode == 0, out.stdout + out.stderr
     assert out.stdout.startswith("ok")
+
+
+GROUPS_PROGRAM = r"""
+#include "ws_kernels.hpp"
+#include <cstdio>
+
+int main() {
+  // the shapes the benchmark times: 40 heads x 4 query tiles over 139 pages
+  // (8-unit history), 19 pages (single unit) and 479 pages (32 units); 12
+  // heads x 1 tile over 13 pages (v0.1)
+  struct { long long h, qt, p, want; } pinned[] = {{40, 4, 139, 64}, {40, 4, 19, 40}, {40, 4, 479, 64},
+                                                   {12, 1, 13, 84}};
+  for (auto& c : pinned) {
+    const long long g = ws::video_group_count(c.h, c.qt, c.p, 256);
+    if (g != c.want) { std::printf("FAIL pinned h=%lld p=%lld got %lld\n", c.h, c.p, g); return 1; }
+  }
+  long long n = 0;
+  for (long long h : {1, 3, 8, 12, 40, 64, 80, 160})
+    for (long long qt : {1, 2, 4})
+      for (long long p : {0, 1, 2, 5, 13, 19, 64, 139, 479})
+        for (long long cus : {4, 20, 85, 256}) {
+          const long long g = ws::video_group_count(h, qt, p, cus);
+          if (p == 0) {
+            if (g != h) { std::printf("FAIL empty\n"); return 1; }
+            continue;
+          }
+          if (g < 1 || g > h * p) { std::printf("FAIL range h=%lld p=%lld g=%lld\n", h, p, g); return 1; }
+          // every head meets at most kMaxVideoSplits ranges
+          if ((g + h - 1) / h + 1 > ws::kMaxVideoSplits) { std::printf("FAIL ranges h=%lld g=%lld\n", h, g); return 1; }
+          // a group count that divides the head count splits no head, and the
+          // partition then gives each head to exactly one group
+          if (!ws::video_heads_split(h, g)) {
+            const ws::VideoPartition part{h, p, 6, g};
+            for (long long x = 0; x < h; ++x)
+              if (ws::video_group_of(part, x * p) != ws::video_group_of(part, x * p + p - 1)) {
+                std::printf("FAIL aligned h=%lld p=%lld g=%lld head=%lld\n", h, p, g, x);
+                return 1;
+              }
+          }
+          ++n;
+        }
+  std::printf("ok %lld\n", n);
+  return 0;
+}
+"""
+
+
+def test_group_count_model(tmp_path):
+    """The host's video group count (ws_kernels.hpp: video_group_count): the
+    counts it picks for the benchmark's shapes (one round of 256 workgroups
+    at 8 and 32 history units; one head per group, so no merge, for a single
+    unit; seven key ranges per head at v0.1), and over a grid of shapes: at
+    least one group and at most one per (head, page) unit, at most
+    kMaxVideoSplits ranges per head, and whenever no head is split
+    (video_heads_split false) each head lies in one group's share."""
+    src = tmp_path / "groups.cpp"
+    exe = tmp_path / "groups"
+    src.write_text(GROUPS_PROGRAM)
+    try:
+        subprocess.run(["g++", "-std=c++17", "-O1", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+                        "-I", CSRC, str(src), "-o", str(exe)], check=True, capture_output=True, text=True)
+    except FileNotFoundError:
+        pytest.skip("no host C++ compiler")
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0, out.stdout + out.stderr
+    assert out.stdout.startswith("ok")
